@@ -195,3 +195,14 @@ def check_owner(segs, labels, n_rows):
     ver = np.full(max(len(sg), 1), -99, np.int32)
     st = lib().oracle_check_owner(_buf(sg), len(sg), _buf(lab), n_rows, _buf(ver))
     return st, ver[:len(sg)]
+
+
+def gctr(key, icb, data):
+    """GCTR_K(ICB, X) (SP 800-38D Algorithm 3) -- lets a test check any block
+    of a long message one at a time."""
+    w = key_expansion(key)
+    cb = _u8(icb, 16)
+    x = _u8(data)
+    y = np.zeros(max(x.size, 1), np.uint8)
+    lib().oracle_gctr(_buf(w), _buf(cb), _buf(x) if x.size else None, x.size, _buf(y))
+    return y[:x.size].tobytes()

@@ -1,0 +1,190 @@
+// Device-side building blocks for segmented AES-256-GCM on gfx950:
+// compile-time AES tables, the AES-256 key schedule, a table-free AES block
+// function for setup/finalize work, GF(2^128) arithmetic in GCM bit order,
+// and small wave-level helpers.  The per-block hot loop lives in
+// gift_kernels.hip and uses LDS-resident tables instead.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace gift {
+
+// ---------------------------------------------------------------------------
+// AES constants, generated at compile time from the field definition
+// (FIPS-197 Sec. 4.2 and Sec. 5.1.1): the S-box is the affine image of the
+// multiplicative inverse in GF(2^8) mod x^8+x^4+x^3+x+1.  Here the inverse
+// is a^254 and the affine map is b ^ rotl(b,1) ^ rotl(b,2) ^ rotl(b,3) ^
+// rotl(b,4) ^ 0x63.
+// ---------------------------------------------------------------------------
+constexpr uint8_t xt(uint8_t a) { return (uint8_t)((a << 1) ^ ((a & 0x80) ? 0x1b : 0)); }
+constexpr uint8_t gmul(uint8_t a, uint8_t b) {
+  uint8_t p = 0;
+  for (int i = 0; i < 8; i++) {
+    if (b & 1) p ^= a;
+    a = xt(a);
+    b >>= 1;
+  }
+  return p;
+}
+constexpr uint8_t rotl8(uint8_t b, int s) { return (uint8_t)((b << s) | (b >> (8 - s))); }
+constexpr uint8_t ginv(uint8_t a) {
+  // a^254 = a^-1 for a != 0 (the multiplicative group has order 255); 0 -> 0
+  uint8_t r = 1, base = a;
+  int e = 254;
+  while (e) {
+    if (e & 1) r = gmul(r, base);
+    base = gmul(base, base);
+    e >>= 1;
+  }
+  return a ? r : 0;
+}
+constexpr uint8_t sbox_of(uint8_t a) {
+  uint8_t b = ginv(a);
+  return (uint8_t)(b ^ rotl8(b, 1) ^ rotl8(b, 2) ^ rotl8(b, 3) ^ rotl8(b, 4) ^ 0x63);
+}
+
+struct AesConst {
+  uint8_t sbox[256];
+  // Te0[x]: the MixColumns image of S(x) placed in row 0, as a little-endian
+  // column word: bytes (2S, S, S, 3S).  Rows 1..3 are byte rotations.
+  uint32_t te0[256];
+};
+
+constexpr AesConst make_aes_const() {
+  AesConst c{};
+  for (int x = 0; x < 256; x++) {
+    uint8_t s = sbox_of((uint8_t)x);
+    c.sbox[x] = s;
+    c.te0[x] = (uint32_t)gmul(s, 2) | ((uint32_t)s << 8) | ((uint32_t)s << 16) | ((uint32_t)gmul(s, 3) << 24);
+  }
+  return c;
+}
+
+__device__ __forceinline__ uint32_t rotl32(uint32_t x, int s) { return (x << s) | (x >> ((32 - s) & 31)); }
+__device__ __forceinline__ uint32_t bswap32(uint32_t x) { return __builtin_bswap32(x); }
+__device__ __forceinline__ uint32_t xor3(uint32_t a, uint32_t b, uint32_t c) {
+  return __builtin_amdgcn_bitop3_b32(a, b, c, 0x96);
+}
+
+// ---------------------------------------------------------------------------
+// AES-256 key schedule (FIPS-197 Sec. 5.2, Nk = 8, Nr = 14).  Words are
+// little-endian u32 of the schedule bytes, so word c of round r XORs
+// directly into state column c.
+// ---------------------------------------------------------------------------
+__device__ inline void aes256_key_schedule(const uint8_t* __restrict__ key, uint32_t rk[60],
+                                           const AesConst& C) {
+  for (int i = 0; i < 8; i++)
+    rk[i] = (uint32_t)key[4 * i] | ((uint32_t)key[4 * i + 1] << 8) | ((uint32_t)key[4 * i + 2] << 16) |
+            ((uint32_t)key[4 * i + 3] << 24);
+  uint8_t rc = 1;
+  for (int i = 8; i < 60; i++) {
+    uint32_t t = rk[i - 1];
+    if ((i & 7) == 0 || (i & 7) == 4) {
+      if ((i & 7) == 0) t = (t >> 8) | (t << 24);  // RotWord on LE bytes
+      t = (uint32_t)C.sbox[t & 0xff] | ((uint32_t)C.sbox[(t >> 8) & 0xff] << 8) |
+          ((uint32_t)C.sbox[(t >> 16) & 0xff] << 16) | ((uint32_t)C.sbox[t >> 24] << 24);
+      if ((i & 7) == 0) {
+        t ^= rc;
+        rc = xt(rc);
+      }
+    }
+    rk[i] = rk[i - 8] ^ t;
+  }
+}
+
+// One AES-256 block from tables in global/constant memory.  Used only where
+// a few blocks per segment are needed (E_K(J0), H, small segments).
+// State words are columns (little-endian), as above.
+__device__ inline void aes256_encrypt_words(const uint32_t* __restrict__ rk, const uint32_t in[4], uint32_t out[4],
+                                            const AesConst& C) {
+  uint32_t s0 = in[0] ^ rk[0], s1 = in[1] ^ rk[1], s2 = in[2] ^ rk[2], s3 = in[3] ^ rk[3];
+#define GIFT_TE(w, k) rotl32(C.te0[((w) >> (8 * (k))) & 0xff], 8 * (k))
+  for (int r = 1; r < 14; r++) {
+    uint32_t t0 = GIFT_TE(s0, 0) ^ GIFT_TE(s1, 1) ^ GIFT_TE(s2, 2) ^ GIFT_TE(s3, 3) ^ rk[4 * r + 0];
+    uint32_t t1 = GIFT_TE(s1, 0) ^ GIFT_TE(s2, 1) ^ GIFT_TE(s3, 2) ^ GIFT_TE(s0, 3) ^ rk[4 * r + 1];
+    uint32_t t2 = GIFT_TE(s2, 0) ^ GIFT_TE(s3, 1) ^ GIFT_TE(s0, 2) ^ GIFT_TE(s1, 3) ^ rk[4 * r + 2];
+    uint32_t t3 = GIFT_TE(s3, 0) ^ GIFT_TE(s0, 1) ^ GIFT_TE(s1, 2) ^ GIFT_TE(s2, 3) ^ rk[4 * r + 3];
+    s0 = t0;
+    s1 = t1;
+    s2 = t2;
+    s3 = t3;
+  }
+#undef GIFT_TE
+#define GIFT_SB(w, k) ((uint32_t)C.sbox[((w) >> (8 * (k))) & 0xff] << (8 * (k)))
+  out[0] = (GIFT_SB(s0, 0) | GIFT_SB(s1, 1) | GIFT_SB(s2, 2) | GIFT_SB(s3, 3)) ^ rk[56];
+  out[1] = (GIFT_SB(s1, 0) | GIFT_SB(s2, 1) | GIFT_SB(s3, 2) | GIFT_SB(s0, 3)) ^ rk[57];
+  out[2] = (GIFT_SB(s2, 0) | GIFT_SB(s3, 1) | GIFT_SB(s0, 2) | GIFT_SB(s1, 3)) ^ rk[58];
+  out[3] = (GIFT_SB(s3, 0) | GIFT_SB(s0, 1) | GIFT_SB(s1, 2) | GIFT_SB(s2, 3)) ^ rk[59];
+#undef GIFT_SB
+}
+
+// ---------------------------------------------------------------------------
+// GF(2^128) in GCM bit order (SP 800-38D Sec. 6.3): a block is 16 bytes,
+// bit 0 = MSB of byte 0 = coefficient of x^0.  In registers a block is four
+// little-endian words w[0..3] (bytes 0..15 in memory order).
+// ---------------------------------------------------------------------------
+struct u128 {
+  uint32_t w[4];
+};
+
+__device__ __forceinline__ u128 u128_zero() { return u128{{0u, 0u, 0u, 0u}}; }
+__device__ __forceinline__ u128 u128_xor(const u128& a, const u128& b) {
+  return u128{{a.w[0] ^ b.w[0], a.w[1] ^ b.w[1], a.w[2] ^ b.w[2], a.w[3] ^ b.w[3]}};
+}
+
+// General product of two field elements: shift-and-add over the bits of x,
+// with y multiplied by x each step (V -> V >> 1, xor R = 0xE1 || 0^120 on
+// carry).  Computed on big-endian words so that "rightshift of the bit
+// string" is a plain 128-bit right shift.  ~1.4k VALU ops; used only outside
+// the per-block loop.
+__device__ inline u128 gf_mul(const u128& x, const u128& y) {
+  uint32_t v0 = bswap32(y.w[0]), v1 = bswap32(y.w[1]), v2 = bswap32(y.w[2]), v3 = bswap32(y.w[3]);
+  uint32_t z0 = 0, z1 = 0, z2 = 0, z3 = 0;
+#pragma unroll
+  for (int j = 0; j < 4; j++) {
+    uint32_t xw = bswap32(x.w[j]);
+#pragma unroll 8
+    for (int b = 31; b >= 0; b--) {
+      uint32_t m = 0u - ((xw >> b) & 1u);
+      z0 ^= v0 & m;
+      z1 ^= v1 & m;
+      z2 ^= v2 & m;
+      z3 ^= v3 & m;
+      uint32_t carry = 0u - (v3 & 1u);
+      v3 = __builtin_amdgcn_alignbit(v2, v3, 1);
+      v2 = __builtin_amdgcn_alignbit(v1, v2, 1);
+      v1 = __builtin_amdgcn_alignbit(v0, v1, 1);
+      v0 = (v0 >> 1) ^ (0xE1000000u & carry);
+    }
+  }
+  return u128{{bswap32(z0), bswap32(z1), bswap32(z2), bswap32(z3)}};
+}
+
+// The element x^p (only bit p set).
+__device__ inline u128 gf_xpow_elem(int p) {
+  u128 r = u128_zero();
+  int byte = p >> 3, bit = 7 - (p & 7);
+  r.w[byte >> 2] = (uint32_t)(1u << bit) << (8 * (byte & 3));
+  return r;
+}
+
+// h^e by square-and-multiply.
+__device__ inline u128 gf_pow(const u128& h, uint64_t e) {
+  u128 r = gf_xpow_elem(0);  // multiplicative identity
+  u128 b = h;
+  while (e) {
+    if (e & 1) r = gf_mul(r, b);
+    e >>= 1;
+    if (e) b = gf_mul(b, b);
+  }
+  return r;
+}
+
+__device__ __forceinline__ uint32_t wave_xor(uint32_t v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v ^= __shfl_xor(v, o, 64);
+  return v;
+}
+
+}  // namespace gift

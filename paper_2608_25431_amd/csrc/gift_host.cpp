@@ -1,0 +1,517 @@
+// Host runtime of the C ABI in include/gift.h: argument validation, IV
+// derivation, segment descriptors, pinned staging, stream-ordered scratch
+// and kernel launches.  Every data-dependent step runs in the kernels of
+// gift_kernels.hip; this file only decides what to launch.
+#include <hip/hip_runtime.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+#include <mutex>
+#include <string>
+#include <utility>
+#include <vector>
+
+#include "gift.h"
+#include "gift_internal.hpp"
+
+using namespace gift;
+
+struct gift_key_table_s {
+  int device;
+  uint32_t n_users;
+  void* mem;
+  size_t bytes;
+  KeyTableDev dev;
+};
+
+namespace {
+
+thread_local std::string g_last_error;
+thread_local hipEvent_t g_prof_before = nullptr, g_prof_after = nullptr;
+
+gift_status fail(gift_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return s;
+}
+
+gift_status hip_fail(hipError_t e, const char* what) {
+  return fail(e == hipErrorOutOfMemory ? GIFT_E_NOMEM : GIFT_E_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+constexpr uint64_t kMaxSegBytes = ((1ull << 32) - 2) * 16ull;  // SP 800-38D Sec. 5.2.1.1
+constexpr int kMaxDevices = 64;
+
+int device_cus(int dev) {
+  static std::mutex mu;
+  static int cus[kMaxDevices] = {0};
+  std::lock_guard<std::mutex> g(mu);
+  if (dev < 0 || dev >= kMaxDevices) return 256;
+  if (cus[dev] == 0) {
+    int v = 0;
+    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0) v = 256;
+    cus[dev] = v;
+  }
+  return cus[dev];
+}
+
+// Pinned host staging ring per device: descriptors are copied here and
+// uploaded with one async copy; a slot is reused only after the event
+// recorded behind its copy has completed.
+class Staging {
+ public:
+  hipError_t upload(void* dst, const void* src, size_t bytes, hipStream_t s) {
+    std::lock_guard<std::mutex> g(mu_);
+    if (bytes == 0) return hipSuccess;
+    if (bytes > kCap / 2) {  // rare: very large tables take a private synchronous path
+      void* tmp = nullptr;
+      hipError_t e = hipHostMalloc(&tmp, bytes, hipHostMallocDefault);
+      if (e != hipSuccess) return e;
+      memcpy(tmp, src, bytes);
+      e = hipMemcpyAsync(dst, tmp, bytes, hipMemcpyHostToDevice, s);
+      hipError_t e2 = hipStreamSynchronize(s);
+      (void)hipHostFree(tmp);
+      return e != hipSuccess ? e : e2;
+    }
+    if (base_ == nullptr) {
+      hipError_t e = hipHostMalloc((void**)&base_, kCap, hipHostMallocDefault);
+      if (e != hipSuccess) {
+        base_ = nullptr;
+        return e;
+      }
+    }
+    size_t need = (bytes + 255) & ~(size_t)255;
+    if (head_ + need > kCap) head_ = 0;
+    // retire completed slots; wait for any slot overlapping [head_, head_+need)
+    for (size_t i = 0; i < live_.size();) {
+      Slot& sl = live_[i];
+      bool overlap = sl.off < head_ + need && head_ < sl.off + sl.len;
+      bool done = hipEventQuery(sl.ev) == hipSuccess;
+      if (overlap && !done) {
+        hipError_t e = hipEventSynchronize(sl.ev);
+        if (e != hipSuccess) return e;
+        done = true;
+      }
+      if (done) {
+        free_ev_.push_back(sl.ev);
+        live_[i] = live_.back();
+        live_.pop_back();
+      } else {
+        i++;
+      }
+    }
+    memcpy(base_ + head_, src, bytes);
+    hipError_t e = hipMemcpyAsync(dst, base_ + head_, bytes, hipMemcpyHostToDevice, s);
+    if (e != hipSuccess) return e;
+    hipEvent_t ev;
+    if (!free_ev_.empty()) {
+      ev = free_ev_.back();
+      free_ev_.pop_back();
+    } else {
+      e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
+      if (e != hipSuccess) {
+        (void)hipStreamSynchronize(s);
+        return e;
+      }
+    }
+    e = hipEventRecord(ev, s);
+    if (e != hipSuccess) {
+      (void)hipStreamSynchronize(s);
+      free_ev_.push_back(ev);
+      return e;
+    }
+    live_.push_back(Slot{head_, need, ev});
+    head_ += need;
+    return hipSuccess;
+  }
+
+ private:
+  static constexpr size_t kCap = 8u << 20;
+  struct Slot {
+    size_t off, len;
+    hipEvent_t ev;
+  };
+  std::mutex mu_;
+  uint8_t* base_ = nullptr;
+  size_t head_ = 0;
+  std::vector<Slot> live_;
+  std::vector<hipEvent_t> free_ev_;
+};
+
+Staging* staging_for(int dev) {
+  static Staging st[kMaxDevices];
+  return (dev >= 0 && dev < kMaxDevices) ? &st[dev] : nullptr;
+}
+
+inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+struct Plan {
+  std::vector<SegDesc> descs;
+  std::vector<ZeroRange> zr;
+  uint32_t n_tiles = 0;
+  uint32_t n_small = 0;
+};
+
+// Checks segments in caller order (INVALID, RANGE, TOO_LARGE), then overlap,
+// then (user, iv_seq) reuse.  With keys == false (owner check) users are not
+// range-checked, the GCM length limit does not apply and iv_seq is unused.
+gift_status check_segments(const gift_segment* segs, uint32_t n, uint64_t n_rows, uint64_t row_bytes,
+                           uint32_t n_users, bool keys) {
+  for (uint32_t i = 0; i < n; i++) {
+    const gift_segment& s = segs[i];
+    if (s.row_count == 0 || s.reserved != 0)
+      return fail(GIFT_E_INVALID, "segment %u: row_count must be >= 1 and reserved 0", i);
+    if (s.user == GIFT_LABEL_PARAM || s.user == GIFT_LABEL_UNOWNED)
+      return fail(GIFT_E_INVALID, "segment %u: user id is a label sentinel", i);
+    if (s.row_begin > n_rows || s.row_count > n_rows - s.row_begin)
+      return fail(GIFT_E_RANGE, "segment %u: rows [%llu, +%llu) exceed n_rows %llu", i,
+                  (unsigned long long)s.row_begin, (unsigned long long)s.row_count, (unsigned long long)n_rows);
+    if (keys && s.user >= n_users)
+      return fail(GIFT_E_RANGE, "segment %u: user %u >= n_users %u", i, s.user, n_users);
+    if (keys && s.row_count > kMaxSegBytes / row_bytes)
+      return fail(GIFT_E_TOO_LARGE, "segment %u: longer than (2^32-2)*16 bytes", i);
+  }
+  if (n > 1) {
+    std::vector<std::pair<uint64_t, uint64_t>> v(n);
+    for (uint32_t i = 0; i < n; i++) v[i] = {segs[i].row_begin, segs[i].row_count};
+    std::sort(v.begin(), v.end());
+    for (uint32_t i = 1; i < n; i++)
+      if (v[i].first < v[i - 1].first + v[i - 1].second)
+        return fail(GIFT_E_OVERLAP, "segments overlap at row %llu", (unsigned long long)v[i].first);
+    if (keys) {
+      for (uint32_t i = 0; i < n; i++) v[i] = {segs[i].user, segs[i].iv_seq};
+      std::sort(v.begin(), v.end());
+      for (uint32_t i = 1; i < n; i++)
+        if (v[i] == v[i - 1])
+          return fail(GIFT_E_NONCE_REUSE, "two segments share user %llu and iv_seq %llu",
+                      (unsigned long long)v[i].first, (unsigned long long)v[i].second);
+    }
+  }
+  return GIFT_OK;
+}
+
+// Descriptors, zero ranges (uncovered rows; for open also every tiled
+// segment, zeroed only when its verdict is not OK) and work counts.
+void build_plan(const gift_segment* segs, uint32_t n, uint64_t n_rows, uint64_t row_bytes, const uint8_t* nonce_base,
+                const void* in, const void* out, bool open, Plan& P) {
+  P.descs.resize(n);
+  std::vector<std::pair<uint64_t, uint64_t>> cover(n);
+  for (uint32_t i = 0; i < n; i++) {
+    const gift_segment& s = segs[i];
+    SegDesc& d = P.descs[i];
+    memset(&d, 0, sizeof d);
+    d.byte_off = s.row_begin * row_bytes;
+    d.len = s.row_count * row_bytes;
+    d.row_begin = s.row_begin;
+    d.row_count = s.row_count;
+    d.user = s.user;
+    const uint64_t nb = (d.len + 15) / 16;
+    d.nblocks = (uint32_t)nb;
+    if (nonce_base) {
+      uint8_t iv[12];
+      memcpy(iv, nonce_base + 12ull * s.user, 12);
+      for (int k = 0; k < 8; k++) iv[11 - k] ^= (uint8_t)(s.iv_seq >> (8 * k));
+      for (int w = 0; w < 3; w++)
+        d.iv[w] = (uint32_t)iv[4 * w] | ((uint32_t)iv[4 * w + 1] << 8) | ((uint32_t)iv[4 * w + 2] << 16) |
+                  ((uint32_t)iv[4 * w + 3] << 24);
+    }
+    const bool aligned = ((((uintptr_t)in + d.byte_off) | ((uintptr_t)out + d.byte_off)) & 15u) == 0;
+    const bool small = nb <= kSmallMaxBlocks;
+    d.flags = (aligned ? kSegAligned : 0u) | (small ? kSegSmall : 0u);
+    if (small)
+      P.n_small++;
+    else
+      P.n_tiles += (uint32_t)((nb + kTileBlocks - 1) / kTileBlocks);
+    cover[i] = {s.row_begin, s.row_count};
+  }
+  std::sort(cover.begin(), cover.end());
+  uint64_t cur = 0;
+  for (auto& c : cover) {
+    if (c.first > cur) P.zr.push_back(ZeroRange{cur * row_bytes, (c.first - cur) * row_bytes, -1, {0, 0, 0}});
+    cur = c.first + c.second;
+  }
+  if (cur < n_rows) P.zr.push_back(ZeroRange{cur * row_bytes, (n_rows - cur) * row_bytes, -1, {0, 0, 0}});
+  if (open)
+    for (uint32_t i = 0; i < n; i++)
+      if (!(P.descs[i].flags & kSegSmall))
+        P.zr.push_back(ZeroRange{P.descs[i].byte_off, P.descs[i].len, (int32_t)i, {0, 0, 0}});
+}
+
+gift_status current_device(int* dev) {
+  hipError_t e = hipGetDevice(dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  return GIFT_OK;
+}
+
+template <bool OPEN>
+gift_status run_gcm(const gift_tensor* t, const gift_segment_table* st, gift_key_table kt, const uint8_t* nonce_base,
+                    void* out, uint8_t* tags_out, const uint8_t* tags_in, hipStream_t stream) {
+  g_last_error.clear();
+  if (!t || !st || !kt) return fail(GIFT_E_INVALID, "null tensor, segment table or key table");
+  const uint32_t n = st->n_segs;
+  if (t->n_rows > 0 && (!t->data || !out)) return fail(GIFT_E_INVALID, "null data or out");
+  if (n > 0 && (!st->segs || !nonce_base || (OPEN ? !tags_in : !tags_out)))
+    return fail(GIFT_E_INVALID, "null segs, nonce_base or tags");
+  if (OPEN && n > 0 && !st->verdicts) return fail(GIFT_E_INVALID, "gift_open needs st->verdicts");
+  if (t->row_bytes == 0) return fail(GIFT_E_INVALID, "row_bytes must be >= 1");
+  if (t->n_rows > UINT64_MAX / t->row_bytes) return fail(GIFT_E_INVALID, "tensor size overflows");
+  const uint64_t total = t->n_rows * t->row_bytes;
+  if (out != t->data && total > 0) {
+    const uintptr_t a = (uintptr_t)t->data, b = (uintptr_t)out;
+    if (a < b + total && b < a + total) return fail(GIFT_E_INVALID, "out partially overlaps data");
+  }
+  gift_status sv = check_segments(st->segs, n, t->n_rows, t->row_bytes, kt->n_users, true);
+  if (sv != GIFT_OK) return sv;
+  if (total == 0) return GIFT_OK;
+
+  // the profiling hook applies to this call only
+  hipEvent_t prof_before = g_prof_before, prof_after = g_prof_after;
+  g_prof_before = g_prof_after = nullptr;
+  int dev;
+  if ((sv = current_device(&dev)) != GIFT_OK) return sv;
+  if (dev != kt->device) return fail(GIFT_E_INVALID, "key table belongs to device %d, current is %d", kt->device, dev);
+
+  Plan P;
+  build_plan(st->segs, n, t->n_rows, t->row_bytes, nonce_base, t->data, out, OPEN, P);
+
+  // scratch: descs | zero ranges | tile_base | small_list | partials | verdicts
+  const size_t o_desc = 0;
+  const size_t o_zr = o_desc + align256(sizeof(SegDesc) * n);
+  const size_t o_tb = o_zr + align256(sizeof(ZeroRange) * P.zr.size());
+  const size_t o_sl = o_tb + align256(4ull * (n + 1));
+  const size_t o_pt = o_sl + align256(4ull * (n ? n : 1));
+  const size_t o_vd = o_pt + align256(16ull * (P.n_tiles ? P.n_tiles : 1));
+  const size_t bytes = o_vd + align256(4ull * (n ? n : 1));
+  uint8_t* scratch = nullptr;
+  hipError_t e = hipMallocAsync((void**)&scratch, bytes, stream);
+  if (e != hipSuccess) return hip_fail(e, "hipMallocAsync(scratch)");
+
+  std::vector<uint8_t> host(o_tb);
+  if (n) memcpy(host.data() + o_desc, P.descs.data(), sizeof(SegDesc) * n);
+  if (!P.zr.empty()) memcpy(host.data() + o_zr, P.zr.data(), sizeof(ZeroRange) * P.zr.size());
+  Staging* sg = staging_for(dev);
+  if (!sg) {
+    (void)hipFreeAsync(scratch, stream);
+    return fail(GIFT_E_INVALID, "device index %d unsupported", dev);
+  }
+  e = sg->upload(scratch, host.data(), o_tb, stream);
+  if (e != hipSuccess) {
+    (void)hipFreeAsync(scratch, stream);
+    return hip_fail(e, "staging upload");
+  }
+
+  const SegDesc* d_desc = (const SegDesc*)(scratch + o_desc);
+  int32_t* verdicts = st->verdicts ? st->verdicts : (int32_t*)(scratch + o_vd);
+  gift_status rs = GIFT_OK;
+  do {
+    if (n > 0) {
+      if (st->row_labels) {
+        e = launch_check_owner(d_desc, n, st->row_labels, verdicts, stream);
+        if (e != hipSuccess) {
+          rs = hip_fail(e, "check_owner launch");
+          break;
+        }
+      }
+      e = launch_expand(d_desc, n, (uint32_t*)(scratch + o_tb), (uint32_t*)(scratch + o_sl), verdicts,
+                        st->row_labels == nullptr, stream);
+      if (e != hipSuccess) {
+        rs = hip_fail(e, "expand launch");
+        break;
+      }
+      GcmArgs a;
+      a.in = (const uint8_t*)t->data;
+      a.out = (uint8_t*)out;
+      a.segs = d_desc;
+      a.n_segs = n;
+      a.tile_base = (const uint32_t*)(scratch + o_tb);
+      a.small_list = (const uint32_t*)(scratch + o_sl);
+      a.n_tiles = P.n_tiles;
+      a.n_small = P.n_small;
+      a.partials = (uint4*)(scratch + o_pt);
+      a.verdicts = verdicts;
+      a.tags_out = tags_out;
+      a.tags_in = tags_in;
+      a.kt = kt->dev;
+      if (prof_before && P.n_tiles > 0) {
+        e = hipEventRecord(prof_before, stream);
+        if (e != hipSuccess) {
+          rs = hip_fail(e, "profiling event");
+          break;
+        }
+      }
+      e = launch_gcm_tiles(a, OPEN, (uint32_t)device_cus(dev), stream);
+      if (e != hipSuccess) {
+        rs = hip_fail(e, "gcm launch");
+        break;
+      }
+      if (prof_after && P.n_tiles > 0) {
+        e = hipEventRecord(prof_after, stream);
+        if (e != hipSuccess) {
+          rs = hip_fail(e, "profiling event");
+          break;
+        }
+      }
+      e = launch_gcm_small(a, OPEN, stream);
+      if (e == hipSuccess) e = launch_gcm_finalize(a, OPEN, stream);
+      if (e != hipSuccess) {
+        rs = hip_fail(e, "gcm launch");
+        break;
+      }
+    }
+    if (!P.zr.empty()) {
+      e = launch_zero_ranges((uint8_t*)out, (const ZeroRange*)(scratch + o_zr), (uint32_t)P.zr.size(), verdicts,
+                             (uint32_t)device_cus(dev) * 4u, stream);
+      if (e != hipSuccess) {
+        rs = hip_fail(e, "zero-fill launch");
+        break;
+      }
+    }
+  } while (0);
+  e = hipFreeAsync(scratch, stream);
+  if (rs == GIFT_OK && e != hipSuccess) rs = hip_fail(e, "hipFreeAsync(scratch)");
+  return rs;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* gift_status_string(gift_status s) {
+  switch (s) {
+    case GIFT_OK: return "ok";
+    case GIFT_E_INVALID: return "invalid argument";
+    case GIFT_E_RANGE: return "segment or user out of range";
+    case GIFT_E_OVERLAP: return "segments overlap";
+    case GIFT_E_NONCE_REUSE: return "(user, iv_seq) reused within the call";
+    case GIFT_E_TOO_LARGE: return "segment exceeds the GCM length limit";
+    case GIFT_E_HIP: return "HIP runtime error";
+    case GIFT_E_NOMEM: return "out of memory";
+  }
+  return "unknown status";
+}
+
+const char* gift_last_error(void) { return g_last_error.c_str(); }
+
+uint32_t gift_key_table_users(gift_key_table kt) { return kt ? kt->n_users : 0u; }
+
+gift_status gift_profile_next_call(hipEvent_t before, hipEvent_t after) {
+  if ((before == nullptr) != (after == nullptr)) return fail(GIFT_E_INVALID, "pass both events or neither");
+  g_prof_before = before;
+  g_prof_after = after;
+  return GIFT_OK;
+}
+
+gift_status gift_key_table_create(const uint8_t* keys, uint32_t n_users, hipStream_t stream, gift_key_table* out) {
+  g_last_error.clear();
+  if (!keys || !out) return fail(GIFT_E_INVALID, "null keys or out");
+  if (n_users == 0 || n_users >= GIFT_LABEL_PARAM) return fail(GIFT_E_INVALID, "n_users out of range");
+  *out = nullptr;
+  int dev;
+  gift_status sv = current_device(&dev);
+  if (sv != GIFT_OK) return sv;
+  const uint64_t u = n_users;
+  const size_t o_rk = 0;
+  const size_t o_h = o_rk + align256(u * 64 * 4);
+  const size_t o_gt = o_h + align256(u * 16);
+  const size_t o_ph = o_gt + align256(u * 512 * 16);
+  const size_t o_pt = o_ph + align256(u * kHPowers * 16);
+  const size_t o_pl = o_pt + align256(u * kFinLanes * 16);
+  const size_t bytes = o_pl + align256(u * 16);
+  uint8_t* mem = nullptr;
+  hipError_t e = hipMalloc((void**)&mem, bytes);
+  if (e != hipSuccess) return hip_fail(e, "hipMalloc(key table)");
+  uint8_t* kdev = nullptr;
+  e = hipMalloc((void**)&kdev, 32ull * u);
+  if (e != hipSuccess) {
+    (void)hipFree(mem);
+    return hip_fail(e, "hipMalloc(keys)");
+  }
+  gift_key_table kt = new gift_key_table_s;
+  kt->device = dev;
+  kt->n_users = n_users;
+  kt->mem = mem;
+  kt->bytes = bytes;
+  kt->dev.rk = (uint32_t*)(mem + o_rk);
+  kt->dev.h = (uint32_t*)(mem + o_h);
+  kt->dev.gtab = (uint4*)(mem + o_gt);
+  kt->dev.pow_h = (uint4*)(mem + o_ph);
+  kt->dev.pow_ht = (uint4*)(mem + o_pt);
+  kt->dev.pow_hlt = (uint4*)(mem + o_pl);
+  kt->dev.n_users = n_users;
+  // The copy reads the caller's buffer; synchronising before return means no
+  // copy of the keys outlives the call on the host side of the library.
+  e = hipMemcpyAsync(kdev, keys, 32ull * u, hipMemcpyHostToDevice, stream);
+  if (e == hipSuccess) e = launch_key_setup(kdev, kt->dev, stream);
+  if (e == hipSuccess) e = launch_wipe(kdev, 32ull * u, stream);
+  hipError_t e2 = hipStreamSynchronize(stream);
+  (void)hipFree(kdev);
+  if (e == hipSuccess) e = e2;
+  if (e != hipSuccess) {
+    (void)hipFree(mem);
+    delete kt;
+    return hip_fail(e, "key table setup");
+  }
+  *out = kt;
+  return GIFT_OK;
+}
+
+gift_status gift_key_table_destroy(gift_key_table kt) {
+  g_last_error.clear();
+  if (!kt) return GIFT_OK;
+  int prev = -1;
+  (void)hipGetDevice(&prev);
+  hipError_t e = hipSetDevice(kt->device);
+  if (e == hipSuccess) e = hipDeviceSynchronize();
+  if (e == hipSuccess) e = hipMemset(kt->mem, 0, kt->bytes);
+  if (e == hipSuccess) e = hipDeviceSynchronize();
+  hipError_t e2 = hipFree(kt->mem);
+  if (prev >= 0) (void)hipSetDevice(prev);
+  delete kt;
+  if (e != hipSuccess) return hip_fail(e, "key table wipe");
+  if (e2 != hipSuccess) return hip_fail(e2, "key table free");
+  return GIFT_OK;
+}
+
+gift_status gift_seal(const gift_tensor* t, const gift_segment_table* st, gift_key_table kt, const uint8_t* nonce_base,
+                      void* out, uint8_t* tags, hipStream_t stream) {
+  return run_gcm<false>(t, st, kt, nonce_base, out, tags, nullptr, stream);
+}
+
+gift_status gift_open(const gift_tensor* t, const gift_segment_table* st, gift_key_table kt, const uint8_t* nonce_base,
+                      void* out, const uint8_t* tags, hipStream_t stream) {
+  return run_gcm<true>(t, st, kt, nonce_base, out, nullptr, tags, stream);
+}
+
+gift_status gift_check_owner(const gift_segment_table* st, const uint32_t* labels, uint64_t n_rows,
+                             hipStream_t stream) {
+  g_last_error.clear();
+  if (!st || !labels) return fail(GIFT_E_INVALID, "null segment table or labels");
+  const uint32_t n = st->n_segs;
+  if (n > 0 && (!st->segs || !st->verdicts)) return fail(GIFT_E_INVALID, "null segs or verdicts");
+  gift_status sv = check_segments(st->segs, n, n_rows, 1, 0, false);
+  if (sv != GIFT_OK) return sv;
+  if (n == 0) return GIFT_OK;
+  int dev;
+  if ((sv = current_device(&dev)) != GIFT_OK) return sv;
+  Plan P;
+  build_plan(st->segs, n, n_rows, 1, nullptr, nullptr, nullptr, false, P);
+  SegDesc* d = nullptr;
+  const size_t bytes = sizeof(SegDesc) * n;
+  hipError_t e = hipMallocAsync((void**)&d, bytes, stream);
+  if (e != hipSuccess) return hip_fail(e, "hipMallocAsync(descs)");
+  Staging* sg = staging_for(dev);
+  e = sg ? sg->upload(d, P.descs.data(), bytes, stream) : hipErrorInvalidDevice;
+  if (e == hipSuccess) e = launch_check_owner(d, n, labels, st->verdicts, stream);
+  hipError_t e2 = hipFreeAsync(d, stream);
+  if (e != hipSuccess) return hip_fail(e, "check_owner");
+  if (e2 != hipSuccess) return hip_fail(e2, "hipFreeAsync(descs)");
+  return GIFT_OK;
+}
+
+}  // extern "C"

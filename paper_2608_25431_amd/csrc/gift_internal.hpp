@@ -1,0 +1,85 @@
+// Types shared by the host runtime (gift_host.cpp) and the kernels
+// (gift_kernels.hip).  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace gift {
+
+// Work decomposition of the per-block kernel.
+constexpr int kThreads = 1024;                             // one workgroup per CU (LDS-bound)
+constexpr int kRows = 128;                                 // 1024-block rows per tile
+constexpr uint32_t kTileBlocks = (uint32_t)kThreads * kRows;  // 131072 blocks = 2 MiB per tile
+constexpr uint32_t kSmallMaxBlocks = 64;                   // segments up to 1 KiB: one wave each
+constexpr int kHPowers = kThreads;                         // H^0 .. H^(kThreads-1) per user
+constexpr int kFinLanes = 64;                              // lanes of the per-segment finalize
+
+enum : uint32_t { kSegAligned = 1u, kSegSmall = 2u };
+
+// Device descriptor of one segment (64 B), built on the host.
+struct SegDesc {
+  uint64_t byte_off;   // first byte of the segment in the tensor
+  uint64_t len;        // bytes (>= 1)
+  uint64_t row_begin;  // rows, for the owner check
+  uint64_t row_count;
+  uint32_t iv[3];      // IV as little-endian words of its 12 bytes
+  uint32_t user;
+  uint32_t nblocks;    // ceil(len / 16), <= 2^32 - 2
+  uint32_t flags;      // kSegAligned | kSegSmall
+  uint32_t pad[2];
+};
+static_assert(sizeof(SegDesc) == 64, "SegDesc layout");
+
+// A byte range of `out` to zero: always (seg < 0) or when the verdict of
+// segment `seg` is not OK.
+struct ZeroRange {
+  uint64_t off;
+  uint64_t len;
+  int32_t seg;
+  uint32_t pad[3];
+};
+static_assert(sizeof(ZeroRange) == 32, "ZeroRange layout");
+
+// Per-user key material in device memory, one allocation.
+struct KeyTableDev {
+  uint32_t* rk;      // [n_users][64] round-key words (60 used)
+  uint32_t* h;       // [n_users][4]  H = E_K(0^128)
+  uint4* gtab;       // [n_users][32][16] 4-bit GHASH tables of M = H^kThreads
+  uint4* pow_h;      // [n_users][kHPowers] H^k
+  uint4* pow_ht;     // [n_users][kFinLanes] H^(k * kTileBlocks)
+  uint4* pow_hlt;    // [n_users] H^(kFinLanes * kTileBlocks)
+  uint32_t n_users;
+};
+
+struct GcmArgs {
+  const uint8_t* in;
+  uint8_t* out;
+  const SegDesc* segs;
+  uint32_t n_segs;
+  const uint32_t* tile_base;   // [n_segs + 1] first tile of each segment (small ones: 0 tiles)
+  const uint32_t* small_list;  // [n_small] indices of small segments
+  uint32_t n_tiles;
+  uint32_t n_small;
+  uint4* partials;             // [n_tiles] GHASH partial of each tile
+  int32_t* verdicts;           // [n_segs]
+  uint8_t* tags_out;           // seal: [n_segs][16]
+  const uint8_t* tags_in;      // open: [n_segs][16]
+  KeyTableDev kt;
+};
+
+// Launch wrappers (gift_kernels.hip).  All enqueue on `s` and return the
+// launch status.
+hipError_t launch_key_setup(const uint8_t* keys_dev, KeyTableDev kt, hipStream_t s);
+hipError_t launch_check_owner(const SegDesc* segs, uint32_t n_segs, const uint32_t* labels, int32_t* verdicts,
+                              hipStream_t s);
+hipError_t launch_expand(const SegDesc* segs, uint32_t n_segs, uint32_t* tile_base, uint32_t* small_list,
+                         int32_t* verdicts, bool init_verdicts, hipStream_t s);
+hipError_t launch_gcm_tiles(const GcmArgs& a, bool open, uint32_t grid, hipStream_t s);
+hipError_t launch_gcm_small(const GcmArgs& a, bool open, hipStream_t s);
+hipError_t launch_gcm_finalize(const GcmArgs& a, bool open, hipStream_t s);
+hipError_t launch_zero_ranges(uint8_t* out, const ZeroRange* r, uint32_t n, const int32_t* verdicts, uint32_t grid,
+                              hipStream_t s);
+hipError_t launch_wipe(void* p, size_t bytes, hipStream_t s);
+
+}  // namespace gift

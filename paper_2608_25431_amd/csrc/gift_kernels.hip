@@ -1,0 +1,585 @@
+// gfx950 kernels for segmented, per-user AES-256-GCM and the owner check.
+//
+// Hot path (k_gcm_tiles): one workgroup of 1024 threads per CU, persistent
+// over 2 MiB tiles.  Each lane handles one 16-byte block per 1024-block row:
+//   - AES-256-CTR keystream from four T-tables in LDS, each replicated 32x so
+//     that lane l reads copy (l mod 32) and a wave's random lookups never
+//     collide in a bank; one v_perm_b32 forms each lookup address;
+//   - one coalesced 16-byte load, XOR, 16-byte store;
+//   - GHASH by per-lane Horner with M = H^1024: Y <- Y*M xor X, where the
+//     multiply by the fixed M uses 32 nibble-indexed tables (8 KiB per user)
+//     staged in LDS.
+// Tiles are aligned to the END of their segment, so the block at distance d
+// from the segment's last block contributes X*H^(d + 2) to the GHASH sum; a
+// tile t contributes P_t * H^(t*T) with P_t the sum over its own blocks, and
+// lane l of a full tile ends at distance (1023 - l) from the tile's end.
+#include <hip/hip_runtime.h>
+
+#include "gift_device.hpp"
+#include "gift_internal.hpp"
+
+namespace gift {
+
+__constant__ AesConst c_aes = make_aes_const();
+
+constexpr int32_t kVerdictOk = 0, kVerdictAuthFail = 1, kVerdictOwnerMixed = 2;
+
+// LDS layout of k_gcm_tiles (bytes).
+constexpr uint32_t kLdsGtab = 0;                    // 32 x 16 x 16 B GHASH tables
+constexpr uint32_t kLdsAes = 8192;                  // T0/T1 (64 KiB) then T2/T3 (64 KiB)
+constexpr uint32_t kLdsRed = kLdsAes + 131072;      // 16 waves x 16 B
+constexpr uint32_t kLdsInfo = kLdsRed + 256;        // broadcast scratch
+constexpr uint32_t kLdsBytes = kLdsInfo + 16;
+
+__device__ __forceinline__ uint32_t lds32(const uint8_t* base, uint32_t off) {
+  return *(const uint32_t*)(base + off);
+}
+__device__ __forceinline__ uint4 lds128(const uint8_t* base, uint32_t off) { return *(const uint4*)(base + off); }
+
+// T-table address of byte k of w for lane copy L: (x << 8) | (lane*4) in the
+// first 64 KiB region (T0 at +0, T1 at +128) or, with the 0x10000 bit taken
+// from L, the second region (T2 at +0, T3 at +128).
+#define GIFT_SEL_A(k) (0x0c0c0000u | ((4u + (k)) << 8))
+#define GIFT_SEL_B(k) (0x0c020000u | ((4u + (k)) << 8))
+#define GIFT_T0(w, k) lds32(tt, __builtin_amdgcn_perm((w), L, GIFT_SEL_A(k)))
+#define GIFT_T1(w, k) lds32(tt + 128, __builtin_amdgcn_perm((w), L, GIFT_SEL_A(k)))
+#define GIFT_T2(w, k) lds32(tt, __builtin_amdgcn_perm((w), L, GIFT_SEL_B(k)))
+#define GIFT_T3(w, k) lds32(tt + 128, __builtin_amdgcn_perm((w), L, GIFT_SEL_B(k)))
+
+// AES-256 on one block whose initial AddRoundKey is already applied.
+__device__ __forceinline__ void aes_rounds_lds(uint32_t& s0, uint32_t& s1, uint32_t& s2, uint32_t& s3,
+                                               const uint32_t* rk, const uint8_t* tt, uint32_t L) {
+#pragma unroll
+  for (int r = 1; r < 14; r++) {
+    uint32_t t0 = xor3(GIFT_T0(s0, 0), GIFT_T1(s1, 1), GIFT_T2(s2, 2));
+    uint32_t t1 = xor3(GIFT_T0(s1, 0), GIFT_T1(s2, 1), GIFT_T2(s3, 2));
+    uint32_t t2 = xor3(GIFT_T0(s2, 0), GIFT_T1(s3, 1), GIFT_T2(s0, 2));
+    uint32_t t3 = xor3(GIFT_T0(s3, 0), GIFT_T1(s0, 1), GIFT_T2(s1, 2));
+    t0 = xor3(t0, GIFT_T3(s3, 3), rk[4 * r + 0]);
+    t1 = xor3(t1, GIFT_T3(s0, 3), rk[4 * r + 1]);
+    t2 = xor3(t2, GIFT_T3(s1, 3), rk[4 * r + 2]);
+    t3 = xor3(t3, GIFT_T3(s2, 3), rk[4 * r + 3]);
+    s0 = t0;
+    s1 = t1;
+    s2 = t2;
+    s3 = t3;
+  }
+  // Last round: S(x) is byte 0 of T2[x], byte 1 of T3[x], byte 2 of T0[x],
+  // byte 3 of T1[x]; v_perm merges them, and the halves do not overlap so
+  // OR = XOR.
+#define GIFT_LAST(a, b, c, d, rkw)                                                              \
+  xor3(__builtin_amdgcn_perm(GIFT_T3(b, 1), GIFT_T2(a, 0), 0x0c0c0500u),                        \
+       __builtin_amdgcn_perm(GIFT_T1(d, 3), GIFT_T0(c, 2), 0x07020c0cu), (rkw))
+  const uint32_t o0 = GIFT_LAST(s0, s1, s2, s3, rk[56]);
+  const uint32_t o1 = GIFT_LAST(s1, s2, s3, s0, rk[57]);
+  const uint32_t o2 = GIFT_LAST(s2, s3, s0, s1, rk[58]);
+  const uint32_t o3 = GIFT_LAST(s3, s0, s1, s2, rk[59]);
+#undef GIFT_LAST
+  s0 = o0;
+  s1 = o1;
+  s2 = o2;
+  s3 = o3;
+}
+
+// Y*M xor X with the 32 nibble tables of M in LDS: nibble q of Y (GCM bits
+// 4q..4q+3; q even = high nibble of byte q/2) selects entry q*256 + v*16.
+__device__ __forceinline__ u128 ghash_step_lds(const u128& y, const u128& x, const uint8_t* gt) {
+  uint32_t a0 = x.w[0], a1 = x.w[1], a2 = x.w[2], a3 = x.w[3];
+#pragma unroll
+  for (int j = 0; j < 4; j++) {
+    const uint32_t w = y.w[j];
+#pragma unroll
+    for (int k = 0; k < 4; k++) {
+      const int q = 2 * (4 * j + k);
+      const uint32_t hi = (w >> (8 * k)) & 0xF0u;
+      const uint32_t lo = ((w >> (8 * k)) << 4) & 0xF0u;
+      const uint4 e = lds128(gt + q * 256, hi);
+      const uint4 f = lds128(gt + (q + 1) * 256, lo);
+      a0 = xor3(a0, e.x, f.x);
+      a1 = xor3(a1, e.y, f.y);
+      a2 = xor3(a2, e.z, f.z);
+      a3 = xor3(a3, e.w, f.w);
+    }
+  }
+  return u128{{a0, a1, a2, a3}};
+}
+
+__device__ __forceinline__ u128 load_block(const uint8_t* p, uint32_t n, bool aligned) {
+  if (aligned && n == 16) {
+    uint4 v = *(const uint4*)p;
+    return u128{{v.x, v.y, v.z, v.w}};
+  }
+  u128 r = u128_zero();
+#pragma unroll
+  for (uint32_t k = 0; k < 16; k++)
+    if (k < n) r.w[k >> 2] |= (uint32_t)p[k] << (8 * (k & 3));
+  return r;
+}
+
+__device__ __forceinline__ void store_block(uint8_t* p, const u128& v, uint32_t n, bool aligned) {
+  if (aligned && n == 16) {
+    *(uint4*)p = make_uint4(v.w[0], v.w[1], v.w[2], v.w[3]);
+    return;
+  }
+#pragma unroll
+  for (uint32_t k = 0; k < 16; k++)
+    if (k < n) p[k] = (uint8_t)(v.w[k >> 2] >> (8 * (k & 3)));
+}
+
+// keep the first n bytes of a block, zero the rest
+__device__ __forceinline__ u128 mask_block(const u128& v, uint32_t n) {
+  if (n >= 16) return v;
+  u128 r = v;
+#pragma unroll
+  for (int j = 0; j < 4; j++) {
+    int keep = (int)n - 4 * j;
+    uint32_t m = keep >= 4 ? 0xFFFFFFFFu : (keep <= 0 ? 0u : ((1u << (8 * keep)) - 1u));
+    r.w[j] &= m;
+  }
+  return r;
+}
+
+__device__ __forceinline__ u128 ld_u128(const uint4* p) {
+  uint4 v = *p;
+  return u128{{v.x, v.y, v.z, v.w}};
+}
+__device__ __forceinline__ void st_u128(uint4* p, const u128& v) { *p = make_uint4(v.w[0], v.w[1], v.w[2], v.w[3]); }
+
+// GHASH length block 0^64 || BE64(8*len) as block words.
+__device__ __forceinline__ u128 length_block(uint64_t len) {
+  uint64_t bits = len * 8ull;
+  return u128{{0u, 0u, bswap32((uint32_t)(bits >> 32)), bswap32((uint32_t)bits)}};
+}
+
+// ---------------------------------------------------------------------------
+// Per-block kernel over 2 MiB tiles of the non-small segments.
+// ---------------------------------------------------------------------------
+template <bool OPEN>
+__global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
+  __shared__ __attribute__((aligned(16))) uint8_t smem[kLdsBytes];
+  const uint32_t tid = threadIdx.x;
+  uint8_t* tt = smem + kLdsAes;
+  const uint8_t* gt = smem + kLdsGtab;
+  uint32_t* info = (uint32_t*)(smem + kLdsInfo);
+  u128* red = (u128*)(smem + kLdsRed);
+
+  // Replicated T-tables: word w = region*16384 + x*64 + slot holds
+  // T_{2*region + slot/32}[x] = rotl(Te0[x], 8*table).
+  for (uint32_t w = tid; w < 32768u; w += kThreads) {
+    uint32_t region = w >> 14, x = (w >> 6) & 255u, slot = w & 63u;
+    uint32_t tab = 2u * region + (slot >> 5);
+    uint32_t v = c_aes.te0[x];
+    uint32_t sh = 8u * tab;
+    ((uint32_t*)tt)[w] = (v << sh) | (v >> ((32u - sh) & 31u));
+  }
+  const uint32_t L = ((tid & 31u) << 2) | 0x10000u;
+  uint32_t cur_user = 0xFFFFFFFFu;
+
+  const SegDesc* __restrict__ segs = a.segs;
+  const uint32_t* __restrict__ tile_base = a.tile_base;
+
+  for (uint32_t g = blockIdx.x; g < a.n_tiles; g += gridDim.x) {
+    __syncthreads();  // previous tile finished with gtab, red and info
+    if (tid == 0) {
+      uint32_t lo = 0, hi = a.n_segs;  // tile_base[lo] <= g < tile_base[hi]
+      while (hi - lo > 1) {
+        uint32_t mid = (lo + hi) >> 1;
+        if (tile_base[mid] <= g)
+          lo = mid;
+        else
+          hi = mid;
+      }
+      info[0] = lo;
+    }
+    __syncthreads();
+    const uint32_t s = __builtin_amdgcn_readfirstlane(info[0]);
+    const SegDesc* sd = segs + s;
+    const uint32_t user = sd->user;
+    const uint32_t m = sd->nblocks;
+    const uint64_t off = sd->byte_off, len = sd->len;
+    const bool aligned = (sd->flags & kSegAligned) != 0;
+    const uint32_t t = g - tile_base[s];
+    const int32_t verdict = a.verdicts[s];
+    const int64_t base = (int64_t)m - (int64_t)(t + 1) * (int64_t)kTileBlocks;  // block index of virtual slot 0
+    const int r_start = base < 0 ? (int)((uint64_t)(-base) / kThreads) : 0;
+
+    if (verdict != kVerdictOk) {
+      // rejected before this call's data is touched: release zeros only
+      for (int r = r_start; r < kRows; r++) {
+        const int64_t i0 = base + (int64_t)r * kThreads + tid;
+        if (i0 >= 0) {
+          const uint64_t rem = len - 16ull * (uint64_t)i0;
+          store_block(a.out + off + 16ull * (uint64_t)i0, u128_zero(), rem >= 16 ? 16u : (uint32_t)rem, aligned);
+        }
+      }
+      continue;
+    }
+
+    if (user != cur_user) {
+      const uint4* src = a.kt.gtab + (size_t)user * 512u;
+      for (uint32_t i = tid; i < 512u; i += kThreads) ((uint4*)(smem + kLdsGtab))[i] = src[i];
+      cur_user = user;
+      __syncthreads();
+    }
+
+    uint32_t rk[60];
+    const uint32_t* rkp = a.kt.rk + (size_t)user * 64u;
+#pragma unroll
+    for (int i = 0; i < 60; i++) rk[i] = rkp[i];
+    const uint32_t k0 = sd->iv[0] ^ rk[0], k1 = sd->iv[1] ^ rk[1], k2 = sd->iv[2] ^ rk[2];
+
+    u128 y = u128_zero();
+    for (int r = r_start; r < kRows; r++) {
+      const int64_t i0 = base + (int64_t)r * kThreads + tid;
+      u128 x = u128_zero();
+      if (i0 >= 0) {
+        uint32_t s0 = k0, s1 = k1, s2 = k2, s3 = bswap32(2u + (uint32_t)i0) ^ rk[3];
+        aes_rounds_lds(s0, s1, s2, s3, rk, tt, L);
+        const uint64_t boff = off + 16ull * (uint64_t)i0;
+        const uint64_t rem = len - 16ull * (uint64_t)i0;
+        const uint32_t n = rem >= 16 ? 16u : (uint32_t)rem;
+        const u128 in = load_block(a.in + boff, n, aligned);
+        u128 o = u128{{in.w[0] ^ s0, in.w[1] ^ s1, in.w[2] ^ s2, in.w[3] ^ s3}};
+        o = mask_block(o, n);
+        store_block(a.out + boff, o, n, aligned);
+        x = OPEN ? in : o;
+      }
+      y = ghash_step_lds(y, x, gt);
+    }
+
+    // lane contribution y * H^(1023 - tid), then the workgroup sum
+    const u128 hp = ld_u128(a.kt.pow_h + (size_t)user * kHPowers + (kThreads - 1 - tid));
+    u128 z = gf_mul(y, hp);
+#pragma unroll
+    for (int j = 0; j < 4; j++) z.w[j] = wave_xor(z.w[j]);
+    if ((tid & 63u) == 0) red[tid >> 6] = z;
+    __syncthreads();
+    if (tid == 0) {
+      u128 p = red[0];
+      for (int w = 1; w < kThreads / 64; w++) p = u128_xor(p, red[w]);
+      st_u128(a.partials + g, p);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Per-segment finalize of tiled segments: S = H*(H*sum_t P_t H^(tT) xor L),
+// tag = E_K(J0) xor S.  One wave per segment; lane l folds tiles l, l+64, ...
+// ---------------------------------------------------------------------------
+template <bool OPEN>
+__global__ __launch_bounds__(kFinLanes) void k_finalize(GcmArgs a) {
+  const uint32_t s = blockIdx.x, lane = threadIdx.x;
+  const SegDesc sd = a.segs[s];
+  if (sd.flags & kSegSmall) return;
+  const int32_t verdict = a.verdicts[s];
+  if (verdict != kVerdictOk) {
+    if (!OPEN && lane < 4) ((uint32_t*)(a.tags_out + 16ull * s))[lane] = 0u;
+    return;
+  }
+  const uint32_t user = sd.user;
+  const uint32_t tb = a.tile_base[s], nt = a.tile_base[s + 1] - tb;
+  u128 z = u128_zero();
+  if (lane < nt) {
+    const u128 hlt = ld_u128(a.kt.pow_hlt + user);
+    const uint32_t K = (nt - 1 - lane) / kFinLanes + 1;
+    for (int k = (int)K - 1; k >= 0; k--) {
+      z = gf_mul(z, hlt);
+      z = u128_xor(z, ld_u128(a.partials + tb + lane + (uint32_t)k * kFinLanes));
+    }
+    z = gf_mul(z, ld_u128(a.kt.pow_ht + (size_t)user * kFinLanes + lane));
+  }
+#pragma unroll
+  for (int j = 0; j < 4; j++) z.w[j] = wave_xor(z.w[j]);
+  if (lane == 0) {
+    const u128 h = ld_u128((const uint4*)(a.kt.h + 4ull * user));
+    u128 sacc = gf_mul(u128_xor(gf_mul(z, h), length_block(sd.len)), h);
+    const uint32_t* rk = a.kt.rk + (size_t)user * 64u;
+    const uint32_t j0[4] = {sd.iv[0], sd.iv[1], sd.iv[2], 0x01000000u};
+    uint32_t e[4];
+    aes256_encrypt_words(rk, j0, e, c_aes);
+    u128 tag = u128{{e[0] ^ sacc.w[0], e[1] ^ sacc.w[1], e[2] ^ sacc.w[2], e[3] ^ sacc.w[3]}};
+    if (!OPEN) {
+      uint32_t* to = (uint32_t*)(a.tags_out + 16ull * s);
+      for (int j = 0; j < 4; j++) to[j] = tag.w[j];
+    } else {
+      const uint8_t* ti = a.tags_in + 16ull * s;
+      uint32_t diff = 0;
+#pragma unroll
+      for (int k = 0; k < 16; k++) diff |= (uint32_t)ti[k] ^ ((tag.w[k >> 2] >> (8 * (k & 3))) & 0xFFu);
+      a.verdicts[s] = diff ? kVerdictAuthFail : kVerdictOk;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Segments of at most 64 blocks: one wave each, lane j owns block j and its
+// GHASH term X_j * H^(m + 1 - j); lane 0 adds L*H.  Open decides the verdict
+// before any plaintext is written.
+// ---------------------------------------------------------------------------
+template <bool OPEN>
+__global__ __launch_bounds__(64) void k_small(GcmArgs a) {
+  const uint32_t s = a.small_list[blockIdx.x];
+  const uint32_t j = threadIdx.x;
+  const SegDesc sd = a.segs[s];
+  const uint32_t m = sd.nblocks;
+  const bool valid = j < m;
+  const bool aligned = (sd.flags & kSegAligned) != 0;
+  const uint64_t rem = valid ? sd.len - 16ull * j : 0;
+  const uint32_t n = rem >= 16 ? 16u : (uint32_t)rem;
+  uint8_t* dst = a.out + sd.byte_off + 16ull * j;
+  const int32_t verdict = a.verdicts[s];
+  if (verdict != kVerdictOk) {
+    if (valid) store_block(dst, u128_zero(), n, aligned);
+    if (!OPEN && j < 4) ((uint32_t*)(a.tags_out + 16ull * s))[j] = 0u;
+    return;
+  }
+  const uint32_t user = sd.user;
+  const uint32_t* rk = a.kt.rk + (size_t)user * 64u;
+  u128 in = u128_zero(), o = u128_zero(), z = u128_zero();
+  if (valid) {
+    in = load_block(a.in + sd.byte_off + 16ull * j, n, aligned);
+    const uint32_t cb[4] = {sd.iv[0], sd.iv[1], sd.iv[2], bswap32(2u + j)};
+    uint32_t ks[4];
+    aes256_encrypt_words(rk, cb, ks, c_aes);
+    o = mask_block(u128{{in.w[0] ^ ks[0], in.w[1] ^ ks[1], in.w[2] ^ ks[2], in.w[3] ^ ks[3]}}, n);
+    const u128 x = OPEN ? in : o;
+    z = gf_mul(x, ld_u128(a.kt.pow_h + (size_t)user * kHPowers + (m + 1 - j)));
+  }
+  const u128 h = ld_u128((const uint4*)(a.kt.h + 4ull * user));
+  if (j == 0) z = u128_xor(z, gf_mul(length_block(sd.len), h));
+#pragma unroll
+  for (int k = 0; k < 4; k++) z.w[k] = wave_xor(z.w[k]);
+  uint32_t ok = 1;
+  if (j == 0) {
+    const uint32_t j0[4] = {sd.iv[0], sd.iv[1], sd.iv[2], 0x01000000u};
+    uint32_t e[4];
+    aes256_encrypt_words(rk, j0, e, c_aes);
+    const u128 tag = u128{{e[0] ^ z.w[0], e[1] ^ z.w[1], e[2] ^ z.w[2], e[3] ^ z.w[3]}};
+    if (!OPEN) {
+      uint32_t* to = (uint32_t*)(a.tags_out + 16ull * s);
+      for (int k = 0; k < 4; k++) to[k] = tag.w[k];
+    } else {
+      const uint8_t* ti = a.tags_in + 16ull * s;
+      uint32_t diff = 0;
+#pragma unroll
+      for (int k = 0; k < 16; k++) diff |= (uint32_t)ti[k] ^ ((tag.w[k >> 2] >> (8 * (k & 3))) & 0xFFu);
+      ok = diff == 0;
+      a.verdicts[s] = ok ? kVerdictOk : kVerdictAuthFail;
+    }
+  }
+  if (OPEN) ok = __shfl(ok, 0, 64);
+  if (valid) store_block(dst, ok ? o : u128_zero(), n, aligned);
+}
+
+// ---------------------------------------------------------------------------
+// Segment-table expansion: per-segment tile counts -> exclusive prefix
+// (tile_base), and the list of small segments.  One workgroup.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(1024) void k_expand(const SegDesc* __restrict__ segs, uint32_t n,
+                                                 uint32_t* __restrict__ tile_base, uint32_t* __restrict__ small_list,
+                                                 int32_t* __restrict__ verdicts, int init_verdicts) {
+  __shared__ uint32_t sc_t[1024], sc_s[1024];
+  const uint32_t tid = threadIdx.x;
+  uint32_t carry_t = 0, carry_s = 0;
+  for (uint32_t b0 = 0; b0 < n; b0 += 1024) {
+    const uint32_t i = b0 + tid;
+    uint32_t nt = 0, sm = 0;
+    if (i < n) {
+      if (segs[i].flags & kSegSmall)
+        sm = 1;
+      else
+        nt = (uint32_t)(((uint64_t)segs[i].nblocks + kTileBlocks - 1) / kTileBlocks);
+      if (init_verdicts) verdicts[i] = kVerdictOk;
+    }
+    sc_t[tid] = nt;
+    sc_s[tid] = sm;
+    __syncthreads();
+    for (uint32_t o = 1; o < 1024; o <<= 1) {
+      const uint32_t vt = tid >= o ? sc_t[tid - o] : 0u, vs = tid >= o ? sc_s[tid - o] : 0u;
+      __syncthreads();
+      sc_t[tid] += vt;
+      sc_s[tid] += vs;
+      __syncthreads();
+    }
+    if (i < n) {
+      tile_base[i] = carry_t + sc_t[tid] - nt;
+      if (sm) small_list[carry_s + sc_s[tid] - sm] = i;
+    }
+    carry_t += sc_t[1023];
+    carry_s += sc_s[1023];
+    __syncthreads();
+  }
+  if (tid == 0) tile_base[n] = carry_t;
+}
+
+// ---------------------------------------------------------------------------
+// Owner-label check: verdict OWNER_MIXED iff some row label differs from the
+// segment's user (the sentinels never equal a user).
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_check_owner(const SegDesc* __restrict__ segs, uint32_t n,
+                                                     const uint32_t* __restrict__ labels,
+                                                     int32_t* __restrict__ verdicts) {
+  for (uint32_t s = blockIdx.x; s < n; s += gridDim.x) {
+    const uint64_t rb = segs[s].row_begin, rc = segs[s].row_count;
+    const uint32_t user = segs[s].user;
+    int bad = 0;
+    for (uint64_t r = threadIdx.x; r < rc; r += blockDim.x) bad |= labels[rb + r] != user;
+    bad = __syncthreads_or(bad);
+    if (threadIdx.x == 0) verdicts[s] = bad ? kVerdictOwnerMixed : kVerdictOk;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Zero-fill of uncovered rows and of rejected segments.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_zero_ranges(uint8_t* out, const ZeroRange* __restrict__ rs, uint32_t n,
+                                                     const int32_t* __restrict__ verdicts) {
+  const uint64_t gtid = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const uint64_t gsz = (uint64_t)gridDim.x * blockDim.x;
+  for (uint32_t i = 0; i < n; i++) {
+    const ZeroRange z = rs[i];
+    if (z.seg >= 0 && verdicts[z.seg] == kVerdictOk) continue;
+    uint8_t* p = out + z.off;
+    uint64_t head = (16u - ((uintptr_t)p & 15u)) & 15u;
+    if (head > z.len) head = z.len;
+    for (uint64_t b = gtid; b < head; b += gsz) p[b] = 0;
+    const uint64_t mid = (z.len - head) / 16u;
+    uint4* q = (uint4*)(p + head);
+    for (uint64_t k = gtid; k < mid; k += gsz) q[k] = make_uint4(0u, 0u, 0u, 0u);
+    for (uint64_t b = head + 16u * mid + gtid; b < z.len; b += gsz) p[b] = 0;
+  }
+}
+
+__global__ __launch_bounds__(256) void k_wipe(uint8_t* p, size_t bytes) {
+  const size_t gsz = (size_t)gridDim.x * blockDim.x;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < bytes; i += gsz) p[i] = 0;
+}
+
+// ---------------------------------------------------------------------------
+// Key-table setup.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(64) void k_key_sched(const uint8_t* __restrict__ keys, KeyTableDev kt) {
+  const uint32_t u = blockIdx.x * blockDim.x + threadIdx.x;
+  if (u >= kt.n_users) return;
+  uint32_t rk[60];
+  aes256_key_schedule(keys + 32ull * u, rk, c_aes);
+  for (int i = 0; i < 60; i++) kt.rk[64ull * u + i] = rk[i];
+  for (int i = 60; i < 64; i++) kt.rk[64ull * u + i] = 0u;
+  const uint32_t zero[4] = {0u, 0u, 0u, 0u};
+  uint32_t h[4];
+  aes256_encrypt_words(rk, zero, h, c_aes);
+  for (int i = 0; i < 4; i++) kt.h[4ull * u + i] = h[i];
+}
+
+constexpr uint32_t kPowersPerUser = kHPowers + kFinLanes + 1;
+
+__global__ __launch_bounds__(256) void k_key_powers(KeyTableDev kt) {
+  const uint64_t idx = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const uint64_t u = idx / kPowersPerUser;
+  const uint32_t j = (uint32_t)(idx % kPowersPerUser);
+  if (u >= kt.n_users) return;
+  const u128 h = ld_u128((const uint4*)(kt.h + 4ull * u));
+  if (j < (uint32_t)kHPowers) {
+    st_u128(kt.pow_h + u * kHPowers + j, gf_pow(h, j));
+  } else if (j < (uint32_t)(kHPowers + kFinLanes)) {
+    const uint32_t l = j - kHPowers;
+    st_u128(kt.pow_ht + u * kFinLanes + l, gf_pow(h, (uint64_t)l * kTileBlocks));
+  } else {
+    st_u128(kt.pow_hlt + u, gf_pow(h, (uint64_t)kFinLanes * kTileBlocks));
+  }
+}
+
+// Nibble tables of M = H^kThreads: entry [q][v] = (v placed at GCM bits
+// 4q..4q+3, MSB first) * M, built from the four products x^(4q+k) * M.
+__global__ __launch_bounds__(256) void k_key_gtab(KeyTableDev kt) {
+  const uint64_t idx = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const uint64_t u = idx / 32u;
+  const int q = (int)(idx % 32u);
+  if (u >= kt.n_users) return;
+  const u128 h = ld_u128((const uint4*)(kt.h + 4ull * u));
+  const u128 mm = gf_pow(h, (uint64_t)kThreads);
+  u128 b[4];
+  for (int k = 0; k < 4; k++) b[k] = gf_mul(gf_xpow_elem(4 * q + k), mm);
+  for (int v = 0; v < 16; v++) {
+    u128 e = u128_zero();
+    for (int k = 0; k < 4; k++)
+      if (v & (8 >> k)) e = u128_xor(e, b[k]);
+    st_u128(kt.gtab + u * 512u + (uint64_t)q * 16u + v, e);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Launch wrappers.
+// ---------------------------------------------------------------------------
+static inline uint32_t cdiv(uint64_t a, uint64_t b) { return (uint32_t)((a + b - 1) / b); }
+
+hipError_t launch_key_setup(const uint8_t* keys_dev, KeyTableDev kt, hipStream_t s) {
+  hipLaunchKernelGGL(k_key_sched, dim3(cdiv(kt.n_users, 64)), dim3(64), 0, s, keys_dev, kt);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_key_powers, dim3(cdiv((uint64_t)kt.n_users * kPowersPerUser, 256)), dim3(256), 0, s, kt);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_key_gtab, dim3(cdiv((uint64_t)kt.n_users * 32u, 256)), dim3(256), 0, s, kt);
+  return hipGetLastError();
+}
+
+hipError_t launch_check_owner(const SegDesc* segs, uint32_t n_segs, const uint32_t* labels, int32_t* verdicts,
+                              hipStream_t s) {
+  if (n_segs == 0) return hipSuccess;
+  const uint32_t grid = n_segs < 65535u ? n_segs : 65535u;
+  hipLaunchKernelGGL(k_check_owner, dim3(grid), dim3(256), 0, s, segs, n_segs, labels, verdicts);
+  return hipGetLastError();
+}
+
+hipError_t launch_expand(const SegDesc* segs, uint32_t n_segs, uint32_t* tile_base, uint32_t* small_list,
+                         int32_t* verdicts, bool init_verdicts, hipStream_t s) {
+  hipLaunchKernelGGL(k_expand, dim3(1), dim3(1024), 0, s, segs, n_segs, tile_base, small_list, verdicts,
+                     init_verdicts ? 1 : 0);
+  return hipGetLastError();
+}
+
+hipError_t launch_gcm_tiles(const GcmArgs& a, bool open, uint32_t grid, hipStream_t s) {
+  if (a.n_tiles == 0) return hipSuccess;
+  const uint32_t g = a.n_tiles < grid ? a.n_tiles : grid;
+  if (open)
+    hipLaunchKernelGGL(k_gcm_tiles<true>, dim3(g), dim3(kThreads), 0, s, a);
+  else
+    hipLaunchKernelGGL(k_gcm_tiles<false>, dim3(g), dim3(kThreads), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_gcm_small(const GcmArgs& a, bool open, hipStream_t s) {
+  if (a.n_small == 0) return hipSuccess;
+  if (open)
+    hipLaunchKernelGGL(k_small<true>, dim3(a.n_small), dim3(64), 0, s, a);
+  else
+    hipLaunchKernelGGL(k_small<false>, dim3(a.n_small), dim3(64), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_gcm_finalize(const GcmArgs& a, bool open, hipStream_t s) {
+  if (a.n_tiles == 0) return hipSuccess;
+  if (open)
+    hipLaunchKernelGGL(k_finalize<true>, dim3(a.n_segs), dim3(kFinLanes), 0, s, a);
+  else
+    hipLaunchKernelGGL(k_finalize<false>, dim3(a.n_segs), dim3(kFinLanes), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_zero_ranges(uint8_t* out, const ZeroRange* r, uint32_t n, const int32_t* verdicts, uint32_t grid,
+                              hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_zero_ranges, dim3(grid), dim3(256), 0, s, out, r, n, verdicts);
+  return hipGetLastError();
+}
+
+hipError_t launch_wipe(void* p, size_t bytes, hipStream_t s) {
+  if (bytes == 0) return hipSuccess;
+  uint32_t grid = cdiv(bytes, 256u * 16u);
+  if (grid > 4096u) grid = 4096u;
+  hipLaunchKernelGGL(k_wipe, dim3(grid), dim3(256), 0, s, (uint8_t*)p, bytes);
+  return hipGetLastError();
+}
+
+}  // namespace gift

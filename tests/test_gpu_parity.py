@@ -1,0 +1,323 @@
+"""Parity of the HIP library (through its C ABI) with the CPU oracle.
+
+Small and ragged cases compare every output byte, tag and verdict.  The
+full-size configurations compare sampled ciphertext blocks one by one (the
+oracle's GCTR on the block's counter), exact tags of the smallest segments,
+and properties that hold at any size: open(seal(P)) = P bit for bit, exactly
+the tampered segments fail, exactly the mixed-owner segments are rejected.
+The tolerance is zero everywhere: all of this is integer work.
+"""
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU")]
+
+import oracle  # noqa: E402
+from gpu_helpers import (DEV, dev_u32, dev_u8, expected_block, host, open_, oracle_segments, seal,  # noqa: E402
+                         status_of)
+from paper_2608_25431_amd import gift  # noqa: E402
+from paper_2608_25431_amd import workloads as W  # noqa: E402
+
+rng = np.random.default_rng(4242)
+
+
+def keyset(n):
+    return rng.integers(0, 256, (n, 32), dtype=np.uint8), rng.integers(0, 256, (n, 12), dtype=np.uint8)
+
+
+@pytest.fixture(scope="module")
+def kt3():
+    keys, nb = keyset(3)
+    kt = gift.KeyTable(keys)
+    yield keys, nb, kt
+    kt.destroy()
+
+
+def full_compare(keys, nb, kt, data, n_rows, rb, table, labels=None, in_place=False):
+    """Seal + open on the GPU vs the oracle, every byte."""
+    st, o_out, o_tags, o_ver = oracle.seal(data, n_rows, rb, table, keys, nb, labels=labels)
+    assert st == 0
+    d = dev_u8(data)
+    lab = None if labels is None else dev_u32(labels)
+    out, tags, ver = seal(d, n_rows, rb, table, kt, nb, labels_dev=lab, out=d if in_place else None)
+    n = len(table)
+    assert host(out).tobytes() == o_out.tobytes()
+    assert host(tags)[:16 * n].tobytes() == o_tags.tobytes()
+    assert host(ver)[:n].tolist() == o_ver.tolist()
+    st, o_back, o_ver2 = oracle.open_(o_out, n_rows, rb, table, keys, nb, o_tags, labels=labels)
+    back, ver2 = open_(out, n_rows, rb, table, kt, nb, tags, labels_dev=lab)
+    assert host(back).tobytes() == o_back.tobytes()
+    assert host(ver2)[:n].tolist() == o_ver2.tolist()
+    return out, tags
+
+
+def test_key_table_lifecycle():
+    keys, _ = keyset(5)
+    kt = gift.KeyTable(keys)
+    assert kt.users == 5
+    kt.destroy()
+    assert status_of(gift.KeyTable, np.zeros(0, np.uint8), 0) == gift.E_INVALID
+
+
+def test_tiny_config_every_byte():
+    w = W.tiny()
+    t = w.tensors[0]
+    kt = gift.KeyTable(w.keys)
+    data = t.generate("cpu").numpy()
+    full_compare(w.keys, w.nonce_base, kt, data, t.n_rows, t.row_bytes, t.segs)
+    kt.destroy()
+
+
+def segmentations(n_rows):
+    import itertools
+    for choice in itertools.product((0, 1, 2), repeat=n_rows):
+        segs, cur = [], None
+        for r, c in enumerate(choice):
+            if c == 0:
+                cur = None
+            elif c == 1 or cur is None:
+                segs.append([r, 1])
+                cur = segs[-1]
+            else:
+                cur[1] += 1
+        yield [tuple(s) for s in segs]
+
+
+@pytest.mark.parametrize("row_bytes", [4, 12, 16, 20, 48])
+def test_brute_force_tiny_tensors(kt3, row_bytes):
+    keys, nb, kt = kt3
+    for n_rows in (1, 2, 3):
+        data = rng.integers(0, 256, n_rows * row_bytes, dtype=np.uint8)
+        for segs in segmentations(n_rows):
+            table = [(b, c, i % 3, 1000 * n_rows + 10 * b + i) for i, (b, c) in enumerate(segs)]
+            full_compare(keys, nb, kt, data, n_rows, row_bytes, table)
+            full_compare(keys, nb, kt, data, n_rows, row_bytes, table, in_place=True)
+
+
+@pytest.mark.parametrize("row_bytes,rows", [
+    (16384, [1, 63, 64, 65, 129, 130, 200]),   # aligned; 2 MiB tiles: 128 rows = 1 tile
+    (1000, [1, 17, 2100, 3, 4200]),            # unaligned starts, multi-tile
+    (65536 + 16, [33, 1, 70]),                 # aligned, tiles end mid-row
+    (48, [1, 2, 21, 22, 23, 44000]),           # small segments next to a 2 MiB one
+])
+def test_ragged_multi_tile_every_byte(kt3, row_bytes, rows):
+    keys, nb, kt = kt3
+    # segments with gaps of one row between them
+    table, r = [], 1
+    for i, n in enumerate(rows):
+        table.append((r, n, i % 3, 7 + i))
+        r += n + 1
+    n_rows = r
+    data = rng.integers(0, 256, n_rows * row_bytes, dtype=np.uint8)
+    full_compare(keys, nb, kt, data, n_rows, row_bytes, table)
+
+
+def test_five_tile_segment_every_byte(kt3):
+    keys, nb, kt = kt3
+    rb = 4096
+    n = 2560 + 7  # 10 MiB + 28 KiB: 5 full tiles and a ragged first tile
+    data = rng.integers(0, 256, n * rb, dtype=np.uint8)
+    full_compare(keys, nb, kt, data, n, rb, [(0, n, 1, 99)])
+
+
+def test_owner_labels_fused_and_standalone(kt3):
+    keys, nb, kt = kt3
+    rb, n_rows = 4096, 700
+    table = [(0, 10, 0, 1), (10, 600, 1, 1), (610, 80, 2, 1), (690, 10, 0, 2)]
+    lab = np.zeros(n_rows, np.uint32)
+    for b, c, u, _ in table:
+        lab[b:b + c] = u
+    data = rng.integers(0, 256, n_rows * rb, dtype=np.uint8)
+    full_compare(keys, nb, kt, data, n_rows, rb, table, labels=lab)
+    for row, v in ((5, 2), (300, gift.LABEL_PARAM), (650, gift.LABEL_UNOWNED), (695, 1)):
+        l2 = lab.copy()
+        l2[row] = v
+        full_compare(keys, nb, kt, data, n_rows, rb, table, labels=l2)
+        ver = torch.full((4,), -1, dtype=torch.int32, device=DEV)
+        gift.check_owner(table, dev_u32(l2), n_rows, ver)
+        st, o = oracle.check_owner(table, l2, n_rows)
+        assert host(ver).tolist() == o.tolist()
+
+
+def test_validation_status_matches_oracle(kt3):
+    keys, nb, kt = kt3
+    n_rows, rb = 6, 16
+    d = dev_u8(np.zeros(n_rows * rb, np.uint8))
+    cases = [
+        [(0, 0, 0, 0)], [(0, 1, 0, 0, 1)], [(0, 1, gift.LABEL_PARAM, 0)], [(0, 1, gift.LABEL_UNOWNED, 0)],
+        [(5, 2, 0, 0)], [(7, 1, 0, 0)], [(0, 1, 3, 0)], [(0, 2, 0, 0), (1, 2, 1, 0)],
+        [(0, 1, 0, 5), (3, 1, 0, 5)], [(0, 1, 0, 5), (3, 1, 1, 5)], [(0, 0, 0, 0), (9, 1, 0, 0)],
+        [(9, 1, 0, 0), (0, 0, 0, 0)], [], [(0, 6, 2, 1)],
+    ]
+    for table in cases:
+        st_o = oracle.seal(np.zeros(n_rows * rb, np.uint8), n_rows, rb, table, keys, nb)[0]
+        st_g = status_of(seal, d, n_rows, rb, table, kt, nb)
+        assert st_g == st_o, table
+    # partial overlap of out and data is rejected; exact aliasing is fine
+    big = dev_u8(np.zeros(2 * n_rows * rb, np.uint8))
+    tags = torch.zeros(16, dtype=torch.uint8, device=DEV)
+    s = status_of(gift.seal, big[:n_rows * rb], n_rows, rb, [(0, 1, 0, 0)], kt, nb, big[16:16 + n_rows * rb], tags)
+    assert s == gift.E_INVALID
+    assert status_of(gift.seal, big, n_rows, rb, [(0, 1, 0, 0)], kt, nb, big, tags) == 0
+    # open needs verdicts
+    assert status_of(gift.open, big, n_rows, rb, [(0, 1, 0, 0)], kt, nb, big, tags, None) == gift.E_INVALID
+
+
+def test_wrong_key_table_fails_every_segment(kt3):
+    keys, nb, kt = kt3
+    keys2, _ = keyset(3)
+    kt2 = gift.KeyTable(keys2)
+    n_rows, rb = 300, 8192
+    data = dev_u8(rng.integers(0, 256, n_rows * rb, dtype=np.uint8))
+    table = [(0, 1, 0, 1), (1, 200, 1, 1), (201, 99, 2, 1)]
+    ct, tags, _ = seal(data, n_rows, rb, table, kt, nb)
+    back, ver = open_(ct, n_rows, rb, table, kt2, nb, tags)
+    assert host(ver)[:3].tolist() == [gift.SEG_AUTH_FAIL] * 3
+    assert not host(back).any()
+    kt2.destroy()
+
+
+def test_non_default_stream(kt3):
+    keys, nb, kt = kt3
+    n_rows, rb = 200, 16384
+    data_np = rng.integers(0, 256, n_rows * rb, dtype=np.uint8)
+    table = [(0, 150, 0, 3), (150, 50, 1, 3)]
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        d = dev_u8(data_np)
+        out, tags, _ = seal(d, n_rows, rb, table, kt, nb)
+    s.synchronize()
+    st, o_out, o_tags, _ = oracle.seal(data_np, n_rows, rb, table, keys, nb)
+    assert host(out).tobytes() == o_out.tobytes() and host(tags)[:32].tobytes() == o_tags.tobytes()
+
+
+# --------------------------------------------------------------------------
+# full-size configurations
+# --------------------------------------------------------------------------
+def sampled_blocks(w, t, out_dev, n_samples=512, seed=5):
+    """Compare n_samples random blocks of the sealed tensor with the oracle."""
+    r = np.random.default_rng(seed)
+    segs = t.segs
+    picks = r.integers(0, len(segs), n_samples)
+    offs, exp = [], []
+    for i in picks:
+        s = segs[int(i)]
+        off, ln = t.seg_bytes(int(i))
+        nblk = (ln + 15) // 16
+        j = int(r.integers(0, nblk)) if r.random() < 0.9 else nblk - 1
+        n = min(16, ln - 16 * j)
+        plain = t.generate("cpu", off + 16 * j, n).numpy().tobytes()
+        exp.append(expected_block(w.keys, w.nonce_base, s, j, plain))
+        offs.append((off + 16 * j, n))
+    idx = torch.tensor([o + k for o, n in offs for k in range(n)], dtype=torch.int64, device=DEV)
+    got = host(out_dev[idx]).tobytes()
+    assert got == b"".join(exp)
+
+
+def smallest_tags(w, t, tags_dev, k=2):
+    lens = [t.seg_bytes(i)[1] for i in range(len(t.segs))]
+    pick = sorted(range(len(lens)), key=lambda i: lens[i])[:k]
+    sub = t.segs[pick]
+    res = oracle_segments(w.keys, w.nonce_base, sub, t.row_bytes,
+                          lambda j: t.generate("cpu", *t.seg_bytes(pick[j])).numpy().tobytes())
+    got = host(tags_dev).reshape(-1, 16)
+    for j, i in enumerate(pick):
+        assert got[i].tobytes() == res[j][1], f"segment {i}"
+
+
+def test_llama3_8b_kv_full_size():
+    w = W.llama3_8b_kv()
+    t = w.tensors[0]
+    kt = gift.KeyTable(w.keys)
+    d = t.generate(DEV)
+    ct, tags, ver = seal(d, t.n_rows, t.row_bytes, t.segs, kt, w.nonce_base)
+    sampled_blocks(w, t, ct)
+    smallest_tags(w, t, tags)
+    back, ver2 = open_(ct, t.n_rows, t.row_bytes, t.segs, kt, w.nonce_base, tags)
+    assert (host(ver2) == 0).all()
+    assert torch.equal(back, d)
+    kt.destroy()
+
+
+def test_tamper_config_full_size():
+    w = W.tamper()
+    t = w.tensors[0]
+    kt = gift.KeyTable(w.keys)
+    d = t.generate(DEV)
+    ct, tags, _ = seal(d, t.n_rows, t.row_bytes, t.segs, kt, w.nonce_base)
+    bad = set()
+    for (_, i, kind, off, bit) in w.tamper:
+        if kind == "ct":
+            ct[off] ^= (1 << bit)
+        else:
+            tags[16 * i + off] ^= (1 << bit)
+        bad.add(i)
+    back, ver = open_(ct, t.n_rows, t.row_bytes, t.segs, kt, w.nonce_base, tags)
+    v = host(ver)
+    assert set(np.nonzero(v)[0].tolist()) == bad
+    assert all(v[i] == gift.SEG_AUTH_FAIL for i in bad)
+    for i in range(len(t.segs)):
+        off, ln = t.seg_bytes(i)
+        if i in bad:
+            assert not back[off:off + ln].any().item()
+        else:
+            assert torch.equal(back[off:off + ln], d[off:off + ln])
+    # owner check: exactly the injected mixed segments
+    lab = dev_u32(t.labels)
+    cv = torch.full((len(t.segs),), -1, dtype=torch.int32, device=DEV)
+    gift.check_owner(t.segs, lab, t.n_rows, cv)
+    mixed = {i for (_, i, _, _) in w.mixed}
+    cvh = host(cv)
+    assert set(np.nonzero(cvh)[0].tolist()) == mixed and all(cvh[i] == gift.SEG_OWNER_MIXED for i in mixed)
+    # fused into seal: mixed segments are zeroed with zero tags, others unchanged
+    ct2, tags2, ver2 = seal(d, t.n_rows, t.row_bytes, t.segs, kt, w.nonce_base, labels_dev=lab)
+    assert set(np.nonzero(host(ver2))[0].tolist()) == mixed
+    t2 = host(tags2).reshape(-1, 16)
+    t1 = host(tags).reshape(-1, 16)
+    for i in range(len(t.segs)):
+        off, ln = t.seg_bytes(i)
+        if i in mixed:
+            assert not t2[i].any() and not ct2[off:off + ln].any().item()
+        elif i not in bad:
+            assert t2[i].tobytes() == t1[i].tobytes()
+    kt.destroy()
+
+
+def test_decode_batch_full_size():
+    w = W.decode_batch()
+    kt = gift.KeyTable(w.keys)
+    for t in w.tensors:
+        data = t.generate("cpu").numpy()
+        d = dev_u8(data)
+        ct, tags, ver = seal(d, t.n_rows, t.row_bytes, t.segs, kt, w.nonce_base)
+        res = oracle_segments(w.keys, w.nonce_base, t.segs, t.row_bytes,
+                              lambda i: data[slice(*(lambda o, l: (o, o + l))(*t.seg_bytes(i)))].tobytes())
+        got = host(ct)
+        gt = host(tags).reshape(-1, 16)
+        for i in range(len(t.segs)):
+            off, ln = t.seg_bytes(i)
+            assert got[off:off + ln].tobytes() == res[i][0], (t.name, i)
+            assert gt[i].tobytes() == res[i][1], (t.name, i)
+        back, ver2 = open_(ct, t.n_rows, t.row_bytes, t.segs, kt, w.nonce_base, tags)
+        assert (host(ver2) == 0).all() and torch.equal(back, d)
+    kt.destroy()
+
+
+def test_llama3_70b_kv_in_place_fused_full_size():
+    w = W.llama3_70b_kv()
+    t = w.tensors[0]
+    kt = gift.KeyTable(w.keys)
+    d = t.generate(DEV)
+    ref = d.clone()
+    lab = dev_u32(t.labels)
+    _, tags, ver = seal(d, t.n_rows, t.row_bytes, t.segs, kt, w.nonce_base, labels_dev=lab, out=d)
+    assert (host(ver) == 0).all()
+    sampled_blocks(w, t, d, n_samples=256)
+    # the sealed cache shares no block with the plaintext
+    assert not torch.equal(d[:1 << 20], ref[:1 << 20])
+    back, ver2 = open_(d, t.n_rows, t.row_bytes, t.segs, kt, w.nonce_base, tags, labels_dev=lab, out=d)
+    assert (host(ver2) == 0).all()
+    assert torch.equal(d, ref)
+    kt.destroy()
