@@ -7,10 +7,19 @@
 
 namespace gift {
 
-// Work decomposition of the per-block kernel.
-constexpr int kThreads = 1024;                             // one workgroup per CU (LDS-bound)
-constexpr int kRows = 128;                                 // 1024-block rows per tile
-constexpr uint32_t kTileBlocks = (uint32_t)kThreads * kRows;  // 131072 blocks = 2 MiB per tile
+// Work decomposition of the per-block kernel: one workgroup per CU (its LDS
+// tables fill most of the CU's 160 KiB), kThreads lanes each owning one
+// 16-byte block of every kThreads-block row, kRows rows per tile.
+#ifndef GIFT_THREADS
+#define GIFT_THREADS 1024
+#endif
+#ifndef GIFT_ROWS
+#define GIFT_ROWS (131072 / GIFT_THREADS)
+#endif
+constexpr int kThreads = GIFT_THREADS;
+constexpr int kRows = GIFT_ROWS;
+constexpr uint32_t kTileBlocks = (uint32_t)kThreads * kRows;  // 2 MiB per tile by default
+static_assert(kThreads % 64 == 0 && kThreads <= 1024, "workgroup size");
 constexpr uint32_t kSmallMaxBlocks = 64;                   // segments up to 1 KiB: one wave each
 constexpr int kHPowers = kThreads;                         // H^0 .. H^(kThreads-1) per user
 constexpr int kFinLanes = 64;                              // lanes of the per-segment finalize

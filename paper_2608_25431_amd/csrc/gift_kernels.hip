@@ -27,8 +27,8 @@ constexpr int32_t kVerdictOk = 0, kVerdictAuthFail = 1, kVerdictOwnerMixed = 2;
 // LDS layout of k_gcm_tiles (bytes).
 constexpr uint32_t kLdsGtab = 0;                    // 32 x 16 x 16 B GHASH tables
 constexpr uint32_t kLdsAes = 8192;                  // T0/T1 (64 KiB) then T2/T3 (64 KiB)
-constexpr uint32_t kLdsRed = kLdsAes + 131072;      // 16 waves x 16 B
-constexpr uint32_t kLdsInfo = kLdsRed + 256;        // broadcast scratch
+constexpr uint32_t kLdsRed = kLdsAes + 131072;      // one 16 B slot per wave
+constexpr uint32_t kLdsInfo = kLdsRed + 16 * (kThreads / 64);  // broadcast scratch
 constexpr uint32_t kLdsBytes = kLdsInfo + 16;
 
 __device__ __forceinline__ uint32_t lds32(const uint8_t* base, uint32_t off) {
@@ -46,23 +46,26 @@ __device__ __forceinline__ uint4 lds128(const uint8_t* base, uint32_t off) { ret
 #define GIFT_T2(w, k) lds32(tt, __builtin_amdgcn_perm((w), L, GIFT_SEL_B(k)))
 #define GIFT_T3(w, k) lds32(tt + 128, __builtin_amdgcn_perm((w), L, GIFT_SEL_B(k)))
 
-// AES-256 on one block whose initial AddRoundKey is already applied.
+// AES-256 rounds R0..13 and the final round on a state that has been through
+// rounds 1..R0-1 already.
+template <int R0>
 __device__ __forceinline__ void aes_rounds_lds(uint32_t& s0, uint32_t& s1, uint32_t& s2, uint32_t& s3,
                                                const uint32_t* rk, const uint8_t* tt, uint32_t L) {
 #pragma unroll
-  for (int r = 1; r < 14; r++) {
-    uint32_t t0 = xor3(GIFT_T0(s0, 0), GIFT_T1(s1, 1), GIFT_T2(s2, 2));
-    uint32_t t1 = xor3(GIFT_T0(s1, 0), GIFT_T1(s2, 1), GIFT_T2(s3, 2));
-    uint32_t t2 = xor3(GIFT_T0(s2, 0), GIFT_T1(s3, 1), GIFT_T2(s0, 2));
-    uint32_t t3 = xor3(GIFT_T0(s3, 0), GIFT_T1(s0, 1), GIFT_T2(s1, 2));
-    t0 = xor3(t0, GIFT_T3(s3, 3), rk[4 * r + 0]);
-    t1 = xor3(t1, GIFT_T3(s0, 3), rk[4 * r + 1]);
-    t2 = xor3(t2, GIFT_T3(s1, 3), rk[4 * r + 2]);
-    t3 = xor3(t3, GIFT_T3(s2, 3), rk[4 * r + 3]);
-    s0 = t0;
-    s1 = t1;
-    s2 = t2;
-    s3 = t3;
+  for (int r = R0; r < 14; r++) {
+    // all 16 lookups of the round are issued before any is combined, so a
+    // wave keeps 16 LDS reads in flight
+    const uint32_t a0 = GIFT_T0(s0, 0), a1 = GIFT_T1(s1, 1), a2 = GIFT_T2(s2, 2), a3 = GIFT_T3(s3, 3);
+    const uint32_t b0 = GIFT_T0(s1, 0), b1 = GIFT_T1(s2, 1), b2 = GIFT_T2(s3, 2), b3 = GIFT_T3(s0, 3);
+    const uint32_t c0 = GIFT_T0(s2, 0), c1 = GIFT_T1(s3, 1), c2 = GIFT_T2(s0, 2), c3 = GIFT_T3(s1, 3);
+    const uint32_t d0 = GIFT_T0(s3, 0), d1 = GIFT_T1(s0, 1), d2 = GIFT_T2(s1, 2), d3 = GIFT_T3(s2, 3);
+    __builtin_amdgcn_sched_group_barrier(0x0002, 16, 0);  // 16 address perms
+    __builtin_amdgcn_sched_group_barrier(0x0100, 16, 0);  // 16 LDS reads
+    __builtin_amdgcn_sched_group_barrier(0x0002, 8, 0);   // 8 xor3
+    s0 = xor3(xor3(a0, a1, a2), a3, rk[4 * r + 0]);
+    s1 = xor3(xor3(b0, b1, b2), b3, rk[4 * r + 1]);
+    s2 = xor3(xor3(c0, c1, c2), c3, rk[4 * r + 2]);
+    s3 = xor3(xor3(d0, d1, d2), d3, rk[4 * r + 3]);
   }
   // Last round: S(x) is byte 0 of T2[x], byte 1 of T3[x], byte 2 of T0[x],
   // byte 3 of T1[x]; v_perm merges them, and the halves do not overlap so
@@ -81,24 +84,99 @@ __device__ __forceinline__ void aes_rounds_lds(uint32_t& s0, uint32_t& s1, uint3
   s3 = o3;
 }
 
+// Counter-mode caching of rounds 1-2.  In a tile, lane l encrypts the counter
+// blocks IV || BE32(c + kThreads*r) for rows r, so (kThreads >= 256) the
+// counter's low 8 bits never change for the lane; the first three state columns are the IV (uniform).
+// After round 1 only column 1 depends on counter bits 8..15 (one lookup per
+// row); columns 2 and 3 depend on bits 16..31, which change at most twice per
+// tile; column 0 is fixed.  Round 2 then has one varying lookup per column.
+// So per row rounds 1-2 cost 5 lookups instead of 32.
+struct CtrCache {
+  uint32_t u1, u2, u3, in0;  // round-1 partial columns
+  uint32_t in2, in3;         // round-1 columns 2, 3 for the current counter bits 16..31
+  uint32_t w0, w1, w2, w3;   // round-2 partial columns
+  uint32_t hi;               // counter bits 16..31 the cache was built for
+};
+
+__device__ __forceinline__ void ctr_cache_init(CtrCache& c, uint32_t k0, uint32_t k1, uint32_t k2, uint32_t c0,
+                                               const uint32_t* rk, const uint8_t* tt, uint32_t L) {
+  // every lane reads its own table copy, so these are equal across the wave
+  const uint32_t u0 = __builtin_amdgcn_readfirstlane(xor3(GIFT_T0(k0, 0), GIFT_T1(k1, 1), GIFT_T2(k2, 2)) ^ rk[4]);
+  c.u1 = __builtin_amdgcn_readfirstlane(xor3(GIFT_T0(k1, 0), GIFT_T1(k2, 1), GIFT_T3(k0, 3)) ^ rk[5]);
+  c.u2 = __builtin_amdgcn_readfirstlane(xor3(GIFT_T0(k2, 0), GIFT_T2(k0, 2), GIFT_T3(k1, 3)) ^ rk[6]);
+  c.u3 = __builtin_amdgcn_readfirstlane(xor3(GIFT_T1(k0, 1), GIFT_T2(k1, 2), GIFT_T3(k2, 3)) ^ rk[7]);
+  c.in0 = u0 ^ GIFT_T3(bswap32(c0) ^ rk[3], 3);  // counter byte 15: fixed per lane
+  c.hi = ~(c0 >> 16);                            // forces a refresh on first use
+}
+
+// Round-2 output for counter ctr (state after rounds 1 and 2).
+__device__ __forceinline__ void ctr_rounds12(CtrCache& c, uint32_t ctr, uint32_t& x0, uint32_t& x1, uint32_t& x2,
+                                             uint32_t& x3, const uint32_t* rk, const uint8_t* tt, uint32_t L) {
+  const uint32_t s3 = bswap32(ctr) ^ rk[3];
+  if ((ctr >> 16) != c.hi) {  // rare and per lane
+    c.hi = ctr >> 16;
+    c.in2 = c.u2 ^ GIFT_T1(s3, 1);
+    c.in3 = c.u3 ^ GIFT_T0(s3, 0);
+    c.w0 = xor3(GIFT_T0(c.in0, 0), GIFT_T2(c.in2, 2), GIFT_T3(c.in3, 3)) ^ rk[8];
+    c.w1 = xor3(GIFT_T1(c.in2, 1), GIFT_T2(c.in3, 2), GIFT_T3(c.in0, 3)) ^ rk[9];
+    c.w2 = xor3(GIFT_T0(c.in2, 0), GIFT_T1(c.in3, 1), GIFT_T2(c.in0, 2)) ^ rk[10];
+    c.w3 = xor3(GIFT_T0(c.in3, 0), GIFT_T1(c.in0, 1), GIFT_T3(c.in2, 3)) ^ rk[11];
+  }
+  const uint32_t in1 = c.u1 ^ GIFT_T2(s3, 2);
+  x0 = c.w0 ^ GIFT_T1(in1, 1);
+  x1 = c.w1 ^ GIFT_T0(in1, 0);
+  x2 = c.w2 ^ GIFT_T3(in1, 3);
+  x3 = c.w3 ^ GIFT_T2(in1, 2);
+}
+
 // Y*M xor X with the 32 nibble tables of M in LDS: nibble q of Y (GCM bits
 // 4q..4q+3; q even = high nibble of byte q/2) selects entry q*256 + v*16.
+// 16 * (high nibble of byte k of w) and 16 * (low nibble of byte k of w),
+// one SDWA instruction each (byte select on the source; for the low nibble
+// the shifted byte is written to byte 0 of a zeroed result).
+__device__ __forceinline__ uint32_t nib_hi16(uint32_t w, int k) {
+  uint32_t r;
+  switch (k) {
+    case 0: asm("v_and_b32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_0 src1_sel:DWORD" : "=v"(r) : "v"(w), "v"(0xF0u)); break;
+    case 1: asm("v_and_b32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_1 src1_sel:DWORD" : "=v"(r) : "v"(w), "v"(0xF0u)); break;
+    case 2: asm("v_and_b32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_2 src1_sel:DWORD" : "=v"(r) : "v"(w), "v"(0xF0u)); break;
+    default: asm("v_and_b32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_3 src1_sel:DWORD" : "=v"(r) : "v"(w), "v"(0xF0u)); break;
+  }
+  return r;
+}
+__device__ __forceinline__ uint32_t nib_lo16(uint32_t w, int k) {
+  uint32_t r;
+  switch (k) {
+    case 0: asm("v_lshlrev_b32_sdwa %0, %1, %2 dst_sel:BYTE_0 dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_0" : "=v"(r) : "v"(4u), "v"(w)); break;
+    case 1: asm("v_lshlrev_b32_sdwa %0, %1, %2 dst_sel:BYTE_0 dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_1" : "=v"(r) : "v"(4u), "v"(w)); break;
+    case 2: asm("v_lshlrev_b32_sdwa %0, %1, %2 dst_sel:BYTE_0 dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_2" : "=v"(r) : "v"(4u), "v"(w)); break;
+    default: asm("v_lshlrev_b32_sdwa %0, %1, %2 dst_sel:BYTE_0 dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_3" : "=v"(r) : "v"(4u), "v"(w)); break;
+  }
+  return r;
+}
+
 __device__ __forceinline__ u128 ghash_step_lds(const u128& y, const u128& x, const uint8_t* gt) {
   uint32_t a0 = x.w[0], a1 = x.w[1], a2 = x.w[2], a3 = x.w[3];
 #pragma unroll
   for (int j = 0; j < 4; j++) {
+    // eight table reads per word of Y in flight, then an xor tree
     const uint32_t w = y.w[j];
+    uint4 e[8];
 #pragma unroll
     for (int k = 0; k < 4; k++) {
       const int q = 2 * (4 * j + k);
-      const uint32_t hi = (w >> (8 * k)) & 0xF0u;
-      const uint32_t lo = ((w >> (8 * k)) << 4) & 0xF0u;
-      const uint4 e = lds128(gt + q * 256, hi);
-      const uint4 f = lds128(gt + (q + 1) * 256, lo);
-      a0 = xor3(a0, e.x, f.x);
-      a1 = xor3(a1, e.y, f.y);
-      a2 = xor3(a2, e.z, f.z);
-      a3 = xor3(a3, e.w, f.w);
+      e[2 * k] = lds128(gt + q * 256, nib_hi16(w, k));
+      e[2 * k + 1] = lds128(gt + (q + 1) * 256, nib_lo16(w, k));
+    }
+    __builtin_amdgcn_sched_group_barrier(0x0002, 8, 1);  // addresses
+    __builtin_amdgcn_sched_group_barrier(0x0100, 8, 1);  // 8 LDS reads
+    __builtin_amdgcn_sched_group_barrier(0x0002, 16, 1); // xor3s
+#pragma unroll
+    for (int k = 0; k < 8; k += 2) {
+      a0 = xor3(a0, e[k].x, e[k + 1].x);
+      a1 = xor3(a1, e[k].y, e[k + 1].y);
+      a2 = xor3(a2, e[k].z, e[k + 1].z);
+      a3 = xor3(a3, e[k].w, e[k + 1].w);
     }
   }
   return u128{{a0, a1, a2, a3}};
@@ -172,7 +250,7 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
     uint32_t sh = 8u * tab;
     ((uint32_t*)tt)[w] = (v << sh) | (v >> ((32u - sh) & 31u));
   }
-  const uint32_t L = ((tid & 31u) << 2) | 0x10000u;
+  const uint32_t L = ((tid & 31u) << 2) | 0x10000u;  // this lane's table copy
   uint32_t cur_user = 0xFFFFFFFFu;
 
   const SegDesc* __restrict__ segs = a.segs;
@@ -222,27 +300,51 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
       __syncthreads();
     }
 
+    // Tile-uniform values live in SGPRs: the kernel also stores to global
+    // memory, so the compiler cannot prove these loads unclobbered and would
+    // otherwise keep all 60 round-key words in VGPRs.
     uint32_t rk[60];
     const uint32_t* rkp = a.kt.rk + (size_t)user * 64u;
 #pragma unroll
-    for (int i = 0; i < 60; i++) rk[i] = rkp[i];
-    const uint32_t k0 = sd->iv[0] ^ rk[0], k1 = sd->iv[1] ^ rk[1], k2 = sd->iv[2] ^ rk[2];
+    for (int i = 0; i < 60; i++) rk[i] = __builtin_amdgcn_readfirstlane(rkp[i]);
+    const uint32_t k0 = __builtin_amdgcn_readfirstlane(sd->iv[0]) ^ rk[0];
+    const uint32_t k1 = __builtin_amdgcn_readfirstlane(sd->iv[1]) ^ rk[1];
+    const uint32_t k2 = __builtin_amdgcn_readfirstlane(sd->iv[2]) ^ rk[2];
+
+    CtrCache cc;
+    const uint32_t c0 = 2u + (uint32_t)(base + (int64_t)tid);  // counter of this lane in row 0, mod 2^32
+    ctr_cache_init(cc, k0, k1, k2, c0, rk, tt, L);
+
+    // rows where every lane holds a whole block and the segment is 16-byte
+    // aligned take the branch-free path
+    const int r_full = base < 0 ? (int)(((uint64_t)(-base) + kThreads - 1) / kThreads) : 0;
+    const int r_end_full = (t == 0 && (len & 15u)) ? kRows - 1 : kRows;
+    const uintptr_t in_lane = (uintptr_t)a.in + off + 16 * (int64_t)(base + (int64_t)tid);
+    const uintptr_t out_lane = (uintptr_t)a.out + off + 16 * (int64_t)(base + (int64_t)tid);
 
     u128 y = u128_zero();
     for (int r = r_start; r < kRows; r++) {
-      const int64_t i0 = base + (int64_t)r * kThreads + tid;
-      u128 x = u128_zero();
-      if (i0 >= 0) {
-        uint32_t s0 = k0, s1 = k1, s2 = k2, s3 = bswap32(2u + (uint32_t)i0) ^ rk[3];
-        aes_rounds_lds(s0, s1, s2, s3, rk, tt, L);
-        const uint64_t boff = off + 16ull * (uint64_t)i0;
-        const uint64_t rem = len - 16ull * (uint64_t)i0;
-        const uint32_t n = rem >= 16 ? 16u : (uint32_t)rem;
-        const u128 in = load_block(a.in + boff, n, aligned);
-        u128 o = u128{{in.w[0] ^ s0, in.w[1] ^ s1, in.w[2] ^ s2, in.w[3] ^ s3}};
-        o = mask_block(o, n);
-        store_block(a.out + boff, o, n, aligned);
-        x = OPEN ? in : o;
+      uint32_t x0, x1, x2, x3;
+      ctr_rounds12(cc, c0 + (uint32_t)kThreads * (uint32_t)r, x0, x1, x2, x3, rk, tt, L);
+      aes_rounds_lds<3>(x0, x1, x2, x3, rk, tt, L);
+      u128 x;
+      if (aligned && r >= r_full && r < r_end_full) {
+        const uint4 v = *(const uint4*)(in_lane + (uintptr_t)r * (16u * kThreads));
+        const uint4 o = make_uint4(v.x ^ x0, v.y ^ x1, v.z ^ x2, v.w ^ x3);
+        *(uint4*)(out_lane + (uintptr_t)r * (16u * kThreads)) = o;
+        x = OPEN ? u128{{v.x, v.y, v.z, v.w}} : u128{{o.x, o.y, o.z, o.w}};
+      } else {
+        x = u128_zero();
+        const int64_t i0 = base + (int64_t)r * kThreads + tid;
+        if (i0 >= 0) {
+          const uint64_t boff = off + 16ull * (uint64_t)i0;
+          const uint64_t rem = len - 16ull * (uint64_t)i0;
+          const uint32_t n = rem >= 16 ? 16u : (uint32_t)rem;
+          const u128 in = load_block(a.in + boff, n, aligned);
+          const u128 o = mask_block(u128{{in.w[0] ^ x0, in.w[1] ^ x1, in.w[2] ^ x2, in.w[3] ^ x3}}, n);
+          store_block(a.out + boff, o, n, aligned);
+          x = OPEN ? in : o;
+        }
       }
       y = ghash_step_lds(y, x, gt);
     }
