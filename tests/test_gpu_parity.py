@@ -321,3 +321,96 @@ def test_llama3_70b_kv_in_place_fused_full_size():
     assert (host(ver2) == 0).all()
     assert torch.equal(d, ref)
     kt.destroy()
+
+
+# --------------------------------------------------------------------------
+# limits
+# --------------------------------------------------------------------------
+def test_segment_at_the_gcm_length_limit():
+    """One segment of exactly 2^32 - 2 blocks (64 GiB - 32 B): the last block
+    uses counter 2^32 - 1.  2^31 - 1 is prime, so the segment is 2 rows of
+    16 * (2^31 - 1) bytes."""
+    keys, nb = keyset(1)
+    kt = gift.KeyTable(keys)
+    rb = 16 * ((1 << 31) - 1)
+    n_rows = 2
+    total = n_rows * rb
+    d = torch.empty(total, dtype=torch.uint8, device=DEV)
+    g = torch.Generator(device=DEV)
+    g.manual_seed(7)
+    chunk = 1 << 30
+    for o in range(0, total, chunk):
+        n = min(chunk, total - o)
+        d[o:o + n] = torch.randint(0, 256, (n,), dtype=torch.uint8, device=DEV, generator=g)
+    ref = d.clone()
+    table = [(0, 2, 0, 123)]
+    tags = torch.zeros(16, dtype=torch.uint8, device=DEV)
+    ver = torch.full((1,), -1, dtype=torch.int32, device=DEV)
+    gift.seal(d, n_rows, rb, table, kt, nb, d, tags, verdicts=ver)
+    seg = oracle.as_segments(table)[0]
+    nblk = (1 << 32) - 2
+    picks = [0, 1, 2, 4095, 65535, 65536, 1 << 20, (1 << 31) - 2, (1 << 31) - 1, nblk - 65537, nblk - 3, nblk - 2,
+             nblk - 1] + [int(x) for x in rng.integers(0, nblk, 48)]
+    idx = torch.tensor([16 * j + k for j in picks for k in range(16)], dtype=torch.int64, device=DEV)
+    plain = host(ref[idx])
+    got = host(d[idx])
+    for n, j in enumerate(picks):
+        exp = expected_block(keys, nb, seg, j, plain[16 * n:16 * n + 16].tobytes())
+        assert got[16 * n:16 * n + 16].tobytes() == exp, j
+    gift.open(d, n_rows, rb, table, kt, nb, d, tags, ver)
+    assert host(ver)[0] == gift.SEG_OK
+    assert torch.equal(d, ref)
+    # a single flipped bit anywhere in the 64 GiB ciphertext fails the segment
+    gift.seal(d, n_rows, rb, table, kt, nb, d, tags, verdicts=ver)
+    d[total - 1] ^= 0x80
+    gift.open(d, n_rows, rb, table, kt, nb, d, tags, ver)
+    assert host(ver)[0] == gift.SEG_AUTH_FAIL
+    assert not d[total - (1 << 20):].any().item() and not d[:1 << 20].any().item()
+    del d, ref
+    torch.cuda.empty_cache()
+    kt.destroy()
+
+
+def test_one_block_over_the_limit_is_rejected(kt3):
+    keys, nb, kt = kt3
+    small = dev_u8(np.zeros(64, np.uint8))
+    tags = torch.zeros(16, dtype=torch.uint8, device=DEV)
+    # 2^32 - 1 blocks: never touched, rejected on the host
+    # (the library trusts the declared tensor size, so only calls that the
+    # host rejects may describe more bytes than the buffer holds)
+    s = status_of(gift.seal, small, 1, 16 * ((1 << 32) - 1), [(0, 1, 0, 0)], kt, nb, small, tags)
+    assert s == gift.E_TOO_LARGE
+    s = status_of(gift.seal, small, 3, 16 * ((1 << 31) - 1), [(0, 3, 0, 0)], kt, nb, small, tags)
+    assert s == gift.E_TOO_LARGE
+
+
+def test_many_segments_and_users():
+    """70,000 segments (descriptors larger than half the pinned ring) over
+    5,000 users, mixing one-block, small and tiled segments."""
+    n_users = 5000
+    keys = rng.integers(0, 256, (n_users, 32), dtype=np.uint8)
+    nb = rng.integers(0, 256, (n_users, 12), dtype=np.uint8)
+    kt = gift.KeyTable(keys)
+    rb = 48
+    sizes = rng.integers(1, 4, 70000)
+    sizes[::997] = 3000  # a few 144 KB segments -> tiled path with a ragged tile
+    table, r = [], 0
+    for i, n in enumerate(sizes):
+        table.append((r, int(n), int(rng.integers(0, n_users)), i))
+        r += int(n) + (i % 3 == 0)
+    n_rows = r
+    data = rng.integers(0, 256, n_rows * rb, dtype=np.uint8)
+    st, o_out, o_tags, _ = oracle.seal(data, n_rows, rb, table, keys, nb)
+    d = dev_u8(data)
+    out, tags, ver = seal(d, n_rows, rb, table, kt, nb)
+    assert host(out).tobytes() == o_out.tobytes()
+    assert host(tags)[:16 * len(table)].tobytes() == o_tags.tobytes()
+    back, ver2 = open_(out, n_rows, rb, table, kt, nb, tags)
+    assert (host(ver2) == 0).all()
+    covered = np.zeros(n_rows, bool)
+    for b, c, _, _ in table:
+        covered[b:b + c] = True
+    exp = data.reshape(n_rows, rb).copy()
+    exp[~covered] = 0
+    assert host(back).tobytes() == exp.tobytes()
+    kt.destroy()
