@@ -118,6 +118,35 @@ def cpu_baseline(w, t, plain_dev, seconds_target=15.0, threads=None):
     }
 
 
+def time_tokens(gift, W, torch, steps=50):
+    """Per-token encryption (GIFT Sec. 4.5) of one decode step's output
+    tokens: the decode_batch workload's 2588 tokens of 1024 users."""
+    import numpy as np
+    w = W.decode_batch()
+    t = w.tensors[1]
+    kt = gift.KeyTable(w.keys)
+    tok = torch.from_numpy(t.generate("cpu").numpy().view(np.int32).astype(np.int64)).cuda()
+    non = torch.from_numpy(W.u64s(w.seed, "token_nonce", t.n_rows).view(np.int64)).cuda()
+    out = torch.empty(16 * t.n_rows, dtype=torch.uint8, device="cuda")
+    back = torch.empty_like(tok)
+    for _ in range(3):
+        gift.token_encrypt(t.segs, tok, non, t.n_rows, kt, 128001, out)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        gift.token_encrypt(t.segs, tok, non, t.n_rows, kt, 128001, out)
+    torch.cuda.synchronize()
+    enc_us = (time.perf_counter() - t0) / steps * 1e6
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        gift.token_decrypt(t.segs, out, t.n_rows, kt, 128001, back)
+    torch.cuda.synchronize()
+    dec_us = (time.perf_counter() - t0) / steps * 1e6
+    assert torch.equal(back, tok)
+    kt.destroy()
+    return {"tokens": t.n_rows, "users": w.n_users, "encrypt_us": round(enc_us, 2), "decrypt_us": round(dec_us, 2)}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -264,6 +293,8 @@ def main():
                      "traffic": profiled_traffic(w.name) if labels is not None else None,
                      "kernel_ms": round(k_ms, 4), "alg_bytes_per_launch": alg_bytes},
     }
+    res["token_encryption"] = time_tokens(gift, W, torch)
+    log(f"[bench] token encryption: {res['token_encryption']}")
     if not args.no_cpu_baseline:
         log("[bench] cpu baseline (oracle) ...")
         res["cpu_baseline"] = cpu_baseline(w, t, data)  # data holds plaintext again here

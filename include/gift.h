@@ -106,9 +106,9 @@ typedef struct gift_key_table_s* gift_key_table;
 
 /*
  * Expands n_users AES-256 keys (host, n_users*32 bytes; user u's key at
- * keys + 32*u) into device-resident key material: the FIPS-197 key schedule,
- * the GHASH key H = E_K(0^128) and the per-user tables of powers of H the
- * kernels use.  The paper keeps user keys in the monitor's protected memory
+ * keys + 32*u) into device-resident key material: the FIPS-197 key schedule
+ * (and that of the equivalent inverse cipher), the GHASH key H = E_K(0^128)
+ * and the per-user tables of powers of H the kernels use.  The paper keeps user keys in the monitor's protected memory
  * (Sec. 3, step 0); here that memory is the GPU's.  The expansion runs on
  * `stream`; the table may be used by later work on that stream at once, and
  * on other streams after the caller has synchronised with it.  Host copies
@@ -170,6 +170,44 @@ gift_status gift_open(const gift_tensor* t, const gift_segment_table* st, gift_k
  */
 gift_status gift_check_owner(const gift_segment_table* st, const uint32_t* labels, uint64_t n_rows,
                              hipStream_t stream);
+
+/*
+ * Per-token encryption with obfuscation (GIFT Sec. 4.5, "Token
+ * encryption").  Tokens are encrypted one by one with a block cipher, not as
+ * one stream, so that the untrusted framework can still append tokens and
+ * split sequences; appending a random nonce keeps identical tokens from
+ * giving identical ciphertexts.  For token i owned by user u (segments index
+ * tokens: row r of a segment is token r):
+ *     out[i] = AES-256_Ku( LE64(tokens[i]) || LE64(nonces[i]) )   (16 bytes)
+ * and a token equal to eos_token is written as the reserved end-of-sequence
+ * ciphertext, sixteen 0xFF bytes, whatever the key, so the framework can
+ * recognise the end of generation.  Tokens covered by no segment give a zero
+ * block.
+ *   tokens, nonces  device, n_tokens u64 each; the nonces are the caller's
+ *                   random draws (the library draws no randomness).
+ *   out             device, n_tokens*16 bytes.
+ *   st              segments over token indices; iv_seq, row_labels and
+ *                   verdicts are not used; users must be < n_users.
+ * Errors: GIFT_E_INVALID, GIFT_E_RANGE, GIFT_E_OVERLAP as for gift_seal.
+ */
+gift_status gift_token_encrypt(const gift_segment_table* st, const uint64_t* tokens, const uint64_t* nonces,
+                               uint64_t n_tokens, gift_key_table kt, uint64_t eos_token, uint8_t* out,
+                               hipStream_t stream);
+
+/*
+ * Inverse of gift_token_encrypt: the reserved all-0xFF block gives
+ * eos_token (nonce 0); any other block gives the first 8 bytes of its AES-256
+ * decryption under the owner's key as the token and the last 8 as the nonce
+ * (the nonce is removed, Sec. 4.5).  A block cipher carries no
+ * authentication: a block decrypted under the wrong key yields an unrelated
+ * token, which the caller can range-check against its vocabulary.  Tokens
+ * covered by no segment give 0.
+ *   blocks      device, n_tokens*16 bytes.
+ *   tokens_out  device, n_tokens u64; nonces_out device, n_tokens u64, or NULL.
+ */
+gift_status gift_token_decrypt(const gift_segment_table* st, const uint8_t* blocks, uint64_t n_tokens,
+                               gift_key_table kt, uint64_t eos_token, uint64_t* tokens_out, uint64_t* nonces_out,
+                               hipStream_t stream);
 
 /*
  * Profiling hook for benchmark harnesses.  On the calling host thread, the

@@ -55,6 +55,10 @@ def lib():
         L.oracle_open.restype = ctypes.c_int
         L.oracle_check_owner.argtypes = [P, U32, P, U64, P]
         L.oracle_check_owner.restype = ctypes.c_int
+        L.oracle_token_encrypt.argtypes = [P, U32, U64, P, P, P, U32, U64, P]
+        L.oracle_token_encrypt.restype = ctypes.c_int
+        L.oracle_token_decrypt.argtypes = [P, U32, U64, P, P, U32, U64, P, P]
+        L.oracle_token_decrypt.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -206,3 +210,28 @@ def gctr(key, icb, data):
     y = np.zeros(max(x.size, 1), np.uint8)
     lib().oracle_gctr(_buf(w), _buf(cb), _buf(x) if x.size else None, x.size, _buf(y))
     return y[:x.size].tobytes()
+
+
+def token_encrypt(segs, tokens, nonces, keys, eos_token):
+    """GIFT Sec. 4.5 per-token encryption.  Returns (status, blocks[n, 16])."""
+    sg = as_segments(segs)
+    t = np.ascontiguousarray(tokens, np.uint64)
+    n = np.ascontiguousarray(nonces, np.uint64)
+    k = np.ascontiguousarray(keys, np.uint8).reshape(-1)
+    out = np.zeros((max(t.size, 1), 16), np.uint8)
+    st = lib().oracle_token_encrypt(_buf(sg) if len(sg) else None, len(sg), t.size, _buf(t), _buf(n), _buf(k),
+                                    k.size // 32, ctypes.c_uint64(eos_token), _buf(out))
+    return st, out[:t.size]
+
+
+def token_decrypt(segs, blocks, keys, eos_token):
+    """Returns (status, tokens[n], nonces[n])."""
+    sg = as_segments(segs)
+    b = np.ascontiguousarray(blocks, np.uint8).reshape(-1, 16)
+    k = np.ascontiguousarray(keys, np.uint8).reshape(-1)
+    nt = b.shape[0]
+    tok = np.zeros(max(nt, 1), np.uint64)
+    non = np.zeros(max(nt, 1), np.uint64)
+    st = lib().oracle_token_decrypt(_buf(sg) if len(sg) else None, len(sg), nt, _buf(b), _buf(k), k.size // 32,
+                                    ctypes.c_uint64(eos_token), _buf(tok), _buf(non))
+    return st, tok[:nt], non[:nt]

@@ -17,6 +17,9 @@
  *     multiply in GF(2^128)), Sec. 6.4 Algorithm 2 GHASH, Sec. 6.5 Algorithm 3
  *     GCTR, Sec. 7.1 Algorithm 4 GCM-AE, Sec. 7.2 Algorithm 5 GCM-AD), with a
  *     96-bit IV, a 128-bit tag and no additional authenticated data.
+ *   - Token encryption: the GIFT paper, Sec. 4.5 (a 64-bit token extended to
+ *     128 bits with a random nonce and enciphered as one block under the
+ *     owner's key; a special ciphertext marks the end of the sequence).
  *   - Segment semantics: the GIFT paper, Sec. 3 (system workflow, steps 3-6:
  *     per-owner keys; manipulated ownership metadata must yield only a
  *     decryption failure; every exported byte is encrypted under its owner's
@@ -100,6 +103,24 @@ int oracle_open(const uint8_t* data, uint64_t n_rows, uint64_t row_bytes, const 
 /* Owner check only: writes verdicts (OK / OWNER_MIXED). */
 int oracle_check_owner(const oracle_segment* segs, uint32_t n_segs, const uint32_t* labels,
                        uint64_t n_rows, int32_t* verdicts);
+
+/* ---- per-token encryption (GIFT Sec. 4.5) ----
+ * Token i (a row of a token buffer; segments index tokens) of user u:
+ *   block = LE64(tokens[i]) || LE64(nonces[i]);  out[i] = CIPH_Ku(block)
+ * except tokens[i] == eos_token, whose ciphertext is the reserved block of
+ * sixteen 0xFF bytes (for every key).  Tokens covered by no segment give a
+ * zero block.  Decryption inverts this: the reserved block gives eos_token
+ * (nonce 0); other blocks give the first 8 bytes of CIPH^-1 as the token and
+ * the last 8 as the nonce; uncovered tokens give 0.  Validation: INVALID,
+ * RANGE (rows, users) and OVERLAP as for the tensor entry points; iv_seq is
+ * unused. */
+#define ORACLE_EOS_BYTE 0xFF
+int oracle_token_encrypt(const oracle_segment* segs, uint32_t n_segs, uint64_t n_tokens, const uint64_t* tokens,
+                         const uint64_t* nonces, const uint8_t* keys, uint32_t n_users, uint64_t eos_token,
+                         uint8_t* out);
+int oracle_token_decrypt(const oracle_segment* segs, uint32_t n_segs, uint64_t n_tokens, const uint8_t* blocks,
+                         const uint8_t* keys, uint32_t n_users, uint64_t eos_token, uint64_t* tokens_out,
+                         uint64_t* nonces_out);
 
 #ifdef __cplusplus
 }

@@ -37,9 +37,10 @@ static int cmp_u64pair(const void* a, const void* b) {
   return 0;
 }
 
-/* Validation shared by the three entry points.  With check_keys == 0 (owner
- * check only, no key set and no cipher) the user range, the GCM length limit
- * and nonce reuse are not checked. */
+/* Validation shared by the entry points.  check_keys: 0 = owner check only
+ * (no key set, no cipher): user range, GCM length limit and nonce reuse are
+ * not checked; 1 = GCM entry points: all checks; 2 = per-token block cipher:
+ * user range only (no IV, no GCM length). */
 static int validate(uint64_t n_rows, uint64_t row_bytes, const oracle_segment* segs, uint32_t n_segs,
                     uint32_t n_users, int check_keys) {
   if (n_segs > 0 && segs == NULL) return ORACLE_E_INVALID;
@@ -51,7 +52,7 @@ static int validate(uint64_t n_rows, uint64_t row_bytes, const oracle_segment* s
     if (s->row_begin > n_rows || s->row_count > n_rows - s->row_begin) return ORACLE_E_RANGE;
     if (check_keys && s->user >= n_users) return ORACLE_E_RANGE;
     /* row_count * row_bytes without overflow, then the GCM length limit */
-    if (check_keys && s->row_count > MAX_SEG_BYTES / row_bytes) return ORACLE_E_TOO_LARGE;
+    if (check_keys == 1 && s->row_count > MAX_SEG_BYTES / row_bytes) return ORACLE_E_TOO_LARGE;
   }
   if (n_segs > 1) {
     uint64_t* v = (uint64_t*)malloc(sizeof(uint64_t) * 2 * n_segs);
@@ -66,7 +67,7 @@ static int validate(uint64_t n_rows, uint64_t row_bytes, const oracle_segment* s
         return ORACLE_E_OVERLAP;
       }
     }
-    if (check_keys) {
+    if (check_keys == 1) {
       for (uint32_t i = 0; i < n_segs; i++) {
         v[2 * i] = segs[i].user;
         v[2 * i + 1] = segs[i].iv_seq;
@@ -164,5 +165,69 @@ int oracle_check_owner(const oracle_segment* segs, uint32_t n_segs, const uint32
   if (st != ORACLE_OK) return st;
   for (uint32_t i = 0; i < n_segs; i++)
     verdicts[i] = segment_mixed(&segs[i], labels) ? ORACLE_SEG_OWNER_MIXED : ORACLE_SEG_OK;
+  return ORACLE_OK;
+}
+
+/* GIFT Sec. 4.5: token obfuscation -- token || random nonce through the block
+ * cipher under the owner's key; a special ciphertext for end-of-sequence. */
+int oracle_token_encrypt(const oracle_segment* segs, uint32_t n_segs, uint64_t n_tokens, const uint64_t* tokens,
+                         const uint64_t* nonces, const uint8_t* keys, uint32_t n_users, uint64_t eos_token,
+                         uint8_t* out) {
+  if ((n_tokens > 0 && (tokens == NULL || nonces == NULL || out == NULL)) || (n_segs > 0 && keys == NULL))
+    return ORACLE_E_INVALID;
+  int st = validate(n_tokens, 1, segs, n_segs, n_users, 2);
+  if (st != ORACLE_OK) return st;
+  memset(out, 0, 16 * (size_t)n_tokens);
+  for (uint32_t i = 0; i < n_segs; i++) {
+    uint8_t w[240];
+    oracle_aes256_key_expansion(keys + 32 * (size_t)segs[i].user, w);
+    for (uint64_t r = segs[i].row_begin; r < segs[i].row_begin + segs[i].row_count; r++) {
+      if (tokens[r] == eos_token) {
+        memset(out + 16 * r, ORACLE_EOS_BYTE, 16);
+        continue;
+      }
+      uint8_t blk[16];
+      for (int k = 0; k < 8; k++) {
+        blk[k] = (uint8_t)(tokens[r] >> (8 * k));
+        blk[8 + k] = (uint8_t)(nonces[r] >> (8 * k));
+      }
+      oracle_aes256_cipher(w, blk, out + 16 * r);
+    }
+  }
+  return ORACLE_OK;
+}
+
+int oracle_token_decrypt(const oracle_segment* segs, uint32_t n_segs, uint64_t n_tokens, const uint8_t* blocks,
+                         const uint8_t* keys, uint32_t n_users, uint64_t eos_token, uint64_t* tokens_out,
+                         uint64_t* nonces_out) {
+  if ((n_tokens > 0 && (blocks == NULL || tokens_out == NULL)) || (n_segs > 0 && keys == NULL))
+    return ORACLE_E_INVALID;
+  int st = validate(n_tokens, 1, segs, n_segs, n_users, 2);
+  if (st != ORACLE_OK) return st;
+  for (uint64_t r = 0; r < n_tokens; r++) {
+    tokens_out[r] = 0;
+    if (nonces_out) nonces_out[r] = 0;
+  }
+  for (uint32_t i = 0; i < n_segs; i++) {
+    uint8_t w[240];
+    oracle_aes256_key_expansion(keys + 32 * (size_t)segs[i].user, w);
+    for (uint64_t r = segs[i].row_begin; r < segs[i].row_begin + segs[i].row_count; r++) {
+      int eos = 1;
+      for (int k = 0; k < 16; k++) eos &= blocks[16 * r + k] == ORACLE_EOS_BYTE;
+      if (eos) {
+        tokens_out[r] = eos_token;
+        continue;
+      }
+      uint8_t p[16];
+      oracle_aes256_inv_cipher(w, blocks + 16 * r, p);
+      uint64_t t = 0, n = 0;
+      for (int k = 0; k < 8; k++) {
+        t |= (uint64_t)p[k] << (8 * k);
+        n |= (uint64_t)p[8 + k] << (8 * k);
+      }
+      tokens_out[r] = t;
+      if (nonces_out) nonces_out[r] = n;
+    }
+  }
   return ORACLE_OK;
 }

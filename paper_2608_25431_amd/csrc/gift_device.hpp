@@ -46,9 +46,13 @@ constexpr uint8_t sbox_of(uint8_t a) {
 
 struct AesConst {
   uint8_t sbox[256];
+  uint8_t inv_sbox[256];
   // Te0[x]: the MixColumns image of S(x) placed in row 0, as a little-endian
   // column word: bytes (2S, S, S, 3S).  Rows 1..3 are byte rotations.
   uint32_t te0[256];
+  // Td0[x]: the InvMixColumns image of S^-1(x) in row 0: bytes
+  // (0e, 09, 0d, 0b) * S^-1(x).  Rows 1..3 are byte rotations.
+  uint32_t td0[256];
 };
 
 constexpr AesConst make_aes_const() {
@@ -56,7 +60,13 @@ constexpr AesConst make_aes_const() {
   for (int x = 0; x < 256; x++) {
     uint8_t s = sbox_of((uint8_t)x);
     c.sbox[x] = s;
+    c.inv_sbox[s] = (uint8_t)x;
     c.te0[x] = (uint32_t)gmul(s, 2) | ((uint32_t)s << 8) | ((uint32_t)s << 16) | ((uint32_t)gmul(s, 3) << 24);
+  }
+  for (int x = 0; x < 256; x++) {
+    uint8_t v = c.inv_sbox[x];
+    c.td0[x] = (uint32_t)gmul(v, 0x0e) | ((uint32_t)gmul(v, 0x09) << 8) | ((uint32_t)gmul(v, 0x0d) << 16) |
+               ((uint32_t)gmul(v, 0x0b) << 24);
   }
   return c;
 }
@@ -117,6 +127,51 @@ __device__ inline void aes256_encrypt_words(const uint32_t* __restrict__ rk, con
   out[2] = (GIFT_SB(s2, 0) | GIFT_SB(s3, 1) | GIFT_SB(s0, 2) | GIFT_SB(s1, 3)) ^ rk[58];
   out[3] = (GIFT_SB(s3, 0) | GIFT_SB(s0, 1) | GIFT_SB(s1, 2) | GIFT_SB(s2, 3)) ^ rk[59];
 #undef GIFT_SB
+}
+
+// InvMixColumns of one column word (FIPS-197 Sec. 5.3.3), used to derive the
+// round keys of the equivalent inverse cipher (Sec. 5.3.5).
+__device__ inline uint32_t inv_mix_column(uint32_t w) {
+  const uint8_t a0 = w & 0xff, a1 = (w >> 8) & 0xff, a2 = (w >> 16) & 0xff, a3 = w >> 24;
+  const uint8_t b0 = gmul(a0, 0x0e) ^ gmul(a1, 0x0b) ^ gmul(a2, 0x0d) ^ gmul(a3, 0x09);
+  const uint8_t b1 = gmul(a0, 0x09) ^ gmul(a1, 0x0e) ^ gmul(a2, 0x0b) ^ gmul(a3, 0x0d);
+  const uint8_t b2 = gmul(a0, 0x0d) ^ gmul(a1, 0x09) ^ gmul(a2, 0x0e) ^ gmul(a3, 0x0b);
+  const uint8_t b3 = gmul(a0, 0x0b) ^ gmul(a1, 0x0d) ^ gmul(a2, 0x09) ^ gmul(a3, 0x0e);
+  return (uint32_t)b0 | ((uint32_t)b1 << 8) | ((uint32_t)b2 << 16) | ((uint32_t)b3 << 24);
+}
+
+// Round keys of the equivalent inverse cipher: dw[i] = w[i] for rounds 0 and
+// 14, InvMixColumns(w[i]) for rounds 1..13 (FIPS-197 Sec. 5.3.5).
+__device__ inline void aes256_dec_key_schedule(const uint32_t rk[60], uint32_t dk[60]) {
+  for (int i = 0; i < 60; i++) dk[i] = (i < 4 || i >= 56) ? rk[i] : inv_mix_column(rk[i]);
+}
+
+// One AES-256 block decryption with the equivalent inverse cipher: start
+// with round key 14, then for rounds 13..1 InvSubBytes + InvShiftRows +
+// InvMixColumns (the Td tables) + dw[round], finally InvSubBytes +
+// InvShiftRows + dw[0].  InvShiftRows takes row r of output column c from
+// input column c - r.
+__device__ inline void aes256_decrypt_words(const uint32_t* __restrict__ dk, const uint32_t in[4], uint32_t out[4],
+                                            const AesConst& C) {
+  uint32_t s0 = in[0] ^ dk[56], s1 = in[1] ^ dk[57], s2 = in[2] ^ dk[58], s3 = in[3] ^ dk[59];
+#define GIFT_TD(w, k) rotl32(C.td0[((w) >> (8 * (k))) & 0xff], 8 * (k))
+  for (int r = 13; r >= 1; r--) {
+    uint32_t t0 = GIFT_TD(s0, 0) ^ GIFT_TD(s3, 1) ^ GIFT_TD(s2, 2) ^ GIFT_TD(s1, 3) ^ dk[4 * r + 0];
+    uint32_t t1 = GIFT_TD(s1, 0) ^ GIFT_TD(s0, 1) ^ GIFT_TD(s3, 2) ^ GIFT_TD(s2, 3) ^ dk[4 * r + 1];
+    uint32_t t2 = GIFT_TD(s2, 0) ^ GIFT_TD(s1, 1) ^ GIFT_TD(s0, 2) ^ GIFT_TD(s3, 3) ^ dk[4 * r + 2];
+    uint32_t t3 = GIFT_TD(s3, 0) ^ GIFT_TD(s2, 1) ^ GIFT_TD(s1, 2) ^ GIFT_TD(s0, 3) ^ dk[4 * r + 3];
+    s0 = t0;
+    s1 = t1;
+    s2 = t2;
+    s3 = t3;
+  }
+#undef GIFT_TD
+#define GIFT_ISB(w, k) ((uint32_t)C.inv_sbox[((w) >> (8 * (k))) & 0xff] << (8 * (k)))
+  out[0] = (GIFT_ISB(s0, 0) | GIFT_ISB(s3, 1) | GIFT_ISB(s2, 2) | GIFT_ISB(s1, 3)) ^ dk[0];
+  out[1] = (GIFT_ISB(s1, 0) | GIFT_ISB(s0, 1) | GIFT_ISB(s3, 2) | GIFT_ISB(s2, 3)) ^ dk[1];
+  out[2] = (GIFT_ISB(s2, 0) | GIFT_ISB(s1, 1) | GIFT_ISB(s0, 2) | GIFT_ISB(s3, 3)) ^ dk[2];
+  out[3] = (GIFT_ISB(s3, 0) | GIFT_ISB(s2, 1) | GIFT_ISB(s1, 2) | GIFT_ISB(s0, 3)) ^ dk[3];
+#undef GIFT_ISB
 }
 
 // ---------------------------------------------------------------------------

@@ -158,11 +158,15 @@ struct Plan {
   uint32_t n_small = 0;
 };
 
+enum class Check { kOwner, kGcm, kBlock };
+
 // Checks segments in caller order (INVALID, RANGE, TOO_LARGE), then overlap,
-// then (user, iv_seq) reuse.  With keys == false (owner check) users are not
+// then (user, iv_seq) reuse.  kOwner (owner check): users are not
 // range-checked, the GCM length limit does not apply and iv_seq is unused.
+// kBlock (per-token block cipher): users are range-checked; there is no IV.
 gift_status check_segments(const gift_segment* segs, uint32_t n, uint64_t n_rows, uint64_t row_bytes,
-                           uint32_t n_users, bool keys) {
+                           uint32_t n_users, Check mode) {
+  const bool keys = mode != Check::kOwner, gcm = mode == Check::kGcm;
   for (uint32_t i = 0; i < n; i++) {
     const gift_segment& s = segs[i];
     if (s.row_count == 0 || s.reserved != 0)
@@ -174,7 +178,7 @@ gift_status check_segments(const gift_segment* segs, uint32_t n, uint64_t n_rows
                   (unsigned long long)s.row_begin, (unsigned long long)s.row_count, (unsigned long long)n_rows);
     if (keys && s.user >= n_users)
       return fail(GIFT_E_RANGE, "segment %u: user %u >= n_users %u", i, s.user, n_users);
-    if (keys && s.row_count > kMaxSegBytes / row_bytes)
+    if (gcm && s.row_count > kMaxSegBytes / row_bytes)
       return fail(GIFT_E_TOO_LARGE, "segment %u: longer than (2^32-2)*16 bytes", i);
   }
   if (n > 1) {
@@ -184,7 +188,7 @@ gift_status check_segments(const gift_segment* segs, uint32_t n, uint64_t n_rows
     for (uint32_t i = 1; i < n; i++)
       if (v[i].first < v[i - 1].first + v[i - 1].second)
         return fail(GIFT_E_OVERLAP, "segments overlap at row %llu", (unsigned long long)v[i].first);
-    if (keys) {
+    if (gcm) {
       for (uint32_t i = 0; i < n; i++) v[i] = {segs[i].user, segs[i].iv_seq};
       std::sort(v.begin(), v.end());
       for (uint32_t i = 1; i < n; i++)
@@ -266,7 +270,7 @@ gift_status run_gcm(const gift_tensor* t, const gift_segment_table* st, gift_key
     const uintptr_t a = (uintptr_t)t->data, b = (uintptr_t)out;
     if (a < b + total && b < a + total) return fail(GIFT_E_INVALID, "out partially overlaps data");
   }
-  gift_status sv = check_segments(st->segs, n, t->n_rows, t->row_bytes, kt->n_users, true);
+  gift_status sv = check_segments(st->segs, n, t->n_rows, t->row_bytes, kt->n_users, Check::kGcm);
   if (sv != GIFT_OK) return sv;
   if (total == 0) return GIFT_OK;
 
@@ -417,7 +421,8 @@ gift_status gift_key_table_create(const uint8_t* keys, uint32_t n_users, hipStre
   if (sv != GIFT_OK) return sv;
   const uint64_t u = n_users;
   const size_t o_rk = 0;
-  const size_t o_h = o_rk + align256(u * 64 * 4);
+  const size_t o_dk = o_rk + align256(u * 64 * 4);
+  const size_t o_h = o_dk + align256(u * 64 * 4);
   const size_t o_gt = o_h + align256(u * 16);
   const size_t o_ph = o_gt + align256(u * 512 * 16);
   const size_t o_pt = o_ph + align256(u * kHPowers * 16);
@@ -438,6 +443,7 @@ gift_status gift_key_table_create(const uint8_t* keys, uint32_t n_users, hipStre
   kt->mem = mem;
   kt->bytes = bytes;
   kt->dev.rk = (uint32_t*)(mem + o_rk);
+  kt->dev.dk = (uint32_t*)(mem + o_dk);
   kt->dev.h = (uint32_t*)(mem + o_h);
   kt->dev.gtab = (uint4*)(mem + o_gt);
   kt->dev.pow_h = (uint4*)(mem + o_ph);
@@ -494,7 +500,7 @@ gift_status gift_check_owner(const gift_segment_table* st, const uint32_t* label
   if (!st || !labels) return fail(GIFT_E_INVALID, "null segment table or labels");
   const uint32_t n = st->n_segs;
   if (n > 0 && (!st->segs || !st->verdicts)) return fail(GIFT_E_INVALID, "null segs or verdicts");
-  gift_status sv = check_segments(st->segs, n, n_rows, 1, 0, false);
+  gift_status sv = check_segments(st->segs, n, n_rows, 1, 0, Check::kOwner);
   if (sv != GIFT_OK) return sv;
   if (n == 0) return GIFT_OK;
   int dev;
@@ -512,6 +518,59 @@ gift_status gift_check_owner(const gift_segment_table* st, const uint32_t* label
   if (e != hipSuccess) return hip_fail(e, "check_owner");
   if (e2 != hipSuccess) return hip_fail(e2, "hipFreeAsync(descs)");
   return GIFT_OK;
+}
+
+// Per-token encryption (GIFT Sec. 4.5), both directions.
+static gift_status run_tokens(bool decrypt, const gift_segment_table* st, uint64_t n_tokens, gift_key_table kt,
+                              uint64_t eos_token, const uint64_t* tokens, const uint64_t* nonces,
+                              const uint8_t* blocks_in, uint8_t* blocks_out, uint64_t* tokens_out,
+                              uint64_t* nonces_out, hipStream_t stream) {
+  g_last_error.clear();
+  if (!st || !kt) return fail(GIFT_E_INVALID, "null segment table or key table");
+  const uint32_t n = st->n_segs;
+  if (n > 0 && !st->segs) return fail(GIFT_E_INVALID, "null segs");
+  if (n_tokens > 0 && (decrypt ? (!blocks_in || !tokens_out) : (!tokens || !nonces || !blocks_out)))
+    return fail(GIFT_E_INVALID, "null token buffers");
+  if (n_tokens > UINT64_MAX / 16) return fail(GIFT_E_INVALID, "token count overflows");
+  gift_status sv = check_segments(st->segs, n, n_tokens, 1, kt->n_users, Check::kBlock);
+  if (sv != GIFT_OK) return sv;
+  if (n_tokens == 0) return GIFT_OK;
+  int dev;
+  if ((sv = current_device(&dev)) != GIFT_OK) return sv;
+  if (dev != kt->device) return fail(GIFT_E_INVALID, "key table belongs to device %d, current is %d", kt->device, dev);
+  Plan P;
+  build_plan(st->segs, n, n_tokens, 1, nullptr, nullptr, nullptr, false, P);
+  SegDesc* d = nullptr;
+  hipError_t e = hipSuccess;
+  if (n > 0) {
+    e = hipMallocAsync((void**)&d, sizeof(SegDesc) * n, stream);
+    if (e != hipSuccess) return hip_fail(e, "hipMallocAsync(descs)");
+    Staging* sg = staging_for(dev);
+    e = sg ? sg->upload(d, P.descs.data(), sizeof(SegDesc) * n, stream) : hipErrorInvalidDevice;
+  }
+  // uncovered tokens: zero output
+  if (e == hipSuccess) e = decrypt ? launch_wipe(tokens_out, 8ull * n_tokens, stream) : launch_wipe(blocks_out, 16ull * n_tokens, stream);
+  if (e == hipSuccess && decrypt && nonces_out) e = launch_wipe(nonces_out, 8ull * n_tokens, stream);
+  if (e == hipSuccess)
+    e = launch_tokens(d, n, decrypt, tokens, nonces, blocks_in, blocks_out, tokens_out, nonces_out, eos_token, kt->dev,
+                      stream);
+  hipError_t e2 = d ? hipFreeAsync(d, stream) : hipSuccess;
+  if (e != hipSuccess) return hip_fail(e, "token kernels");
+  if (e2 != hipSuccess) return hip_fail(e2, "hipFreeAsync(descs)");
+  return GIFT_OK;
+}
+
+gift_status gift_token_encrypt(const gift_segment_table* st, const uint64_t* tokens, const uint64_t* nonces,
+                               uint64_t n_tokens, gift_key_table kt, uint64_t eos_token, uint8_t* out,
+                               hipStream_t stream) {
+  return run_tokens(false, st, n_tokens, kt, eos_token, tokens, nonces, nullptr, out, nullptr, nullptr, stream);
+}
+
+gift_status gift_token_decrypt(const gift_segment_table* st, const uint8_t* blocks, uint64_t n_tokens,
+                               gift_key_table kt, uint64_t eos_token, uint64_t* tokens_out, uint64_t* nonces_out,
+                               hipStream_t stream) {
+  return run_tokens(true, st, n_tokens, kt, eos_token, nullptr, nullptr, blocks, nullptr, tokens_out, nonces_out,
+                    stream);
 }
 
 }  // extern "C"

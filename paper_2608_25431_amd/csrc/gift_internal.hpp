@@ -53,6 +53,7 @@ static_assert(sizeof(ZeroRange) == 32, "ZeroRange layout");
 // Per-user key material in device memory, one allocation.
 struct KeyTableDev {
   uint32_t* rk;      // [n_users][64] round-key words (60 used)
+  uint32_t* dk;      // [n_users][64] equivalent-inverse-cipher round keys (60 used)
   uint32_t* h;       // [n_users][4]  H = E_K(0^128)
   uint4* gtab;       // [n_users][32][16] 4-bit GHASH tables of M = H^kThreads
   uint4* pow_h;      // [n_users][kHPowers] H^k
@@ -90,5 +91,10 @@ hipError_t launch_gcm_finalize(const GcmArgs& a, bool open, hipStream_t s);
 hipError_t launch_zero_ranges(uint8_t* out, const ZeroRange* r, uint32_t n, const int32_t* verdicts, uint32_t grid,
                               hipStream_t s);
 hipError_t launch_wipe(void* p, size_t bytes, hipStream_t s);
+// Per-token block encryption (decrypt == true: the inverse).  Rows of the
+// descriptors are token indices.
+hipError_t launch_tokens(const SegDesc* segs, uint32_t n_segs, bool decrypt, const uint64_t* tokens,
+                         const uint64_t* nonces, const uint8_t* blocks_in, uint8_t* blocks_out, uint64_t* tokens_out,
+                         uint64_t* nonces_out, uint64_t eos_token, KeyTableDev kt, hipStream_t s);
 
 }  // namespace gift

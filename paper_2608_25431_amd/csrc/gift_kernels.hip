@@ -558,6 +558,53 @@ __global__ __launch_bounds__(256) void k_wipe(uint8_t* p, size_t bytes) {
 }
 
 // ---------------------------------------------------------------------------
+// Per-token encryption (token || nonce as one block under the owner's key,
+// the end-of-sequence token as the all-0xFF block).  One workgroup per
+// segment; outputs of uncovered tokens were zeroed before this launch.
+// ---------------------------------------------------------------------------
+template <bool DECRYPT>
+__global__ __launch_bounds__(64) void k_tokens(const SegDesc* __restrict__ segs, uint32_t n_segs,
+                                               const uint64_t* __restrict__ tokens,
+                                               const uint64_t* __restrict__ nonces,
+                                               const uint8_t* __restrict__ blocks_in, uint8_t* __restrict__ blocks_out,
+                                               uint64_t* __restrict__ tokens_out, uint64_t* __restrict__ nonces_out,
+                                               uint64_t eos_token, KeyTableDev kt) {
+  for (uint32_t s = blockIdx.x; s < n_segs; s += gridDim.x) {
+    const uint64_t rb = segs[s].row_begin, rc = segs[s].row_count;
+    const uint32_t user = segs[s].user;
+    for (uint64_t i = threadIdx.x; i < rc; i += blockDim.x) {
+      const uint64_t r = rb + i;
+      if (!DECRYPT) {
+        const uint64_t t = tokens[r], n = nonces[r];
+        uint32_t o[4];
+        if (t == eos_token) {
+          o[0] = o[1] = o[2] = o[3] = 0xFFFFFFFFu;
+        } else {
+          const uint32_t blk[4] = {(uint32_t)t, (uint32_t)(t >> 32), (uint32_t)n, (uint32_t)(n >> 32)};
+          aes256_encrypt_words(kt.rk + 64ull * user, blk, o, c_aes);
+        }
+        *(uint4*)(blocks_out + 16ull * r) = make_uint4(o[0], o[1], o[2], o[3]);
+      } else {
+        const uint4 b = *(const uint4*)(blocks_in + 16ull * r);
+        uint64_t t, n;
+        if ((b.x & b.y & b.z & b.w) == 0xFFFFFFFFu) {
+          t = eos_token;
+          n = 0;
+        } else {
+          const uint32_t blk[4] = {b.x, b.y, b.z, b.w};
+          uint32_t p[4];
+          aes256_decrypt_words(kt.dk + 64ull * user, blk, p, c_aes);
+          t = (uint64_t)p[0] | ((uint64_t)p[1] << 32);
+          n = (uint64_t)p[2] | ((uint64_t)p[3] << 32);
+        }
+        tokens_out[r] = t;
+        if (nonces_out) nonces_out[r] = n;
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Key-table setup.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(64) void k_key_sched(const uint8_t* __restrict__ keys, KeyTableDev kt) {
@@ -567,6 +614,10 @@ __global__ __launch_bounds__(64) void k_key_sched(const uint8_t* __restrict__ ke
   aes256_key_schedule(keys + 32ull * u, rk, c_aes);
   for (int i = 0; i < 60; i++) kt.rk[64ull * u + i] = rk[i];
   for (int i = 60; i < 64; i++) kt.rk[64ull * u + i] = 0u;
+  uint32_t dk[60];
+  aes256_dec_key_schedule(rk, dk);
+  for (int i = 0; i < 60; i++) kt.dk[64ull * u + i] = dk[i];
+  for (int i = 60; i < 64; i++) kt.dk[64ull * u + i] = 0u;
   const uint32_t zero[4] = {0u, 0u, 0u, 0u};
   uint32_t h[4];
   aes256_encrypt_words(rk, zero, h, c_aes);
@@ -673,6 +724,20 @@ hipError_t launch_zero_ranges(uint8_t* out, const ZeroRange* r, uint32_t n, cons
                               hipStream_t s) {
   if (n == 0) return hipSuccess;
   hipLaunchKernelGGL(k_zero_ranges, dim3(grid), dim3(256), 0, s, out, r, n, verdicts);
+  return hipGetLastError();
+}
+
+hipError_t launch_tokens(const SegDesc* segs, uint32_t n_segs, bool decrypt, const uint64_t* tokens,
+                         const uint64_t* nonces, const uint8_t* blocks_in, uint8_t* blocks_out, uint64_t* tokens_out,
+                         uint64_t* nonces_out, uint64_t eos_token, KeyTableDev kt, hipStream_t s) {
+  if (n_segs == 0) return hipSuccess;
+  const uint32_t grid = n_segs < 65535u ? n_segs : 65535u;
+  if (decrypt)
+    hipLaunchKernelGGL(k_tokens<true>, dim3(grid), dim3(64), 0, s, segs, n_segs, tokens, nonces, blocks_in,
+                       blocks_out, tokens_out, nonces_out, eos_token, kt);
+  else
+    hipLaunchKernelGGL(k_tokens<false>, dim3(grid), dim3(64), 0, s, segs, n_segs, tokens, nonces, blocks_in,
+                       blocks_out, tokens_out, nonces_out, eos_token, kt);
   return hipGetLastError();
 }
 

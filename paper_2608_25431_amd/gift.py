@@ -46,7 +46,8 @@ class _SegTable(ctypes.Structure):
 assert ctypes.sizeof(_Segment) == SEGMENT_DTYPE.itemsize == 32
 
 EXPORTS = ("gift_key_table_create", "gift_key_table_users", "gift_key_table_destroy", "gift_seal", "gift_open",
-           "gift_check_owner", "gift_profile_next_call", "gift_status_string", "gift_last_error")
+           "gift_check_owner", "gift_token_encrypt", "gift_token_decrypt", "gift_profile_next_call",
+           "gift_status_string", "gift_last_error")
 
 _lib = None
 
@@ -72,6 +73,10 @@ def lib():
         L.gift_open.restype = st
         L.gift_check_owner.argtypes = [ctypes.POINTER(_SegTable), P, ctypes.c_uint64, P]
         L.gift_check_owner.restype = st
+        L.gift_token_encrypt.argtypes = [ctypes.POINTER(_SegTable), P, P, ctypes.c_uint64, P, ctypes.c_uint64, P, P]
+        L.gift_token_encrypt.restype = st
+        L.gift_token_decrypt.argtypes = [ctypes.POINTER(_SegTable), P, ctypes.c_uint64, P, ctypes.c_uint64, P, P, P]
+        L.gift_token_decrypt.restype = st
         L.gift_profile_next_call.argtypes = [P, P]
         L.gift_profile_next_call.restype = st
         L.gift_status_string.argtypes = [st]
@@ -214,6 +219,22 @@ def check_owner(segs, labels, n_rows, verdicts, stream=None):
     """gift_check_owner."""
     tab, keep = _table(segs, None, verdicts)
     _check(lib().gift_check_owner(ctypes.byref(tab), _ptr(labels), n_rows, _stream(stream)))
+    del keep
+
+
+def token_encrypt(segs, tokens, nonces, n_tokens, kt, eos_token, out, stream=None):
+    """gift_token_encrypt: tokens/nonces device u64[n_tokens], out device u8[n_tokens*16]."""
+    tab, keep = _table(segs, None, None)
+    _check(lib().gift_token_encrypt(ctypes.byref(tab), _ptr(tokens), _ptr(nonces), n_tokens, kt.handle, eos_token,
+                                    _ptr(out), _stream(stream)))
+    del keep
+
+
+def token_decrypt(segs, blocks, n_tokens, kt, eos_token, tokens_out, nonces_out=None, stream=None):
+    """gift_token_decrypt."""
+    tab, keep = _table(segs, None, None)
+    _check(lib().gift_token_decrypt(ctypes.byref(tab), _ptr(blocks), n_tokens, kt.handle, eos_token, _ptr(tokens_out),
+                                    _ptr(nonces_out), _stream(stream)))
     del keep
 
 

@@ -414,3 +414,55 @@ def test_many_segments_and_users():
     exp[~covered] = 0
     assert host(back).tobytes() == exp.tobytes()
     kt.destroy()
+
+
+# --------------------------------------------------------------------------
+# per-token encryption (GIFT Sec. 4.5)
+# --------------------------------------------------------------------------
+def dev_u64(a):
+    return torch.from_numpy(np.ascontiguousarray(a, np.uint64).view(np.int64).copy()).to(DEV)
+
+
+def host_u64(t):
+    return host(t).view(np.uint64)
+
+
+def token_case(keys, kt, segs, tok, non, eos):
+    n = tok.size
+    st, o_blocks = oracle.token_encrypt(segs, tok, non, keys, eos)
+    assert st == 0
+    out = torch.full((max(n, 1) * 16,), 0x5A, dtype=torch.uint8, device=DEV)
+    gift.token_encrypt(segs, dev_u64(tok), dev_u64(non), n, kt, eos, out)
+    assert host(out)[:16 * n].tobytes() == o_blocks.tobytes()
+    st, o_tok, o_non = oracle.token_decrypt(segs, o_blocks, keys, eos)
+    t_out = torch.full((max(n, 1),), 77, dtype=torch.int64, device=DEV)
+    n_out = torch.full((max(n, 1),), 77, dtype=torch.int64, device=DEV)
+    gift.token_decrypt(segs, out, n, kt, eos, t_out, n_out)
+    assert (host_u64(t_out)[:n] == o_tok).all() and (host_u64(n_out)[:n] == o_non).all()
+
+
+def test_token_encryption_matches_oracle():
+    w = W.decode_batch()
+    t = w.tensors[1]  # int32 token buffer with the decode batch's ownership
+    kt = gift.KeyTable(w.keys)
+    tok = t.generate("cpu").numpy().view(np.int32).astype(np.uint64)
+    eos = 128001
+    tok[::97] = eos
+    non = W.u64s(w.seed, "token_nonce", tok.size)
+    token_case(w.keys, kt, t.segs, tok, non, eos)
+    # gaps, EOS everywhere, a single token, a user appearing twice, no segments
+    token_case(w.keys, kt, [(1, 3, 5, 0), (7, 2, 5, 1)], tok[:12], non[:12], eos)
+    token_case(w.keys, kt, [(0, 12, 3, 0)], np.full(12, eos, np.uint64), non[:12], eos)
+    token_case(w.keys, kt, [(0, 1, 1023, 0)], tok[:1], non[:1], eos)
+    token_case(w.keys, kt, [], tok[:5], non[:5], eos)
+    # 100k tokens of one user (many rows per workgroup)
+    big = W.u64s(1, "big_tok", 100000) % np.uint64(128256)
+    token_case(w.keys, kt, [(0, 100000, 7, 0)], big, W.u64s(1, "big_non", 100000), eos)
+    # validation agrees with the oracle
+    dt, dn = dev_u64(tok[:8]), dev_u64(non[:8])
+    out = torch.zeros(128, dtype=torch.uint8, device=DEV)
+    for segs in ([(0, 0, 0, 0)], [(7, 2, 0, 0)], [(0, 2, 1024, 0)], [(0, 2, 0, 0), (1, 2, 1, 0)],
+                 [(0, 2, 0, 7), (2, 2, 0, 7)]):
+        st_o = oracle.token_encrypt(segs, tok[:8], non[:8], w.keys, eos)[0]
+        assert status_of(gift.token_encrypt, segs, dt, dn, 8, kt, eos, out) == st_o, segs
+    kt.destroy()
