@@ -172,6 +172,72 @@ gift_status gift_check_owner(const gift_segment_table* st, const uint32_t* label
                              hipStream_t stream);
 
 /*
+ * Paged KV cache (GIFT Sec. 4.2: PagedAttention splits the cache into KV
+ * blocks and ownership is recorded per block; Sec. 4.5: the monitor keeps
+ * the block tables in its own memory).  The cache is one device allocation;
+ * the chunk of (layer l, block id b, part p) -- p selects K/V planes when they
+ * are stored apart -- is the chunk_bytes bytes at
+ *     base + l*layer_stride + b*block_stride + p*part_stride.
+ * Requirements (else GIFT_E_INVALID): base 16-byte aligned; chunk_bytes a
+ * power of two >= 16; strides multiples of 16; n_layers, n_parts, n_blocks
+ * >= 1; and the three strided dimensions do not overlap: sorted by stride,
+ * each stride is at least the extent of everything inside it (the chunk,
+ * then each smaller dimension times its count).  cache_bytes bounds every
+ * chunk the call touches (GIFT_E_RANGE).
+ */
+typedef struct {
+  void* base; /* device */
+  uint64_t cache_bytes;
+  uint64_t layer_stride, block_stride, part_stride; /* bytes */
+  uint64_t chunk_bytes;
+  uint32_t n_layers, n_parts;
+  uint64_t n_blocks; /* block ids are < n_blocks */
+} gift_paged_kv;
+
+/* One request's KV: its block table (host, in sequence order) and owner.
+ * Its sealed stream is the chunks in the order: for each block of the table,
+ * for each layer, for each part -- one GCM message under the user's key and
+ * IV nonce_base[user] XOR (0^32 || BE64(iv_seq)). */
+typedef struct {
+  const uint32_t* block_ids; /* host */
+  uint32_t n_block_ids;      /* >= 1 */
+  uint32_t user;
+  uint64_t iv_seq;
+} gift_request;
+
+/*
+ * Seal requests straight out of a paged cache into a contiguous export
+ * buffer (KV handoff or swap-out): request i's ciphertext is written at
+ * out + sum_{j<i} len_j, len_j = n_block_ids_j * n_layers * n_parts *
+ * chunk_bytes, in caller order; tags[i] is its tag.
+ *   block_labels  device, n_blocks u32, or NULL: when given, a request whose
+ *                 table holds a block labelled with anyone else (including
+ *                 the sentinels) is rejected -- zero ciphertext and tag,
+ *                 verdict OWNER_MIXED (Sec. 4.3 rule step 5; this is the
+ *                 check that stops a manipulated block table from exporting
+ *                 another user's KV under the wrong key, Sec. 2.2).
+ *   verdicts      device, n_reqs int32, or NULL.
+ *   out           device; must not overlap the cache allocation.
+ * A block id may appear only once in the whole call (GIFT_E_OVERLAP).
+ */
+gift_status gift_seal_paged(const gift_paged_kv* kv, const gift_request* reqs, uint32_t n_reqs,
+                            const uint32_t* block_labels, gift_key_table kt, const uint8_t* nonce_base, void* out,
+                            uint8_t* tags, int32_t* verdicts, hipStream_t stream);
+
+/*
+ * Open a contiguous sealed buffer (laid out as gift_seal_paged writes it)
+ * into the paged cache: request i's plaintext is scattered into the chunks
+ * of its block table (which may differ from the blocks it was sealed from,
+ * e.g. on swap-in).  A request that fails authentication (AUTH_FAIL) or the
+ * label check (OWNER_MIXED) has every chunk of its table zeroed.
+ *   in        device, the sealed buffer; must not overlap the cache.
+ *   tags      device, n_reqs*16 bytes.  verdicts: device, required.
+ */
+gift_status gift_open_paged(const gift_paged_kv* kv, const gift_request* reqs, uint32_t n_reqs,
+                            const uint32_t* block_labels, gift_key_table kt, const uint8_t* nonce_base,
+                            const void* in, const uint8_t* tags, int32_t* verdicts, hipStream_t stream);
+
+/*
  * Per-token encryption with obfuscation (GIFT Sec. 4.5, "Token
  * encryption").  Tokens are encrypted one by one with a block cipher, not as
  * one stream, so that the untrusted framework can still append tokens and
@@ -211,7 +277,8 @@ gift_status gift_token_decrypt(const gift_segment_table* st, const uint8_t* bloc
 
 /*
  * Profiling hook for benchmark harnesses.  On the calling host thread, the
- * next gift_seal or gift_open that launches the per-block kernel records
+ * next gift_seal, gift_open, gift_seal_paged or gift_open_paged that
+ * launches the per-block kernel records
  * `before` on its stream immediately before that launch and `after`
  * immediately after it, so hipEventElapsedTime(before, after) is that
  * kernel's duration; the hook is then cleared.  Both events must have been

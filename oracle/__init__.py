@@ -55,6 +55,10 @@ def lib():
         L.oracle_open.restype = ctypes.c_int
         L.oracle_check_owner.argtypes = [P, U32, P, U64, P]
         L.oracle_check_owner.restype = ctypes.c_int
+        L.oracle_seal_paged.argtypes = [P, P, P, U32, P, P, U32, P, P, P, P]
+        L.oracle_seal_paged.restype = ctypes.c_int
+        L.oracle_open_paged.argtypes = [P, P, P, U32, P, P, U32, P, P, P, P]
+        L.oracle_open_paged.restype = ctypes.c_int
         L.oracle_token_encrypt.argtypes = [P, U32, U64, P, P, P, U32, U64, P]
         L.oracle_token_encrypt.restype = ctypes.c_int
         L.oracle_token_decrypt.argtypes = [P, U32, U64, P, P, U32, U64, P, P]
@@ -235,3 +239,58 @@ def token_decrypt(segs, blocks, keys, eos_token):
     st = lib().oracle_token_decrypt(_buf(sg) if len(sg) else None, len(sg), nt, _buf(b), _buf(k), k.size // 32,
                                     ctypes.c_uint64(eos_token), _buf(tok), _buf(non))
     return st, tok[:nt], non[:nt]
+
+
+class PagedKV(ctypes.Structure):
+    _fields_ = [("cache_bytes", ctypes.c_uint64), ("layer_stride", ctypes.c_uint64),
+                ("block_stride", ctypes.c_uint64), ("part_stride", ctypes.c_uint64),
+                ("chunk_bytes", ctypes.c_uint64), ("n_layers", ctypes.c_uint32), ("n_parts", ctypes.c_uint32),
+                ("n_blocks", ctypes.c_uint64)]
+
+
+class _Request(ctypes.Structure):
+    _fields_ = [("block_ids", ctypes.c_void_p), ("n_block_ids", ctypes.c_uint32), ("user", ctypes.c_uint32),
+                ("iv_seq", ctypes.c_uint64)]
+
+
+def _requests(reqs):
+    """reqs: list of (block_ids, user, iv_seq); returns (ctypes array, keep-alive list)."""
+    keep = [np.ascontiguousarray(b, np.uint32) for b, _, _ in reqs]
+    arr = (_Request * max(len(reqs), 1))()
+    for i, ((_, u, q), b) in enumerate(zip(reqs, keep)):
+        arr[i] = _Request(b.ctypes.data if b.size else None, b.size, u, q)
+    return arr, keep
+
+
+def seal_paged(cache, geom, reqs, keys, nonce_base, labels=None):
+    """cache: host uint8 array of geom.cache_bytes; geom: PagedKV; reqs: list of
+    (block_ids, user, iv_seq).  Returns (status, out, tags[n,16], verdicts[n])."""
+    c = np.ascontiguousarray(cache, np.uint8).reshape(-1)
+    arr, keep = _requests(reqs)
+    per = geom.n_layers * geom.n_parts * geom.chunk_bytes
+    total = sum(per * len(b) for b in keep)
+    out = np.zeros(max(total, 1), np.uint8)
+    tags = np.zeros((max(len(reqs), 1), 16), np.uint8)
+    ver = np.full(max(len(reqs), 1), -99, np.int32)
+    lab = None if labels is None else np.ascontiguousarray(labels, np.uint32)
+    k = np.ascontiguousarray(keys, np.uint8).reshape(-1)
+    nb = np.ascontiguousarray(nonce_base, np.uint8).reshape(-1)
+    st = lib().oracle_seal_paged(_buf(c), ctypes.byref(geom), ctypes.addressof(arr), len(reqs), _buf(lab), _buf(k),
+                                 k.size // 32, _buf(nb), _buf(out), _buf(tags), _buf(ver))
+    return st, out[:total], tags[:len(reqs)], ver[:len(reqs)]
+
+
+def open_paged(cache, geom, reqs, keys, nonce_base, sealed, tags, labels=None):
+    """Opens into a copy of cache; returns (status, cache_after, verdicts[n])."""
+    c = np.array(cache, np.uint8).reshape(-1)
+    arr, keep = _requests(reqs)
+    s_ = np.ascontiguousarray(sealed, np.uint8).reshape(-1)
+    t = np.ascontiguousarray(tags, np.uint8).reshape(-1)
+    ver = np.full(max(len(reqs), 1), -99, np.int32)
+    lab = None if labels is None else np.ascontiguousarray(labels, np.uint32)
+    k = np.ascontiguousarray(keys, np.uint8).reshape(-1)
+    nb = np.ascontiguousarray(nonce_base, np.uint8).reshape(-1)
+    st = lib().oracle_open_paged(_buf(c), ctypes.byref(geom), ctypes.addressof(arr), len(reqs), _buf(lab), _buf(k),
+                                 k.size // 32, _buf(nb), _buf(s_) if s_.size else None, _buf(t) if t.size else None,
+                                 _buf(ver))
+    return st, c, ver[:len(reqs)]

@@ -6,7 +6,7 @@ import os
 import subprocess
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-SOURCES = ["aes256.c", "gcm.c", "segments.c"]
+SOURCES = ["aes256.c", "gcm.c", "segments.c", "paged.c"]
 LIB = os.path.join(HERE, "liboracle.so")
 
 

@@ -104,6 +104,43 @@ int oracle_open(const uint8_t* data, uint64_t n_rows, uint64_t row_bytes, const 
 int oracle_check_owner(const oracle_segment* segs, uint32_t n_segs, const uint32_t* labels,
                        uint64_t n_rows, int32_t* verdicts);
 
+/* ---- paged KV cache (GIFT Sec. 4.2 KV blocks, Sec. 4.5 index tables) ----
+ * cache: host copy of the cache allocation (cache_bytes bytes).  Chunk
+ * (layer l, block b, part p) = cache[l*ls + b*bs + p*ps, + chunk_bytes).
+ * A request's stream is its chunks for each block of its table, each layer,
+ * each part, in that order; it is one GCM message.  Seal writes request i's
+ * ciphertext at out + (sum of earlier requests' lengths).  With
+ * block_labels, a request holding a block labelled with anyone else is
+ * rejected (zero ciphertext and tag on seal; on open its chunks are zeroed).
+ * Open scatters verified plaintext into the table's chunks and zeroes the
+ * chunks of failed requests.
+ * Validation: geometry (INVALID: chunk a power of two >= 16, strides multiples
+ * of 16, counts >= 1, strided dimensions that do not overlap), then per
+ * request in order: INVALID (empty table, sentinel user), RANGE (block id,
+ * user, chunk beyond cache_bytes), TOO_LARGE; then OVERLAP (a block id twice
+ * in the call); then NONCE_REUSE. */
+typedef struct {
+  uint64_t cache_bytes;
+  uint64_t layer_stride, block_stride, part_stride;
+  uint64_t chunk_bytes;
+  uint32_t n_layers, n_parts;
+  uint64_t n_blocks;
+} oracle_paged_kv;
+
+typedef struct {
+  const uint32_t* block_ids;
+  uint32_t n_block_ids;
+  uint32_t user;
+  uint64_t iv_seq;
+} oracle_request;
+
+int oracle_seal_paged(const uint8_t* cache, const oracle_paged_kv* kv, const oracle_request* reqs, uint32_t n_reqs,
+                      const uint32_t* block_labels, const uint8_t* keys, uint32_t n_users, const uint8_t* nonce_base,
+                      uint8_t* out, uint8_t* tags, int32_t* verdicts);
+int oracle_open_paged(uint8_t* cache, const oracle_paged_kv* kv, const oracle_request* reqs, uint32_t n_reqs,
+                      const uint32_t* block_labels, const uint8_t* keys, uint32_t n_users, const uint8_t* nonce_base,
+                      const uint8_t* in, const uint8_t* tags, int32_t* verdicts);
+
 /* ---- per-token encryption (GIFT Sec. 4.5) ----
  * Token i (a row of a token buffer; segments index tokens) of user u:
  *   block = LE64(tokens[i]) || LE64(nonces[i]);  out[i] = CIPH_Ku(block)

@@ -316,7 +316,7 @@ gift_status run_gcm(const gift_tensor* t, const gift_segment_table* st, gift_key
   do {
     if (n > 0) {
       if (st->row_labels) {
-        e = launch_check_owner(d_desc, n, st->row_labels, verdicts, stream);
+        e = launch_check_owner(d_desc, n, st->row_labels, nullptr, verdicts, stream);
         if (e != hipSuccess) {
           rs = hip_fail(e, "check_owner launch");
           break;
@@ -331,6 +331,9 @@ gift_status run_gcm(const gift_tensor* t, const gift_segment_table* st, gift_key
       GcmArgs a;
       a.in = (const uint8_t*)t->data;
       a.out = (uint8_t*)out;
+      a.chunk_off = nullptr;
+      a.pbase = nullptr;
+      a.chunk_shift = 0;
       a.segs = d_desc;
       a.n_segs = n;
       a.tile_base = (const uint32_t*)(scratch + o_tb);
@@ -349,7 +352,7 @@ gift_status run_gcm(const gift_tensor* t, const gift_segment_table* st, gift_key
           break;
         }
       }
-      e = launch_gcm_tiles(a, OPEN, (uint32_t)device_cus(dev), stream);
+      e = launch_gcm_tiles(a, OPEN ? kModeOpen : 0, (uint32_t)device_cus(dev), stream);
       if (e != hipSuccess) {
         rs = hip_fail(e, "gcm launch");
         break;
@@ -382,9 +385,236 @@ gift_status run_gcm(const gift_tensor* t, const gift_segment_table* st, gift_key
   return rs;
 }
 
+// ---------------------------------------------------------------------------
+// Paged KV calls.
+// ---------------------------------------------------------------------------
+bool mul_ok(uint64_t a, uint64_t b, uint64_t* r) { return !__builtin_mul_overflow(a, b, r); }
+bool add_ok(uint64_t a, uint64_t b, uint64_t* r) { return !__builtin_add_overflow(a, b, r); }
+
+// Geometry rules of gift_paged_kv (see gift.h).
+gift_status check_paged_geometry(const gift_paged_kv* kv) {
+  const uint64_t cb = kv->chunk_bytes;
+  if (!kv->base || ((uintptr_t)kv->base & 15u)) return fail(GIFT_E_INVALID, "paged: base null or not 16-byte aligned");
+  if (cb < 16 || (cb & (cb - 1))) return fail(GIFT_E_INVALID, "paged: chunk_bytes must be a power of two >= 16");
+  if ((kv->layer_stride | kv->block_stride | kv->part_stride) & 15u)
+    return fail(GIFT_E_INVALID, "paged: strides must be multiples of 16");
+  if (kv->n_layers == 0 || kv->n_parts == 0 || kv->n_blocks == 0)
+    return fail(GIFT_E_INVALID, "paged: n_layers, n_parts and n_blocks must be >= 1");
+  struct Dim {
+    uint64_t stride, count;
+  } dims[3] = {{kv->layer_stride, kv->n_layers}, {kv->block_stride, kv->n_blocks}, {kv->part_stride, kv->n_parts}};
+  std::sort(dims, dims + 3, [](const Dim& x, const Dim& y) { return x.stride < y.stride; });
+  uint64_t extent = cb;
+  for (const Dim& d : dims) {
+    if (d.count <= 1) continue;
+    uint64_t span;
+    if (d.stride < extent || !mul_ok(d.stride, d.count - 1, &span) || !add_ok(span, extent, &extent))
+      return fail(GIFT_E_INVALID, "paged: strided dimensions overlap");
+  }
+  return GIFT_OK;
+}
+
+template <bool OPEN>
+gift_status run_paged(const gift_paged_kv* kv, const gift_request* reqs, uint32_t n, const uint32_t* labels,
+                      gift_key_table kt, const uint8_t* nonce_base, const void* in, void* out, uint8_t* tags_out,
+                      const uint8_t* tags_in, int32_t* verdicts_user, hipStream_t stream) {
+  g_last_error.clear();
+  if (!kv || !kt) return fail(GIFT_E_INVALID, "null cache description or key table");
+  if (n > 0 && (!reqs || !nonce_base || (OPEN ? (!in || !tags_in || !verdicts_user) : (!out || !tags_out))))
+    return fail(GIFT_E_INVALID, "null requests, nonce_base, buffer, tags or verdicts");
+  gift_status sv = check_paged_geometry(kv);
+  if (sv != GIFT_OK) return sv;
+  const uint64_t per_block_chunks = (uint64_t)kv->n_layers * kv->n_parts;
+  uint64_t per_block_bytes;
+  if (!mul_ok(per_block_chunks, kv->chunk_bytes, &per_block_bytes)) return fail(GIFT_E_INVALID, "paged: sizes overflow");
+  // fixed part of the farthest chunk: last layer and part
+  uint64_t fixed = kv->chunk_bytes, t1, t2;
+  if (!mul_ok(kv->layer_stride, kv->n_layers - 1, &t1) || !mul_ok(kv->part_stride, kv->n_parts - 1, &t2) ||
+      !add_ok(fixed, t1, &fixed) || !add_ok(fixed, t2, &fixed))
+    return fail(GIFT_E_RANGE, "paged: chunks exceed the cache");
+  uint64_t total_bytes = 0, total_bids = 0;
+  for (uint32_t i = 0; i < n; i++) {
+    const gift_request& r = reqs[i];
+    if (r.n_block_ids == 0 || !r.block_ids) return fail(GIFT_E_INVALID, "request %u: empty block table", i);
+    if (r.user == GIFT_LABEL_PARAM || r.user == GIFT_LABEL_UNOWNED)
+      return fail(GIFT_E_INVALID, "request %u: user id is a label sentinel", i);
+    uint32_t maxb = 0;
+    for (uint32_t j = 0; j < r.n_block_ids; j++) maxb = r.block_ids[j] > maxb ? r.block_ids[j] : maxb;
+    if (maxb >= kv->n_blocks) return fail(GIFT_E_RANGE, "request %u: block id %u >= n_blocks", i, maxb);
+    if (r.user >= kt->n_users) return fail(GIFT_E_RANGE, "request %u: user %u >= n_users", i, r.user);
+    uint64_t far;
+    if (!mul_ok(kv->block_stride, maxb, &far) || !add_ok(far, fixed, &far) || far > kv->cache_bytes)
+      return fail(GIFT_E_RANGE, "request %u: chunks exceed cache_bytes", i);
+    uint64_t len;
+    if (!mul_ok(per_block_bytes, r.n_block_ids, &len) || len > kMaxSegBytes)
+      return fail(GIFT_E_TOO_LARGE, "request %u: longer than (2^32-2)*16 bytes", i);
+    if (!add_ok(total_bytes, len, &total_bytes)) return fail(GIFT_E_INVALID, "paged: sizes overflow");
+    total_bids += r.n_block_ids;
+  }
+  {
+    std::vector<uint32_t> all;
+    all.reserve(total_bids);
+    for (uint32_t i = 0; i < n; i++) all.insert(all.end(), reqs[i].block_ids, reqs[i].block_ids + reqs[i].n_block_ids);
+    std::sort(all.begin(), all.end());
+    for (size_t j = 1; j < all.size(); j++)
+      if (all[j] == all[j - 1]) return fail(GIFT_E_OVERLAP, "block id %u appears twice", all[j]);
+    std::vector<std::pair<uint64_t, uint64_t>> v(n);
+    for (uint32_t i = 0; i < n; i++) v[i] = {reqs[i].user, reqs[i].iv_seq};
+    std::sort(v.begin(), v.end());
+    for (uint32_t i = 1; i < n; i++)
+      if (v[i] == v[i - 1])
+        return fail(GIFT_E_NONCE_REUSE, "two requests share user %llu and iv_seq %llu", (unsigned long long)v[i].first,
+                    (unsigned long long)v[i].second);
+  }
+  const void* flat = OPEN ? in : out;
+  if (total_bytes > 0) {
+    const uintptr_t a0 = (uintptr_t)kv->base, b0 = (uintptr_t)flat;
+    if (a0 < b0 + total_bytes && b0 < a0 + kv->cache_bytes)
+      return fail(GIFT_E_INVALID, "the contiguous buffer overlaps the cache allocation");
+    if (b0 & 15u) return fail(GIFT_E_INVALID, "the contiguous buffer must be 16-byte aligned");
+  }
+  if (n == 0) return GIFT_OK;
+  int dev;
+  if ((sv = current_device(&dev)) != GIFT_OK) return sv;
+  if (dev != kt->device) return fail(GIFT_E_INVALID, "key table belongs to device %d, current is %d", kt->device, dev);
+
+  // descriptors: rows = positions in the uploaded block-id array
+  std::vector<SegDesc> descs(n);
+  uint64_t boff = 0, bpos = 0, cpos = 0;
+  uint32_t n_tiles = 0;
+  for (uint32_t i = 0; i < n; i++) {
+    const gift_request& r = reqs[i];
+    SegDesc& d = descs[i];
+    memset(&d, 0, sizeof d);
+    d.byte_off = boff;
+    d.len = per_block_bytes * r.n_block_ids;
+    d.row_begin = bpos;
+    d.row_count = r.n_block_ids;
+    d.user = r.user;
+    d.nblocks = (uint32_t)(d.len / 16);
+    d.flags = kSegAligned;
+    d.chunk0 = cpos;
+    uint8_t iv[12];
+    memcpy(iv, nonce_base + 12ull * r.user, 12);
+    for (int k = 0; k < 8; k++) iv[11 - k] ^= (uint8_t)(r.iv_seq >> (8 * k));
+    for (int w = 0; w < 3; w++)
+      d.iv[w] = (uint32_t)iv[4 * w] | ((uint32_t)iv[4 * w + 1] << 8) | ((uint32_t)iv[4 * w + 2] << 16) |
+                ((uint32_t)iv[4 * w + 3] << 24);
+    n_tiles += (uint32_t)(((uint64_t)d.nblocks + kTileBlocks - 1) / kTileBlocks);
+    boff += d.len;
+    bpos += r.n_block_ids;
+    cpos += per_block_chunks * r.n_block_ids;
+  }
+  uint32_t shift = 0;
+  while ((16ull << shift) < kv->chunk_bytes) shift++;
+
+  // scratch: descs | bids | tile_base | small_list | partials | verdicts | chunk offsets
+  const size_t o_desc = 0;
+  const size_t o_bid = o_desc + align256(sizeof(SegDesc) * n);
+  const size_t o_tb = o_bid + align256(4ull * total_bids);
+  const size_t o_sl = o_tb + align256(4ull * (n + 1));
+  const size_t o_pt = o_sl + align256(4ull * n);
+  const size_t o_vd = o_pt + align256(16ull * (n_tiles ? n_tiles : 1));
+  const size_t o_ck = o_vd + align256(4ull * n);
+  const size_t bytes = o_ck + align256(8ull * cpos);
+  uint8_t* scratch = nullptr;
+  hipError_t e = hipMallocAsync((void**)&scratch, bytes, stream);
+  if (e != hipSuccess) return hip_fail(e, "hipMallocAsync(scratch)");
+  std::vector<uint8_t> host(o_tb);
+  memcpy(host.data() + o_desc, descs.data(), sizeof(SegDesc) * n);
+  {
+    uint32_t* bp = (uint32_t*)(host.data() + o_bid);
+    for (uint32_t i = 0; i < n; i++) {
+      memcpy(bp, reqs[i].block_ids, 4ull * reqs[i].n_block_ids);
+      bp += reqs[i].n_block_ids;
+    }
+  }
+  Staging* sg = staging_for(dev);
+  e = sg ? sg->upload(scratch, host.data(), o_tb, stream) : hipErrorInvalidDevice;
+  if (e != hipSuccess) {
+    (void)hipFreeAsync(scratch, stream);
+    return hip_fail(e, "staging upload");
+  }
+  const SegDesc* d_desc = (const SegDesc*)(scratch + o_desc);
+  const uint32_t* d_bid = (const uint32_t*)(scratch + o_bid);
+  uint64_t* d_ck = (uint64_t*)(scratch + o_ck);
+  int32_t* verdicts = verdicts_user ? verdicts_user : (int32_t*)(scratch + o_vd);
+  gift_status rs = GIFT_OK;
+  do {
+    if (labels) {
+      e = launch_check_owner(d_desc, n, labels, d_bid, verdicts, stream);
+      if (e != hipSuccess) {
+        rs = hip_fail(e, "check_owner launch");
+        break;
+      }
+    }
+    e = launch_expand(d_desc, n, (uint32_t*)(scratch + o_tb), (uint32_t*)(scratch + o_sl), verdicts, labels == nullptr,
+                      stream);
+    if (e == hipSuccess)
+      e = launch_chunk_table(d_desc, n, d_bid, kv->n_layers, kv->n_parts, kv->layer_stride, kv->block_stride,
+                             kv->part_stride, d_ck, stream);
+    if (e != hipSuccess) {
+      rs = hip_fail(e, "paged expansion");
+      break;
+    }
+    GcmArgs a;
+    a.in = (const uint8_t*)in;
+    a.out = (uint8_t*)out;
+    a.chunk_off = d_ck;
+    a.pbase = (uint8_t*)kv->base;
+    a.chunk_shift = shift;
+    a.segs = d_desc;
+    a.n_segs = n;
+    a.tile_base = (const uint32_t*)(scratch + o_tb);
+    a.small_list = (const uint32_t*)(scratch + o_sl);
+    a.n_tiles = n_tiles;
+    a.n_small = 0;
+    a.partials = (uint4*)(scratch + o_pt);
+    a.verdicts = verdicts;
+    a.tags_out = tags_out;
+    a.tags_in = tags_in;
+    a.kt = kt->dev;
+    if (g_prof_before) {
+      e = hipEventRecord(g_prof_before, stream);
+      if (e != hipSuccess) {
+        rs = hip_fail(e, "profiling event");
+        break;
+      }
+    }
+    e = launch_gcm_tiles(a, OPEN ? (kModeOpen | kModeScatter) : kModeGather, (uint32_t)device_cus(dev), stream);
+    if (e == hipSuccess && g_prof_after) e = hipEventRecord(g_prof_after, stream);
+    if (e == hipSuccess) e = launch_gcm_finalize(a, OPEN, stream);
+    if (e == hipSuccess && OPEN)
+      e = launch_zero_chunks(d_desc, n, verdicts, d_ck, (uint8_t*)kv->base, kv->chunk_bytes,
+                             (uint32_t)device_cus(dev) * 4u, stream);
+    if (e != hipSuccess) {
+      rs = hip_fail(e, "paged gcm launch");
+      break;
+    }
+  } while (0);
+  g_prof_before = g_prof_after = nullptr;
+  e = hipFreeAsync(scratch, stream);
+  if (rs == GIFT_OK && e != hipSuccess) rs = hip_fail(e, "hipFreeAsync(scratch)");
+  return rs;
+}
+
 }  // namespace
 
 extern "C" {
+
+gift_status gift_seal_paged(const gift_paged_kv* kv, const gift_request* reqs, uint32_t n_reqs,
+                            const uint32_t* block_labels, gift_key_table kt, const uint8_t* nonce_base, void* out,
+                            uint8_t* tags, int32_t* verdicts, hipStream_t stream) {
+  return run_paged<false>(kv, reqs, n_reqs, block_labels, kt, nonce_base, nullptr, out, tags, nullptr, verdicts,
+                          stream);
+}
+
+gift_status gift_open_paged(const gift_paged_kv* kv, const gift_request* reqs, uint32_t n_reqs,
+                            const uint32_t* block_labels, gift_key_table kt, const uint8_t* nonce_base,
+                            const void* in, const uint8_t* tags, int32_t* verdicts, hipStream_t stream) {
+  return run_paged<true>(kv, reqs, n_reqs, block_labels, kt, nonce_base, in, nullptr, nullptr, tags, verdicts, stream);
+}
+
 
 const char* gift_status_string(gift_status s) {
   switch (s) {
@@ -513,7 +743,7 @@ gift_status gift_check_owner(const gift_segment_table* st, const uint32_t* label
   if (e != hipSuccess) return hip_fail(e, "hipMallocAsync(descs)");
   Staging* sg = staging_for(dev);
   e = sg ? sg->upload(d, P.descs.data(), bytes, stream) : hipErrorInvalidDevice;
-  if (e == hipSuccess) e = launch_check_owner(d, n, labels, st->verdicts, stream);
+  if (e == hipSuccess) e = launch_check_owner(d, n, labels, nullptr, st->verdicts, stream);
   hipError_t e2 = hipFreeAsync(d, stream);
   if (e != hipSuccess) return hip_fail(e, "check_owner");
   if (e2 != hipSuccess) return hip_fail(e2, "hipFreeAsync(descs)");

@@ -36,7 +36,7 @@ struct SegDesc {
   uint32_t user;
   uint32_t nblocks;    // ceil(len / 16), <= 2^32 - 2
   uint32_t flags;      // kSegAligned | kSegSmall
-  uint32_t pad[2];
+  uint64_t chunk0;     // paged calls: index of the segment's first chunk in the chunk table
 };
 static_assert(sizeof(SegDesc) == 64, "SegDesc layout");
 
@@ -62,9 +62,18 @@ struct KeyTableDev {
   uint32_t n_users;
 };
 
+// Addressing of k_gcm_tiles: contiguous tensor, or a paged cache on the
+// input side (seal: gather) or the output side (open: scatter).
+enum : int { kModeOpen = 1, kModeGather = 2, kModeScatter = 4 };
+
 struct GcmArgs {
   const uint8_t* in;
   uint8_t* out;
+  // paged calls: chunk c of a segment starts at pbase + chunk_off[chunk0 + c]
+  // and holds 2^chunk_shift blocks
+  const uint64_t* chunk_off;
+  uint8_t* pbase;
+  uint32_t chunk_shift;
   const SegDesc* segs;
   uint32_t n_segs;
   const uint32_t* tile_base;   // [n_segs + 1] first tile of each segment (small ones: 0 tiles)
@@ -81,16 +90,26 @@ struct GcmArgs {
 // Launch wrappers (gift_kernels.hip).  All enqueue on `s` and return the
 // launch status.
 hipError_t launch_key_setup(const uint8_t* keys_dev, KeyTableDev kt, hipStream_t s);
-hipError_t launch_check_owner(const SegDesc* segs, uint32_t n_segs, const uint32_t* labels, int32_t* verdicts,
-                              hipStream_t s);
+// labels are indexed by row, or by bids[row] when bids is not NULL (paged:
+// rows are positions in the uploaded block tables)
+hipError_t launch_check_owner(const SegDesc* segs, uint32_t n_segs, const uint32_t* labels, const uint32_t* bids,
+                              int32_t* verdicts, hipStream_t s);
 hipError_t launch_expand(const SegDesc* segs, uint32_t n_segs, uint32_t* tile_base, uint32_t* small_list,
                          int32_t* verdicts, bool init_verdicts, hipStream_t s);
-hipError_t launch_gcm_tiles(const GcmArgs& a, bool open, uint32_t grid, hipStream_t s);
+hipError_t launch_gcm_tiles(const GcmArgs& a, int mode, uint32_t grid, hipStream_t s);
 hipError_t launch_gcm_small(const GcmArgs& a, bool open, hipStream_t s);
 hipError_t launch_gcm_finalize(const GcmArgs& a, bool open, hipStream_t s);
 hipError_t launch_zero_ranges(uint8_t* out, const ZeroRange* r, uint32_t n, const int32_t* verdicts, uint32_t grid,
                               hipStream_t s);
 hipError_t launch_wipe(void* p, size_t bytes, hipStream_t s);
+// Paged calls: chunk offsets from the block tables (segment rows index bids),
+// and zeroing of every chunk of segments whose verdict is not OK.
+hipError_t launch_chunk_table(const SegDesc* segs, uint32_t n_segs, const uint32_t* bids, uint32_t n_layers,
+                              uint32_t n_parts, uint64_t layer_stride, uint64_t block_stride, uint64_t part_stride,
+                              uint64_t* chunk_off, hipStream_t s);
+hipError_t launch_zero_chunks(const SegDesc* segs, uint32_t n_segs, const int32_t* verdicts,
+                              const uint64_t* chunk_off, uint8_t* pbase, uint64_t chunk_bytes, uint32_t grid,
+                              hipStream_t s);
 // Per-token block encryption (decrypt == true: the inverse).  Rows of the
 // descriptors are token indices.
 hipError_t launch_tokens(const SegDesc* segs, uint32_t n_segs, bool decrypt, const uint64_t* tokens,

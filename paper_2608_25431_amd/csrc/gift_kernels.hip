@@ -232,8 +232,10 @@ __device__ __forceinline__ u128 length_block(uint64_t len) {
 // ---------------------------------------------------------------------------
 // Per-block kernel over 2 MiB tiles of the non-small segments.
 // ---------------------------------------------------------------------------
-template <bool OPEN>
+template <int MODE>
 __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
+  constexpr bool OPEN = (MODE & kModeOpen) != 0;
+  constexpr bool GATHER = (MODE & kModeGather) != 0, SCATTER = (MODE & kModeScatter) != 0;
   __shared__ __attribute__((aligned(16))) uint8_t smem[kLdsBytes];
   const uint32_t tid = threadIdx.x;
   uint8_t* tt = smem + kLdsAes;
@@ -281,13 +283,21 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
     const int64_t base = (int64_t)m - (int64_t)(t + 1) * (int64_t)kTileBlocks;  // block index of virtual slot 0
     const int r_start = base < 0 ? (int)((uint64_t)(-base) / kThreads) : 0;
 
+    // paged side: block i of the segment lives in chunk i >> shift
+    const uint64_t chunk0 = sd->chunk0;
+    const uint64_t cmask = (1ull << a.chunk_shift) - 1;
+    auto paged = [&](uint64_t i) -> uint8_t* {
+      return a.pbase + a.chunk_off[chunk0 + (i >> a.chunk_shift)] + ((i & cmask) << 4);
+    };
+
     if (verdict != kVerdictOk) {
       // rejected before this call's data is touched: release zeros only
       for (int r = r_start; r < kRows; r++) {
         const int64_t i0 = base + (int64_t)r * kThreads + tid;
         if (i0 >= 0) {
           const uint64_t rem = len - 16ull * (uint64_t)i0;
-          store_block(a.out + off + 16ull * (uint64_t)i0, u128_zero(), rem >= 16 ? 16u : (uint32_t)rem, aligned);
+          uint8_t* dst = SCATTER ? paged((uint64_t)i0) : a.out + off + 16ull * (uint64_t)i0;
+          store_block(dst, u128_zero(), rem >= 16 ? 16u : (uint32_t)rem, aligned);
         }
       }
       continue;
@@ -329,9 +339,19 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
       aes_rounds_lds<3>(x0, x1, x2, x3, rk, tt, L);
       u128 x;
       if (aligned && r >= r_full && r < r_end_full) {
-        const uint4 v = *(const uint4*)(in_lane + (uintptr_t)r * (16u * kThreads));
+        const uint8_t* src;
+        uint8_t* dst;
+        if (GATHER || SCATTER) {
+          const uint64_t i0 = (uint64_t)(base + (int64_t)r * kThreads + tid);
+          src = GATHER ? paged(i0) : a.in + off + 16ull * i0;
+          dst = SCATTER ? paged(i0) : a.out + off + 16ull * i0;
+        } else {
+          src = (const uint8_t*)(in_lane + (uintptr_t)r * (16u * kThreads));
+          dst = (uint8_t*)(out_lane + (uintptr_t)r * (16u * kThreads));
+        }
+        const uint4 v = *(const uint4*)src;
         const uint4 o = make_uint4(v.x ^ x0, v.y ^ x1, v.z ^ x2, v.w ^ x3);
-        *(uint4*)(out_lane + (uintptr_t)r * (16u * kThreads)) = o;
+        *(uint4*)dst = o;
         x = OPEN ? u128{{v.x, v.y, v.z, v.w}} : u128{{o.x, o.y, o.z, o.w}};
       } else {
         x = u128_zero();
@@ -340,9 +360,9 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
           const uint64_t boff = off + 16ull * (uint64_t)i0;
           const uint64_t rem = len - 16ull * (uint64_t)i0;
           const uint32_t n = rem >= 16 ? 16u : (uint32_t)rem;
-          const u128 in = load_block(a.in + boff, n, aligned);
+          const u128 in = load_block(GATHER ? paged((uint64_t)i0) : a.in + boff, n, aligned);
           const u128 o = mask_block(u128{{in.w[0] ^ x0, in.w[1] ^ x1, in.w[2] ^ x2, in.w[3] ^ x3}}, n);
-          store_block(a.out + boff, o, n, aligned);
+          store_block(SCATTER ? paged((uint64_t)i0) : a.out + boff, o, n, aligned);
           x = OPEN ? in : o;
         }
       }
@@ -520,12 +540,13 @@ __global__ __launch_bounds__(1024) void k_expand(const SegDesc* __restrict__ seg
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void k_check_owner(const SegDesc* __restrict__ segs, uint32_t n,
                                                      const uint32_t* __restrict__ labels,
+                                                     const uint32_t* __restrict__ bids,
                                                      int32_t* __restrict__ verdicts) {
   for (uint32_t s = blockIdx.x; s < n; s += gridDim.x) {
     const uint64_t rb = segs[s].row_begin, rc = segs[s].row_count;
     const uint32_t user = segs[s].user;
     int bad = 0;
-    for (uint64_t r = threadIdx.x; r < rc; r += blockDim.x) bad |= labels[rb + r] != user;
+    for (uint64_t r = threadIdx.x; r < rc; r += blockDim.x) bad |= labels[bids ? bids[rb + r] : rb + r] != user;
     bad = __syncthreads_or(bad);
     if (threadIdx.x == 0) verdicts[s] = bad ? kVerdictOwnerMixed : kVerdictOk;
   }
@@ -605,6 +626,40 @@ __global__ __launch_bounds__(64) void k_tokens(const SegDesc* __restrict__ segs,
 }
 
 // ---------------------------------------------------------------------------
+// Paged KV: offsets of a segment's chunks in stream order (for each block of
+// its table, each layer, each part), and zeroing of rejected segments' chunks.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_chunk_table(const SegDesc* __restrict__ segs, uint32_t n,
+                                                     const uint32_t* __restrict__ bids, uint32_t n_layers,
+                                                     uint32_t n_parts, uint64_t ls, uint64_t bs, uint64_t ps,
+                                                     uint64_t* __restrict__ chunk_off) {
+  const uint64_t per_block = (uint64_t)n_layers * n_parts;
+  for (uint32_t s = blockIdx.x; s < n; s += gridDim.x) {
+    const uint64_t bid0 = segs[s].row_begin, nchunks = segs[s].row_count * per_block, c0 = segs[s].chunk0;
+    for (uint64_t c = threadIdx.x; c < nchunks; c += blockDim.x) {
+      const uint64_t j = c / per_block, rem = c % per_block;
+      const uint64_t l = rem / n_parts, p = rem % n_parts;
+      chunk_off[c0 + c] = l * ls + (uint64_t)bids[bid0 + j] * bs + p * ps;
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) void k_zero_chunks(const SegDesc* __restrict__ segs, uint32_t n,
+                                                     const int32_t* __restrict__ verdicts,
+                                                     const uint64_t* __restrict__ chunk_off, uint8_t* pbase,
+                                                     uint64_t chunk_bytes) {
+  const uint64_t gtid = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const uint64_t gsz = (uint64_t)gridDim.x * blockDim.x;
+  const uint64_t per_chunk = chunk_bytes / 16;
+  for (uint32_t s = 0; s < n; s++) {
+    if (verdicts[s] == kVerdictOk) continue;
+    const uint64_t nblk = segs[s].len / 16, c0 = segs[s].chunk0;
+    for (uint64_t i = gtid; i < nblk; i += gsz)
+      *(uint4*)(pbase + chunk_off[c0 + i / per_chunk] + 16 * (i % per_chunk)) = make_uint4(0u, 0u, 0u, 0u);
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Key-table setup.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(64) void k_key_sched(const uint8_t* __restrict__ keys, KeyTableDev kt) {
@@ -677,11 +732,11 @@ hipError_t launch_key_setup(const uint8_t* keys_dev, KeyTableDev kt, hipStream_t
   return hipGetLastError();
 }
 
-hipError_t launch_check_owner(const SegDesc* segs, uint32_t n_segs, const uint32_t* labels, int32_t* verdicts,
-                              hipStream_t s) {
+hipError_t launch_check_owner(const SegDesc* segs, uint32_t n_segs, const uint32_t* labels, const uint32_t* bids,
+                              int32_t* verdicts, hipStream_t s) {
   if (n_segs == 0) return hipSuccess;
   const uint32_t grid = n_segs < 65535u ? n_segs : 65535u;
-  hipLaunchKernelGGL(k_check_owner, dim3(grid), dim3(256), 0, s, segs, n_segs, labels, verdicts);
+  hipLaunchKernelGGL(k_check_owner, dim3(grid), dim3(256), 0, s, segs, n_segs, labels, bids, verdicts);
   return hipGetLastError();
 }
 
@@ -692,13 +747,18 @@ hipError_t launch_expand(const SegDesc* segs, uint32_t n_segs, uint32_t* tile_ba
   return hipGetLastError();
 }
 
-hipError_t launch_gcm_tiles(const GcmArgs& a, bool open, uint32_t grid, hipStream_t s) {
+hipError_t launch_gcm_tiles(const GcmArgs& a, int mode, uint32_t grid, hipStream_t s) {
   if (a.n_tiles == 0) return hipSuccess;
   const uint32_t g = a.n_tiles < grid ? a.n_tiles : grid;
-  if (open)
-    hipLaunchKernelGGL(k_gcm_tiles<true>, dim3(g), dim3(kThreads), 0, s, a);
-  else
-    hipLaunchKernelGGL(k_gcm_tiles<false>, dim3(g), dim3(kThreads), 0, s, a);
+  switch (mode) {
+    case 0: hipLaunchKernelGGL(k_gcm_tiles<0>, dim3(g), dim3(kThreads), 0, s, a); break;
+    case kModeOpen: hipLaunchKernelGGL(k_gcm_tiles<kModeOpen>, dim3(g), dim3(kThreads), 0, s, a); break;
+    case kModeGather: hipLaunchKernelGGL(k_gcm_tiles<kModeGather>, dim3(g), dim3(kThreads), 0, s, a); break;
+    case kModeOpen | kModeScatter:
+      hipLaunchKernelGGL(k_gcm_tiles<kModeOpen | kModeScatter>, dim3(g), dim3(kThreads), 0, s, a);
+      break;
+    default: return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 
@@ -738,6 +798,25 @@ hipError_t launch_tokens(const SegDesc* segs, uint32_t n_segs, bool decrypt, con
   else
     hipLaunchKernelGGL(k_tokens<false>, dim3(grid), dim3(64), 0, s, segs, n_segs, tokens, nonces, blocks_in,
                        blocks_out, tokens_out, nonces_out, eos_token, kt);
+  return hipGetLastError();
+}
+
+hipError_t launch_chunk_table(const SegDesc* segs, uint32_t n_segs, const uint32_t* bids, uint32_t n_layers,
+                              uint32_t n_parts, uint64_t layer_stride, uint64_t block_stride, uint64_t part_stride,
+                              uint64_t* chunk_off, hipStream_t s) {
+  if (n_segs == 0) return hipSuccess;
+  const uint32_t grid = n_segs < 65535u ? n_segs : 65535u;
+  hipLaunchKernelGGL(k_chunk_table, dim3(grid), dim3(256), 0, s, segs, n_segs, bids, n_layers, n_parts, layer_stride,
+                     block_stride, part_stride, chunk_off);
+  return hipGetLastError();
+}
+
+hipError_t launch_zero_chunks(const SegDesc* segs, uint32_t n_segs, const int32_t* verdicts,
+                              const uint64_t* chunk_off, uint8_t* pbase, uint64_t chunk_bytes, uint32_t grid,
+                              hipStream_t s) {
+  if (n_segs == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_zero_chunks, dim3(grid), dim3(256), 0, s, segs, n_segs, verdicts, chunk_off, pbase,
+                     chunk_bytes);
   return hipGetLastError();
 }
 

@@ -43,10 +43,21 @@ class _SegTable(ctypes.Structure):
                 ("verdicts", ctypes.c_void_p)]
 
 
+class _PagedKV(ctypes.Structure):
+    _fields_ = [("base", ctypes.c_void_p), ("cache_bytes", ctypes.c_uint64), ("layer_stride", ctypes.c_uint64),
+                ("block_stride", ctypes.c_uint64), ("part_stride", ctypes.c_uint64), ("chunk_bytes", ctypes.c_uint64),
+                ("n_layers", ctypes.c_uint32), ("n_parts", ctypes.c_uint32), ("n_blocks", ctypes.c_uint64)]
+
+
+class _Request(ctypes.Structure):
+    _fields_ = [("block_ids", ctypes.c_void_p), ("n_block_ids", ctypes.c_uint32), ("user", ctypes.c_uint32),
+                ("iv_seq", ctypes.c_uint64)]
+
+
 assert ctypes.sizeof(_Segment) == SEGMENT_DTYPE.itemsize == 32
 
 EXPORTS = ("gift_key_table_create", "gift_key_table_users", "gift_key_table_destroy", "gift_seal", "gift_open",
-           "gift_check_owner", "gift_token_encrypt", "gift_token_decrypt", "gift_profile_next_call",
+           "gift_check_owner", "gift_seal_paged", "gift_open_paged", "gift_token_encrypt", "gift_token_decrypt", "gift_profile_next_call",
            "gift_status_string", "gift_last_error")
 
 _lib = None
@@ -73,6 +84,10 @@ def lib():
         L.gift_open.restype = st
         L.gift_check_owner.argtypes = [ctypes.POINTER(_SegTable), P, ctypes.c_uint64, P]
         L.gift_check_owner.restype = st
+        L.gift_seal_paged.argtypes = [ctypes.POINTER(_PagedKV), P, ctypes.c_uint32, P, P, P, P, P, P, P]
+        L.gift_seal_paged.restype = st
+        L.gift_open_paged.argtypes = [ctypes.POINTER(_PagedKV), P, ctypes.c_uint32, P, P, P, P, P, P, P]
+        L.gift_open_paged.restype = st
         L.gift_token_encrypt.argtypes = [ctypes.POINTER(_SegTable), P, P, ctypes.c_uint64, P, ctypes.c_uint64, P, P]
         L.gift_token_encrypt.restype = st
         L.gift_token_decrypt.argtypes = [ctypes.POINTER(_SegTable), P, ctypes.c_uint64, P, ctypes.c_uint64, P, P, P]
@@ -219,6 +234,40 @@ def check_owner(segs, labels, n_rows, verdicts, stream=None):
     """gift_check_owner."""
     tab, keep = _table(segs, None, verdicts)
     _check(lib().gift_check_owner(ctypes.byref(tab), _ptr(labels), n_rows, _stream(stream)))
+    del keep
+
+
+def paged_kv(cache, cache_bytes, layer_stride, block_stride, part_stride, chunk_bytes, n_layers, n_parts, n_blocks):
+    """gift_paged_kv for a device allocation (torch tensor or address)."""
+    return _PagedKV(_ptr(cache), cache_bytes, layer_stride, block_stride, part_stride, chunk_bytes, n_layers, n_parts,
+                    n_blocks)
+
+
+def _requests(reqs):
+    keep = [np.ascontiguousarray(b, np.uint32) for b, _, _ in reqs]
+    arr = (_Request * max(len(reqs), 1))()
+    for i, ((_, u, q), b) in enumerate(zip(reqs, keep)):
+        arr[i] = _Request(b.ctypes.data if b.size else None, b.size, u, q)
+    return arr, keep
+
+
+def seal_paged(kv, reqs, kt, nonce_base, out, tags, block_labels=None, verdicts=None, stream=None):
+    """gift_seal_paged.  kv from paged_kv(); reqs: list of (block_ids, user, iv_seq)."""
+    arr, keep = _requests(reqs)
+    nb = _nonce(nonce_base, kt)
+    _check(lib().gift_seal_paged(ctypes.byref(kv), ctypes.addressof(arr) if reqs else None, len(reqs),
+                                 _ptr(block_labels), kt.handle, nb.ctypes.data, _ptr(out), _ptr(tags), _ptr(verdicts),
+                                 _stream(stream)))
+    del keep
+
+
+def open_paged(kv, reqs, kt, nonce_base, sealed, tags, verdicts, block_labels=None, stream=None):
+    """gift_open_paged."""
+    arr, keep = _requests(reqs)
+    nb = _nonce(nonce_base, kt)
+    _check(lib().gift_open_paged(ctypes.byref(kv), ctypes.addressof(arr) if reqs else None, len(reqs),
+                                 _ptr(block_labels), kt.handle, nb.ctypes.data, _ptr(sealed), _ptr(tags),
+                                 _ptr(verdicts), _stream(stream)))
     del keep
 
 

@@ -466,3 +466,172 @@ def test_token_encryption_matches_oracle():
         st_o = oracle.token_encrypt(segs, tok[:8], non[:8], w.keys, eos)[0]
         assert status_of(gift.token_encrypt, segs, dt, dn, 8, kt, eos, out) == st_o, segs
     kt.destroy()
+
+
+# --------------------------------------------------------------------------
+# paged KV: seal from / open into a paged cache through block tables
+# --------------------------------------------------------------------------
+def paged_geom(layout, layers, parts, blocks, chunk):
+    if layout == "lbp":
+        ps, bs, ls = chunk, parts * chunk, blocks * parts * chunk
+    else:
+        bs, ps, ls = chunk, blocks * chunk, parts * blocks * chunk
+    return oracle.PagedKV(layers * ls, ls, bs, ps, chunk, layers, parts, blocks)
+
+
+def dev_kv(g, cache_dev):
+    return gift.paged_kv(cache_dev, g.cache_bytes, g.layer_stride, g.block_stride, g.part_stride, g.chunk_bytes,
+                         g.n_layers, g.n_parts, g.n_blocks)
+
+
+def paged_case(keys, nb, kt, g, reqs, moved=None, labels=None, tamper=None):
+    cache = rng.integers(0, 256, g.cache_bytes, dtype=np.uint8)
+    st, o_sealed, o_tags, o_ver = oracle.seal_paged(cache, g, reqs, keys, nb, labels=labels)
+    assert st == 0
+    c_dev = dev_u8(cache)
+    kv = dev_kv(g, c_dev)
+    n = len(reqs)
+    total = o_sealed.size
+    sealed = torch.full((max(total, 16),), 0x5A, dtype=torch.uint8, device=DEV)
+    tags = torch.zeros(16 * n, dtype=torch.uint8, device=DEV)
+    ver = torch.full((n,), -1, dtype=torch.int32, device=DEV)
+    lab = None if labels is None else dev_u32(labels)
+    gift.seal_paged(kv, reqs, kt, nb, sealed, tags, block_labels=lab, verdicts=ver)
+    assert host(sealed)[:total].tobytes() == o_sealed.tobytes()
+    assert host(tags).tobytes() == o_tags.tobytes()
+    assert host(ver).tolist() == o_ver.tolist()
+    assert torch.equal(c_dev, dev_u8(cache))  # the source cache is untouched
+    if tamper is not None:
+        o_sealed = o_sealed.copy()
+        o_sealed[tamper] ^= 1
+        sealed[tamper] ^= 1
+    dst = moved if moved is not None else reqs
+    st, o_after, o_ver2 = oracle.open_paged(cache, g, dst, keys, nb, o_sealed, o_tags, labels=labels)
+    ver2 = torch.full((n,), -1, dtype=torch.int32, device=DEV)
+    gift.open_paged(kv, dst, kt, nb, sealed, tags, ver2, block_labels=lab)
+    assert host(ver2).tolist() == o_ver2.tolist()
+    assert host(c_dev).tobytes() == o_after.tobytes()
+    return o_ver, o_ver2
+
+
+def random_tables(n_blocks, sizes, n_users, rng_):
+    perm = rng_.permutation(n_blocks)
+    reqs, p = [], 0
+    for i, k in enumerate(sizes):
+        reqs.append((perm[p:p + k].astype(np.uint32), int(rng_.integers(0, n_users)), 100 + i))
+        p += k
+    return reqs, perm[p:]
+
+
+@pytest.mark.parametrize("layout,layers,parts,blocks,chunk,sizes", [
+    ("lbp", 4, 1, 40, 65536, [4, 1, 3, 6, 2, 5]),      # K+V in one 64 KiB chunk per layer
+    ("lpb", 3, 2, 64, 32768, [3, 3, 1, 8, 2]),         # K and V planes apart
+    ("lbp", 5, 2, 300, 256, [20, 1, 37, 64, 5, 90]),   # rows span many chunks
+    ("lpb", 2, 1, 5000, 16, [1000, 1, 2047, 900]),     # one block per chunk
+])
+def test_paged_seal_open_every_byte(kt3, layout, layers, parts, blocks, chunk, sizes):
+    keys, nb, kt = kt3
+    g = paged_geom(layout, layers, parts, blocks, chunk)
+    r_ = np.random.default_rng(blocks)
+    reqs, spare = random_tables(blocks, sizes, 3, r_)
+    ver, ver2 = paged_case(keys, nb, kt, g, reqs)
+    assert (ver == 0).all() and (ver2 == 0).all()
+    # swap-in: the same sealed data opened into other (spare + shuffled) blocks
+    pool = r_.permutation(np.concatenate([np.concatenate([b for b, _, _ in reqs]), spare]))
+    moved, p = [], 0
+    for b, u, q in reqs:
+        moved.append((pool[p:p + len(b)].astype(np.uint32), u, q))
+        p += len(b)
+    paged_case(keys, nb, kt, g, reqs, moved=moved)
+
+
+def test_paged_manipulated_table_and_tamper(kt3):
+    keys, nb, kt = kt3
+    g = paged_geom("lbp", 3, 2, 50, 4096)
+    r_ = np.random.default_rng(11)
+    reqs, _ = random_tables(50, [5, 4, 6, 3], 3, r_)
+    labels = np.full(50, gift.LABEL_UNOWNED, np.uint32)
+    for b, u, _ in reqs:
+        labels[b] = u
+    ver, ver2 = paged_case(keys, nb, kt, g, reqs, labels=labels)
+    assert (ver == 0).all() and (ver2 == 0).all()
+    # request 1's table now also names request 0's block (different owner)
+    other = reqs[0][1] if reqs[0][1] != reqs[1][1] else None
+    evil = list(reqs)
+    if other is None:
+        labels[reqs[0][0][0]] = (reqs[1][1] + 1) % 3
+    evil[1] = (np.concatenate([reqs[1][0], reqs[0][0][:1]]), reqs[1][1], reqs[1][2])
+    evil[0] = (reqs[0][0][1:], reqs[0][1], reqs[0][2])
+    ver, ver2 = paged_case(keys, nb, kt, g, evil, labels=labels)
+    assert ver[1] == gift.SEG_OWNER_MIXED and ver2[1] == gift.SEG_OWNER_MIXED
+    # a flipped ciphertext bit in request 2 fails it and zeroes its blocks
+    per = g.n_layers * g.n_parts * g.chunk_bytes
+    off = per * (len(reqs[0][0]) + len(reqs[1][0])) + 77
+    ver, ver2 = paged_case(keys, nb, kt, g, reqs, tamper=off)
+    assert ver2.tolist() == [0, 0, gift.SEG_AUTH_FAIL, 0]
+
+
+def test_paged_validation_matches_oracle(kt3):
+    keys, nb, kt = kt3
+    g = paged_geom("lbp", 3, 2, 10, 64)
+    cache = np.zeros(g.cache_bytes, np.uint8)
+    c_dev = dev_u8(cache)
+    out = torch.zeros(1 << 16, dtype=torch.uint8, device=DEV)
+    tags = torch.zeros(64, dtype=torch.uint8, device=DEV)
+    geoms = [g, paged_geom("lbp", 3, 2, 10, 48),
+             oracle.PagedKV(g.cache_bytes, g.layer_stride, 32, g.part_stride, 64, 3, 2, 10),
+             oracle.PagedKV(g.cache_bytes // 2, g.layer_stride, g.block_stride, g.part_stride, 64, 3, 2, 10)]
+    tables = [[([1], 0, 0)], [([], 0, 0)], [([10], 0, 0)], [([1], 3, 0)], [([1, 2], 0, 0), ([2], 1, 0)],
+              [([1], 0, 4), ([2], 0, 4)], [([1], gift.LABEL_PARAM, 0)]]
+    for gg in geoms:
+        for reqs in tables:
+            st_o = oracle.seal_paged(cache, gg, reqs, keys, nb)[0]
+            st_g = status_of(gift.seal_paged, dev_kv(gg, c_dev), reqs, kt, nb, out, tags)
+            assert st_g == st_o, (gg.chunk_bytes, gg.block_stride, gg.cache_bytes, reqs)
+    # the export buffer may not overlap the cache
+    assert status_of(gift.seal_paged, dev_kv(g, c_dev), [([1], 0, 0)], kt, nb, c_dev[64:], tags) == gift.E_INVALID
+
+
+def test_paged_full_size_equals_contiguous_seal():
+    """The llama3_8b_kv tensor scattered into a vLLM-style per-layer cache
+    ([layer][block][64 KiB], 5% spare blocks, random placement): sealing
+    through the block tables reproduces the contiguous seal exactly, and
+    opening into fresh blocks restores every chunk."""
+    w = W.llama3_8b_kv()
+    t = w.tensors[0]
+    kt = gift.KeyTable(w.keys)
+    L, C = 32, t.row_bytes
+    nblk_req = [int(s["row_count"]) // L for s in t.segs]
+    B = sum(nblk_req)
+    NB = B + B // 20
+    d = t.generate(DEV)
+    ct, tags, _ = seal(d, t.n_rows, t.row_bytes, t.segs, kt, w.nonce_base)
+    r_ = np.random.default_rng(3)
+    perm = r_.permutation(NB)[:B]
+    cache = torch.zeros(L * NB * C, dtype=torch.uint8, device=DEV)
+    cv = cache.view(L, NB, C)
+    pidx = torch.from_numpy(perm).to(DEV)
+    cv[:, pidx, :] = d.view(B, L, C).transpose(0, 1)
+    reqs, p = [], 0
+    for i, k in enumerate(nblk_req):
+        s = t.segs[i]
+        reqs.append((perm[p:p + k].astype(np.uint32), int(s["user"]), int(s["iv_seq"])))
+        p += k
+    kv = gift.paged_kv(cache, cache.numel(), NB * C, C, 0, C, L, 1, NB)
+    sealed = torch.empty_like(d)
+    ptags = torch.zeros_like(tags)
+    ver = torch.full((len(reqs),), -1, dtype=torch.int32, device=DEV)
+    gift.seal_paged(kv, reqs, kt, w.nonce_base, sealed, ptags, verdicts=ver)
+    assert (host(ver) == 0).all()
+    assert torch.equal(sealed, ct) and torch.equal(ptags, tags)
+    # open into a fresh placement
+    perm2 = r_.permutation(NB)[:B]
+    moved, p = [], 0
+    for (b, u, q), k in zip(reqs, nblk_req):
+        moved.append((perm2[p:p + k].astype(np.uint32), u, q))
+        p += k
+    cache.zero_()
+    gift.open_paged(kv, moved, kt, w.nonce_base, sealed, ptags, ver)
+    assert (host(ver) == 0).all()
+    assert torch.equal(cv[:, torch.from_numpy(perm2).to(DEV), :], d.view(B, L, C).transpose(0, 1))
+    kt.destroy()
