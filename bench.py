@@ -147,6 +147,45 @@ def time_tokens(gift, W, torch, steps=50):
     return {"tokens": t.n_rows, "users": w.n_users, "encrypt_us": round(enc_us, 2), "decrypt_us": round(dec_us, 2)}
 
 
+def time_host_tracking(gift, rows=2048, hidden=4096, reps=200):
+    """Host cost of ownership tracking per kernel launch (GIFT Sec. 4.1
+    Insight 3: it runs on the CPU beside the GPU work): the AddBias rule over
+    a [rows, hidden] hidden-state matrix, and a race check of an attention
+    launch reading 64 KV blocks while a swap stream writes others."""
+    o = gift.Ownership()
+    base = 1 << 44
+    x, y, bias = base, base + (1 << 36), base + (2 << 36)
+    o.register(x, (rows, hidden), 2)
+    o.register(y, (rows, hidden), 2)
+    o.register(bias, (hidden,), 2, odims=())
+    o.set(bias, 0, 1, gift.LABEL_PARAM)
+    for u in range(64):
+        o.set(x, u * rows // 64, rows // 64, u)
+    ops0 = o.ops
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        assert o.add_bias(y, x, bias, rows, hidden, 2) == gift.OK
+    rule_s = (time.perf_counter() - t0) / reps
+    ops = (o.ops - ops0) // reps
+    o.destroy()
+    c = gift.RaceChecker()
+    blk = 1 << 21
+    kv = gift.ranges([(base + i * blk, blk) for i in range(4096)])
+    t0 = time.perf_counter()
+    for r in range(reps):
+        reads = kv[(r * 64) % 2048:(r * 64) % 2048 + 64]
+        swap = kv[2048 + (r * 8) % 2048:2048 + (r * 8) % 2048 + 8]
+        assert c.launch(0, reads=reads)[0] == gift.OK
+        assert c.launch(1, writes=swap)[0] == gift.OK
+        if r % 16 == 15:
+            c.sync_all()
+    race_s = (time.perf_counter() - t0) / (2 * reps)
+    c.destroy()
+    return {"add_bias_rows": rows, "add_bias_us": round(rule_s * 1e6, 2), "add_bias_record_ops": int(ops),
+            "ns_per_record_op": round(rule_s * 1e9 / ops, 2), "race_check_us_per_launch": round(race_s * 1e6, 2),
+            "race_ranges_per_launch": "64 reads / 8 writes", "note": "host CPU, ctypes call included"}
+
+
 def time_paged(gift, t, w, kt, data, out, steps, warmup, torch):
     """Seal through block tables: the same requests scattered into a
     vLLM-style per-layer cache [layer][block][64 KiB] with 5% spare blocks
@@ -337,6 +376,8 @@ def main():
         log(f"[bench] paged seal: {res['paged_seal']}")
     res["token_encryption"] = time_tokens(gift, W, torch)
     log(f"[bench] token encryption: {res['token_encryption']}")
+    res["host_tracking"] = time_host_tracking(gift)
+    log(f"[bench] host ownership tracking: {res['host_tracking']}")
     if not args.no_cpu_baseline:
         log("[bench] cpu baseline (oracle) ...")
         res["cpu_baseline"] = cpu_baseline(w, t, data)  # data holds plaintext again here

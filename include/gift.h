@@ -60,7 +60,9 @@ typedef enum {
   GIFT_E_NONCE_REUSE = -4, /* two segments of one call share (user, iv_seq) */
   GIFT_E_TOO_LARGE = -5,   /* segment longer than (2^32-2)*16 bytes (SP 800-38D Sec. 5.2.1.1) */
   GIFT_E_HIP = -6,         /* a HIP runtime call failed */
-  GIFT_E_NOMEM = -7        /* device or pinned host allocation failed */
+  GIFT_E_NOMEM = -7,       /* device or pinned host allocation failed */
+  GIFT_E_REJECTED = -8,    /* an IFT rule refused a launch (include/gift_ift.h) */
+  GIFT_E_RACE = -9         /* a launch would race with another stream (include/gift_ift.h) */
 } gift_status;
 
 /* per-segment verdicts, int32 */

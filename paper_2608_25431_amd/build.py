@@ -10,7 +10,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libgift.so")
-SOURCES = [os.path.join(CSRC, "gift_kernels.hip"), os.path.join(CSRC, "gift_host.cpp")]
+SOURCES = [os.path.join(CSRC, "gift_kernels.hip"), os.path.join(CSRC, "gift_host.cpp"), os.path.join(CSRC, "gift_ift.cpp")]
 ARCH = "gfx950"
 
 # Packed-FP32 instructions are disabled for all device code.

@@ -14,6 +14,7 @@
 #include <vector>
 
 #include "gift.h"
+#include "gift_ift.h"
 #include "gift_internal.hpp"
 
 using namespace gift;
@@ -626,6 +627,8 @@ const char* gift_status_string(gift_status s) {
     case GIFT_E_TOO_LARGE: return "segment exceeds the GCM length limit";
     case GIFT_E_HIP: return "HIP runtime error";
     case GIFT_E_NOMEM: return "out of memory";
+    case GIFT_E_REJECTED: return "IFT rule rejected the kernel launch";
+    case GIFT_E_RACE: return "launch races with an unfinished kernel on another stream";
   }
   return "unknown status";
 }

@@ -15,6 +15,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libgift.so")
 
 OK, E_INVALID, E_RANGE, E_OVERLAP, E_NONCE_REUSE, E_TOO_LARGE, E_HIP, E_NOMEM = 0, -1, -2, -3, -4, -5, -6, -7
+E_REJECTED, E_RACE = -8, -9
 SEG_OK, SEG_AUTH_FAIL, SEG_OWNER_MIXED = 0, 1, 2
 LABEL_PARAM, LABEL_UNOWNED = 0xFFFFFFFE, 0xFFFFFFFF
 
@@ -49,6 +50,10 @@ class _PagedKV(ctypes.Structure):
                 ("n_layers", ctypes.c_uint32), ("n_parts", ctypes.c_uint32), ("n_blocks", ctypes.c_uint64)]
 
 
+class _Range(ctypes.Structure):
+    _fields_ = [("addr", ctypes.c_uint64), ("bytes", ctypes.c_uint64)]
+
+
 class _Request(ctypes.Structure):
     _fields_ = [("block_ids", ctypes.c_void_p), ("n_block_ids", ctypes.c_uint32), ("user", ctypes.c_uint32),
                 ("iv_seq", ctypes.c_uint64)]
@@ -58,7 +63,13 @@ assert ctypes.sizeof(_Segment) == SEGMENT_DTYPE.itemsize == 32
 
 EXPORTS = ("gift_key_table_create", "gift_key_table_users", "gift_key_table_destroy", "gift_seal", "gift_open",
            "gift_check_owner", "gift_seal_paged", "gift_open_paged", "gift_token_encrypt", "gift_token_decrypt", "gift_profile_next_call",
-           "gift_status_string", "gift_last_error")
+           "gift_status_string", "gift_last_error",
+           # include/gift_ift.h
+           "gift_own_create", "gift_own_destroy", "gift_own_register", "gift_own_release", "gift_own_units",
+           "gift_own_flat_index", "gift_own_set", "gift_own_get", "gift_own_labels", "gift_own_ops",
+           "gift_ift_add_residual", "gift_ift_add_bias", "gift_ift_find_max", "gift_ift_matmul",
+           "gift_race_create", "gift_race_destroy", "gift_race_launch", "gift_race_wait", "gift_race_sync", "gift_race_sync_all",
+           "gift_race_release")
 
 _lib = None
 
@@ -98,6 +109,25 @@ def lib():
         L.gift_status_string.restype = ctypes.c_char_p
         L.gift_last_error.argtypes = []
         L.gift_last_error.restype = ctypes.c_char_p
+        u32, u64 = ctypes.c_uint32, ctypes.c_uint64
+        H = P
+        for name, args in (
+                ("gift_own_create", [ctypes.POINTER(ctypes.c_void_p)]), ("gift_own_destroy", [H]),
+                ("gift_own_register", [H, P, u32, P, u32, u32]), ("gift_own_release", [H, P]),
+                ("gift_own_units", [H, P, ctypes.POINTER(u64)]),
+                ("gift_own_flat_index", [H, P, P, ctypes.POINTER(u64)]), ("gift_own_set", [H, P, u64, u64, u32]),
+                ("gift_own_get", [H, P, u64, ctypes.POINTER(u32)]), ("gift_own_labels", [H, P, P, u64]),
+                ("gift_ift_add_residual", [H, P, P, P, u64, u64, u32]),
+                ("gift_ift_add_bias", [H, P, P, P, u64, u64, u32]),
+                ("gift_ift_find_max", [H, P, P, u64, u64, u32, u32]),
+                ("gift_ift_matmul", [H, P, P, P, u64, u64, u64, u32]),
+                ("gift_race_create", [ctypes.POINTER(ctypes.c_void_p)]), ("gift_race_destroy", [H]),
+                ("gift_race_launch", [H, u32, P, u32, P, u32, ctypes.POINTER(u64)]),
+                ("gift_race_wait", [H, u32, u32, u64]), ("gift_race_sync", [H, u32]), ("gift_race_sync_all", [H]), ("gift_race_release", [H, _Range])):
+            getattr(L, name).argtypes = args
+            getattr(L, name).restype = st
+        L.gift_own_ops.argtypes = [H]
+        L.gift_own_ops.restype = u64
         _lib = L
     return _lib
 
@@ -295,3 +325,137 @@ def profile_next_call(before, after):
 def raw_status(fn_name, *args):
     """Calls an entry point and returns its status instead of raising (tests)."""
     return getattr(lib(), fn_name)(*args)
+
+
+# --- include/gift_ift.h: host-side ownership records, IFT rules, race checks ---
+
+def _check_host(s):
+    # the host-only tracking entry points report through their status alone
+    if s != OK:
+        raise GiftError(s, status_string(s))
+
+
+class Ownership:
+    """Owns a gift_ownership handle (ownership records and IFT rules).
+
+    Tensors are named by their base address (a torch tensor, numpy array or
+    int); nothing is dereferenced."""
+
+    def __init__(self):
+        h = ctypes.c_void_p()
+        _check_host(lib().gift_own_create(ctypes.byref(h)))
+        self.handle = h.value
+
+    def destroy(self):
+        if self.handle:
+            h, self.handle = self.handle, None
+            _check_host(lib().gift_own_destroy(h))
+
+    def __del__(self):
+        try:
+            self.destroy()
+        except Exception:
+            pass
+
+    def register(self, base, shape, elem_size, odims=(0,)):
+        sh = np.ascontiguousarray(shape, np.uint64)
+        mask = 0
+        for d in odims:
+            mask |= 1 << d
+        _check_host(lib().gift_own_register(self.handle, _ptr(base), sh.size, sh.ctypes.data, elem_size, mask))
+
+    def release(self, base):
+        _check_host(lib().gift_own_release(self.handle, _ptr(base)))
+
+    def units(self, base):
+        n = ctypes.c_uint64()
+        _check_host(lib().gift_own_units(self.handle, _ptr(base), ctypes.byref(n)))
+        return n.value
+
+    def flat_index(self, base, subs):
+        s = np.ascontiguousarray(subs, np.uint64)
+        f = ctypes.c_uint64()
+        _check_host(lib().gift_own_flat_index(self.handle, _ptr(base), s.ctypes.data if s.size else None,
+                                              ctypes.byref(f)))
+        return f.value
+
+    def set(self, base, flat_begin, count, owner):
+        _check_host(lib().gift_own_set(self.handle, _ptr(base), flat_begin, count, owner))
+
+    def get(self, base, flat):
+        o = ctypes.c_uint32()
+        _check_host(lib().gift_own_get(self.handle, _ptr(base), flat, ctypes.byref(o)))
+        return o.value
+
+    def labels(self, base):
+        n = self.units(base)
+        out = np.empty(n, np.uint32)
+        _check_host(lib().gift_own_labels(self.handle, _ptr(base), out.ctypes.data, n))
+        return out
+
+    @property
+    def ops(self):
+        return lib().gift_own_ops(self.handle)
+
+    # IFT rules: return the status (OK or E_REJECTED) instead of raising, since
+    # a refusal is an expected outcome of the monitor.
+    def add_residual(self, out, inp, res, rows, cols, elem_size):
+        return lib().gift_ift_add_residual(self.handle, _ptr(out), _ptr(inp), _ptr(res), rows, cols, elem_size)
+
+    def add_bias(self, out, inp, bias, rows, cols, elem_size):
+        return lib().gift_ift_add_bias(self.handle, _ptr(out), _ptr(inp), _ptr(bias), rows, cols, elem_size)
+
+    def find_max(self, out, inp, rows, cols, in_elem_size, out_elem_size):
+        return lib().gift_ift_find_max(self.handle, _ptr(out), _ptr(inp), rows, cols, in_elem_size, out_elem_size)
+
+    def matmul(self, out, inp, weight, rows, k, n, elem_size):
+        return lib().gift_ift_matmul(self.handle, _ptr(out), _ptr(inp), _ptr(weight), rows, k, n, elem_size)
+
+
+def ranges(rs):
+    """gift_range array (uint64 [n, 2]: addr, bytes) from (addr, bytes) pairs."""
+    if isinstance(rs, np.ndarray) and rs.dtype == np.uint64 and rs.ndim == 2 and rs.shape[1] == 2:
+        return np.ascontiguousarray(rs)
+    return np.asarray(list(rs or ()), np.uint64).reshape(-1, 2)
+
+
+class RaceChecker:
+    """Owns a gift_race handle (launch-order checking across streams)."""
+
+    def __init__(self):
+        h = ctypes.c_void_p()
+        _check_host(lib().gift_race_create(ctypes.byref(h)))
+        self.handle = h.value
+
+    def destroy(self):
+        if self.handle:
+            h, self.handle = self.handle, None
+            _check_host(lib().gift_race_destroy(h))
+
+    def __del__(self):
+        try:
+            self.destroy()
+        except Exception:
+            pass
+
+    def launch(self, stream, reads=(), writes=()):
+        """Returns (status, seq); reads/writes are (addr, bytes) pairs or a
+        ranges() array."""
+        r, w = ranges(reads), ranges(writes)
+        seq = ctypes.c_uint64()
+        s = lib().gift_race_launch(self.handle, stream, r.ctypes.data if len(r) else None, len(r),
+                                   w.ctypes.data if len(w) else None, len(w), ctypes.byref(seq))
+        return s, seq.value
+
+    def wait(self, stream, on_stream, seq):
+        """Returns the status (OK, or E_RANGE for a kernel not yet launched)."""
+        return lib().gift_race_wait(self.handle, stream, on_stream, seq)
+
+    def sync(self, stream):
+        _check_host(lib().gift_race_sync(self.handle, stream))
+
+    def sync_all(self):
+        _check_host(lib().gift_race_sync_all(self.handle))
+
+    def release(self, addr, nbytes):
+        _check_host(lib().gift_race_release(self.handle, _Range(addr, nbytes)))

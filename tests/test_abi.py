@@ -42,7 +42,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_status_strings(lib):
-    for s in range(-7, 1):
+    for s in range(-9, 1):
         assert gift.status_string(s)
     assert gift.status_string(-100) == "unknown status"
     assert gift.last_error() == ""
