@@ -141,6 +141,41 @@ def test_owner_labels_fused_and_standalone(kt3):
         assert host(ver).tolist() == o.tolist()
 
 
+def test_propagated_labels_drive_the_fused_check(kt3):
+    # host ownership tracking of a hidden-state tensor through AddBias and
+    # AddResidual, then a seal whose segments the framework claims: segments
+    # that disagree with the propagated labels are rejected on the device
+    keys, nb, kt = kt3
+    rows, cols = 96, 2048  # bf16: 4096-byte rows
+    rb = 2 * cols
+    x = torch.empty(rows * rb, dtype=torch.uint8, device=DEV)
+    res = torch.empty_like(x)
+    y = torch.empty_like(x)
+    bias = torch.empty(rb, dtype=torch.uint8, device=DEV)
+    o = gift.Ownership()
+    for t in (x, res, y):
+        o.register(t, (rows, cols), 2)
+    o.register(bias, (cols,), 2, odims=())
+    o.set(bias, 0, 1, gift.LABEL_PARAM)
+    for t in (x, res):
+        o.set(t, 0, 40, 0)
+        o.set(t, 40, 50, 1)
+        o.set(t, 90, 6, 2)
+    assert o.add_bias(x, x, bias, rows, cols, 2) == gift.OK
+    assert o.add_residual(y, x, res, rows, cols, 2) == gift.OK
+    o.set(res, 45, 1, 2)  # one row of the residual now holds user 2's data
+    assert o.add_residual(y, x, res, rows, cols, 2) == gift.E_REJECTED  # nothing changes
+    labels = o.labels(y)
+    data = rng.integers(0, 256, rows * rb, dtype=np.uint8)
+    honest = [(0, 40, 0, 7), (40, 50, 1, 7), (90, 6, 2, 7)]
+    forged = [(0, 41, 0, 8), (41, 49, 1, 8), (90, 6, 1, 9)]  # claims a user-1 row and user 2's rows
+    for table in (honest, forged):
+        full_compare(keys, nb, kt, data, rows, rb, table, labels=labels)
+    _, _, ver = seal(dev_u8(data), rows, rb, forged, kt, nb, labels_dev=dev_u32(labels))
+    assert host(ver)[:3].tolist() == [gift.SEG_OWNER_MIXED, gift.SEG_OK, gift.SEG_OWNER_MIXED]
+    o.destroy()
+
+
 def test_validation_status_matches_oracle(kt3):
     keys, nb, kt = kt3
     n_rows, rb = 6, 16
