@@ -53,6 +53,10 @@ __device__ __forceinline__ void aes_rounds_lds(uint32_t& s0, uint32_t& s1, uint3
                                                const uint32_t* rk, const uint8_t* tt, uint32_t L) {
 #pragma unroll
   for (int r = R0; r < 14; r++) {
+    // The LDS is the bottleneck: a wave that is forming addresses and issuing
+    // its reads runs at raised priority, so the LDS queue is refilled as soon
+    // as possible, and drops back while it combines results.
+    __builtin_amdgcn_s_setprio(2);
     // all 16 lookups of the round are issued before any is combined, so a
     // wave keeps 16 LDS reads in flight
     const uint32_t a0 = GIFT_T0(s0, 0), a1 = GIFT_T1(s1, 1), a2 = GIFT_T2(s2, 2), a3 = GIFT_T3(s3, 3);
@@ -62,6 +66,7 @@ __device__ __forceinline__ void aes_rounds_lds(uint32_t& s0, uint32_t& s1, uint3
     __builtin_amdgcn_sched_group_barrier(0x0002, 16, 0);  // 16 address perms
     __builtin_amdgcn_sched_group_barrier(0x0100, 16, 0);  // 16 LDS reads
     __builtin_amdgcn_sched_group_barrier(0x0002, 8, 0);   // 8 xor3
+    __builtin_amdgcn_s_setprio(0);
     s0 = xor3(xor3(a0, a1, a2), a3, rk[4 * r + 0]);
     s1 = xor3(xor3(b0, b1, b2), b3, rk[4 * r + 1]);
     s2 = xor3(xor3(c0, c1, c2), c3, rk[4 * r + 2]);
@@ -366,6 +371,9 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
           x = OPEN ? in : o;
         }
       }
+      // GHASH table reads at a priority between the AES issue and combine
+      // phases; the next AES round sets its own
+      __builtin_amdgcn_s_setprio(1);
       y = ghash_step_lds(y, x, gt);
     }
 
