@@ -334,27 +334,28 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
     // aligned take the branch-free path
     const int r_full = base < 0 ? (int)(((uint64_t)(-base) + kThreads - 1) / kThreads) : 0;
     const int r_end_full = (t == 0 && (len & 15u)) ? kRows - 1 : kRows;
-    const uintptr_t in_lane = (uintptr_t)a.in + off + 16 * (int64_t)(base + (int64_t)tid);
-    const uintptr_t out_lane = (uintptr_t)a.out + off + 16 * (int64_t)(base + (int64_t)tid);
 
     u128 y = u128_zero();
     for (int r = r_start; r < kRows; r++) {
+      // the whole-block rows load their input before the AES rounds, so the
+      // HBM latency overlaps the keystream
+      const bool fast = aligned && r >= r_full && r < r_end_full;
+      const uint8_t* src = nullptr;
+      uint8_t* dst = nullptr;
+      uint4 v = make_uint4(0, 0, 0, 0);
+      if (fast) {
+        // every lane's block index is >= 0 in these rows; pointer arithmetic
+        // (not integers) keeps the global address space for the compiler
+        const uint64_t i0 = (uint64_t)(base + (int64_t)r * kThreads + tid);
+        src = GATHER ? paged(i0) : a.in + off + 16ull * i0;
+        dst = SCATTER ? paged(i0) : a.out + off + 16ull * i0;
+        v = *(const uint4*)src;
+      }
       uint32_t x0, x1, x2, x3;
       ctr_rounds12(cc, c0 + (uint32_t)kThreads * (uint32_t)r, x0, x1, x2, x3, rk, tt, L);
       aes_rounds_lds<3>(x0, x1, x2, x3, rk, tt, L);
       u128 x;
-      if (aligned && r >= r_full && r < r_end_full) {
-        const uint8_t* src;
-        uint8_t* dst;
-        if (GATHER || SCATTER) {
-          const uint64_t i0 = (uint64_t)(base + (int64_t)r * kThreads + tid);
-          src = GATHER ? paged(i0) : a.in + off + 16ull * i0;
-          dst = SCATTER ? paged(i0) : a.out + off + 16ull * i0;
-        } else {
-          src = (const uint8_t*)(in_lane + (uintptr_t)r * (16u * kThreads));
-          dst = (uint8_t*)(out_lane + (uintptr_t)r * (16u * kThreads));
-        }
-        const uint4 v = *(const uint4*)src;
+      if (fast) {
         const uint4 o = make_uint4(v.x ^ x0, v.y ^ x1, v.z ^ x2, v.w ^ x3);
         *(uint4*)dst = o;
         x = OPEN ? u128{{v.x, v.y, v.z, v.w}} : u128{{o.x, o.y, o.z, o.w}};
