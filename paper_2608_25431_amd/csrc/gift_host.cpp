@@ -246,6 +246,13 @@ void build_plan(const gift_segment* segs, uint32_t n, uint64_t n_rows, uint64_t 
     for (uint32_t i = 0; i < n; i++)
       if (!(P.descs[i].flags & kSegSmall))
         P.zr.push_back(ZeroRange{P.descs[i].byte_off, P.descs[i].len, (int32_t)i, {0, 0, 0}});
+  // pieces of at most kZeroPieceBytes, so that one workgroup takes one piece
+  std::vector<ZeroRange> pieces;
+  pieces.reserve(P.zr.size());
+  for (const ZeroRange& z : P.zr)
+    for (uint64_t o = 0; o < z.len; o += kZeroPieceBytes)
+      pieces.push_back(ZeroRange{z.off + o, std::min(kZeroPieceBytes, z.len - o), z.seg, {0, 0, 0}});
+  P.zr.swap(pieces);
 }
 
 gift_status current_device(int* dev) {
@@ -586,8 +593,8 @@ gift_status run_paged(const gift_paged_kv* kv, const gift_request* reqs, uint32_
     if (e == hipSuccess && g_prof_after) e = hipEventRecord(g_prof_after, stream);
     if (e == hipSuccess) e = launch_gcm_finalize(a, OPEN, stream);
     if (e == hipSuccess && OPEN)
-      e = launch_zero_chunks(d_desc, n, verdicts, d_ck, (uint8_t*)kv->base, kv->chunk_bytes,
-                             (uint32_t)device_cus(dev) * 4u, stream);
+      e = launch_zero_chunks(d_desc, n, (const uint32_t*)(scratch + o_tb), n_tiles, verdicts, d_ck,
+                             (uint8_t*)kv->base, shift, (uint32_t)device_cus(dev) * 4u, stream);
     if (e != hipSuccess) {
       rs = hip_fail(e, "paged gcm launch");
       break;
@@ -660,7 +667,8 @@ gift_status gift_key_table_create(const uint8_t* keys, uint32_t n_users, hipStre
   const size_t o_ph = o_gt + align256(u * 512 * 16);
   const size_t o_pt = o_ph + align256(u * kHPowers * 16);
   const size_t o_pl = o_pt + align256(u * kFinLanes * 16);
-  const size_t bytes = o_pl + align256(u * 16);
+  const size_t o_px = o_pl + align256(u * 16);
+  const size_t bytes = o_px + align256(u * kHxLanes * 16);
   uint8_t* mem = nullptr;
   hipError_t e = hipMalloc((void**)&mem, bytes);
   if (e != hipSuccess) return hip_fail(e, "hipMalloc(key table)");
@@ -682,6 +690,7 @@ gift_status gift_key_table_create(const uint8_t* keys, uint32_t n_users, hipStre
   kt->dev.pow_h = (uint4*)(mem + o_ph);
   kt->dev.pow_ht = (uint4*)(mem + o_pt);
   kt->dev.pow_hlt = (uint4*)(mem + o_pl);
+  kt->dev.pow_hxl = (uint4*)(mem + o_px);
   kt->dev.n_users = n_users;
   // The copy reads the caller's buffer; synchronising before return means no
   // copy of the keys outlives the call on the host side of the library.

@@ -21,7 +21,8 @@ constexpr int kRows = GIFT_ROWS;
 constexpr uint32_t kTileBlocks = (uint32_t)kThreads * kRows;  // 2 MiB per tile by default
 static_assert(kThreads % 64 == 0 && kThreads <= 1024, "workgroup size");
 constexpr uint32_t kSmallMaxBlocks = 64;                   // segments up to 1 KiB: one wave each
-constexpr int kHPowers = kThreads;                         // H^0 .. H^(kThreads-1) per user
+constexpr int kHPowers = kThreads + 2;                     // H^0 .. H^(kThreads+1) per user
+constexpr int kHxLanes = 64;                               // H * x^(64+k), k < 64, per user
 constexpr int kFinLanes = 64;                              // lanes of the per-segment finalize
 
 enum : uint32_t { kSegAligned = 1u, kSegSmall = 2u };
@@ -49,6 +50,7 @@ struct ZeroRange {
   uint32_t pad[3];
 };
 static_assert(sizeof(ZeroRange) == 32, "ZeroRange layout");
+constexpr uint64_t kZeroPieceBytes = 4ull << 20;  // zero ranges are cut into pieces of at most this size
 
 // Per-user key material in device memory, one allocation.
 struct KeyTableDev {
@@ -59,6 +61,7 @@ struct KeyTableDev {
   uint4* pow_h;      // [n_users][kHPowers] H^k
   uint4* pow_ht;     // [n_users][kFinLanes] H^(k * kTileBlocks)
   uint4* pow_hlt;    // [n_users] H^(kFinLanes * kTileBlocks)
+  uint4* pow_hxl;    // [n_users][kHxLanes] H * x^(64+k): the products H * L needs
   uint32_t n_users;
 };
 
@@ -107,9 +110,9 @@ hipError_t launch_wipe(void* p, size_t bytes, hipStream_t s);
 hipError_t launch_chunk_table(const SegDesc* segs, uint32_t n_segs, const uint32_t* bids, uint32_t n_layers,
                               uint32_t n_parts, uint64_t layer_stride, uint64_t block_stride, uint64_t part_stride,
                               uint64_t* chunk_off, hipStream_t s);
-hipError_t launch_zero_chunks(const SegDesc* segs, uint32_t n_segs, const int32_t* verdicts,
-                              const uint64_t* chunk_off, uint8_t* pbase, uint64_t chunk_bytes, uint32_t grid,
-                              hipStream_t s);
+hipError_t launch_zero_chunks(const SegDesc* segs, uint32_t n_segs, const uint32_t* tile_base, uint32_t n_tiles,
+                              const int32_t* verdicts, const uint64_t* chunk_off, uint8_t* pbase,
+                              uint32_t chunk_shift, uint32_t grid, hipStream_t s);
 // Per-token block encryption (decrypt == true: the inverse).  Rows of the
 // descriptors are token indices.
 hipError_t launch_tokens(const SegDesc* segs, uint32_t n_segs, bool decrypt, const uint64_t* tokens,

@@ -11,8 +11,9 @@
 //     staged in LDS.
 // Tiles are aligned to the END of their segment, so the block at distance d
 // from the segment's last block contributes X*H^(d + 2) to the GHASH sum; a
-// tile t contributes P_t * H^(t*T) with P_t the sum over its own blocks, and
-// lane l of a full tile ends at distance (1023 - l) from the tile's end.
+// tile t contributes P_t * H^(t*T) with P_t = sum of X*H^(d_t + 2) over its
+// own blocks (d_t: distance from the tile's end), and lane l of a full tile
+// ends at distance (1023 - l) from the tile's end.
 #include <hip/hip_runtime.h>
 
 #include "gift_device.hpp"
@@ -378,8 +379,9 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
       y = ghash_step_lds(y, x, gt);
     }
 
-    // lane contribution y * H^(1023 - tid), then the workgroup sum
-    const u128 hp = ld_u128(a.kt.pow_h + (size_t)user * kHPowers + (kThreads - 1 - tid));
+    // lane contribution y * H^(1023 - tid) times the H^2 that every block's
+    // GHASH term carries, then the workgroup sum
+    const u128 hp = ld_u128(a.kt.pow_h + (size_t)user * kHPowers + (kThreads + 1 - tid));
     u128 z = gf_mul(y, hp);
 #pragma unroll
     for (int j = 0; j < 4; j++) z.w[j] = wave_xor(z.w[j]);
@@ -394,12 +396,17 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Per-segment finalize of tiled segments: S = H*(H*sum_t P_t H^(tT) xor L),
+// Per-segment finalize of tiled segments: S = sum_t P_t H^(tT) xor H*L and
 // tag = E_K(J0) xor S.  One wave per segment; lane l folds tiles l, l+64, ...
+// H*L is a wave sum over the set bits of L (only its low 64 bits can be set)
+// of the products H*x^(64+k); E_K(J0) uses a T-table copy in LDS.
 // ---------------------------------------------------------------------------
 template <bool OPEN>
 __global__ __launch_bounds__(kFinLanes) void k_finalize(GcmArgs a) {
+  __shared__ uint32_t te[256];
   const uint32_t s = blockIdx.x, lane = threadIdx.x;
+  for (uint32_t i = lane; i < 256u; i += kFinLanes) te[i] = c_aes.te0[i];
+  __syncthreads();
   const SegDesc sd = a.segs[s];
   if (sd.flags & kSegSmall) return;
   const int32_t verdict = a.verdicts[s];
@@ -411,24 +418,43 @@ __global__ __launch_bounds__(kFinLanes) void k_finalize(GcmArgs a) {
   const uint32_t tb = a.tile_base[s], nt = a.tile_base[s + 1] - tb;
   u128 z = u128_zero();
   if (lane < nt) {
-    const u128 hlt = ld_u128(a.kt.pow_hlt + user);
     const uint32_t K = (nt - 1 - lane) / kFinLanes + 1;
-    for (int k = (int)K - 1; k >= 0; k--) {
-      z = gf_mul(z, hlt);
-      z = u128_xor(z, ld_u128(a.partials + tb + lane + (uint32_t)k * kFinLanes));
+    z = ld_u128(a.partials + tb + lane + (K - 1) * kFinLanes);
+    if (K > 1) {
+      const u128 hlt = ld_u128(a.kt.pow_hlt + user);
+      for (int k = (int)K - 2; k >= 0; k--)
+        z = u128_xor(gf_mul(z, hlt), ld_u128(a.partials + tb + lane + (uint32_t)k * kFinLanes));
     }
-    z = gf_mul(z, ld_u128(a.kt.pow_ht + (size_t)user * kFinLanes + lane));
+    if (lane > 0) z = gf_mul(z, ld_u128(a.kt.pow_ht + (size_t)user * kFinLanes + lane));
   }
+  // H*L: bit 64+lane of L (GCM order) is bit 63-lane of the 64-bit length in bits
+  const uint64_t lbits = sd.len * 8ull;
+  if ((lbits >> (63 - lane)) & 1ull) z = u128_xor(z, ld_u128(a.kt.pow_hxl + (size_t)user * kHxLanes + lane));
 #pragma unroll
   for (int j = 0; j < 4; j++) z.w[j] = wave_xor(z.w[j]);
   if (lane == 0) {
-    const u128 h = ld_u128((const uint4*)(a.kt.h + 4ull * user));
-    u128 sacc = gf_mul(u128_xor(gf_mul(z, h), length_block(sd.len)), h);
     const uint32_t* rk = a.kt.rk + (size_t)user * 64u;
-    const uint32_t j0[4] = {sd.iv[0], sd.iv[1], sd.iv[2], 0x01000000u};
-    uint32_t e[4];
-    aes256_encrypt_words(rk, j0, e, c_aes);
-    u128 tag = u128{{e[0] ^ sacc.w[0], e[1] ^ sacc.w[1], e[2] ^ sacc.w[2], e[3] ^ sacc.w[3]}};
+    uint32_t s0 = sd.iv[0] ^ rk[0], s1 = sd.iv[1] ^ rk[1], s2 = sd.iv[2] ^ rk[2], s3 = 0x01000000u ^ rk[3];
+#define GIFT_TL(w, k) rotl32(te[((w) >> (8 * (k))) & 0xffu], 8 * (k))
+    for (int r = 1; r < 14; r++) {
+      const uint32_t t0 = GIFT_TL(s0, 0) ^ GIFT_TL(s1, 1) ^ GIFT_TL(s2, 2) ^ GIFT_TL(s3, 3) ^ rk[4 * r + 0];
+      const uint32_t t1 = GIFT_TL(s1, 0) ^ GIFT_TL(s2, 1) ^ GIFT_TL(s3, 2) ^ GIFT_TL(s0, 3) ^ rk[4 * r + 1];
+      const uint32_t t2 = GIFT_TL(s2, 0) ^ GIFT_TL(s3, 1) ^ GIFT_TL(s0, 2) ^ GIFT_TL(s1, 3) ^ rk[4 * r + 2];
+      const uint32_t t3 = GIFT_TL(s3, 0) ^ GIFT_TL(s0, 1) ^ GIFT_TL(s1, 2) ^ GIFT_TL(s2, 3) ^ rk[4 * r + 3];
+      s0 = t0;
+      s1 = t1;
+      s2 = t2;
+      s3 = t3;
+    }
+#undef GIFT_TL
+    // last round: S(x) is byte 1 of Te0[x]
+#define GIFT_SL(w, k) (((te[((w) >> (8 * (k))) & 0xffu] >> 8) & 0xffu) << (8 * (k)))
+    const uint32_t e0 = (GIFT_SL(s0, 0) | GIFT_SL(s1, 1) | GIFT_SL(s2, 2) | GIFT_SL(s3, 3)) ^ rk[56];
+    const uint32_t e1 = (GIFT_SL(s1, 0) | GIFT_SL(s2, 1) | GIFT_SL(s3, 2) | GIFT_SL(s0, 3)) ^ rk[57];
+    const uint32_t e2 = (GIFT_SL(s2, 0) | GIFT_SL(s3, 1) | GIFT_SL(s0, 2) | GIFT_SL(s1, 3)) ^ rk[58];
+    const uint32_t e3 = (GIFT_SL(s3, 0) | GIFT_SL(s0, 1) | GIFT_SL(s1, 2) | GIFT_SL(s2, 3)) ^ rk[59];
+#undef GIFT_SL
+    const u128 tag = u128{{e0 ^ z.w[0], e1 ^ z.w[1], e2 ^ z.w[2], e3 ^ z.w[3]}};
     if (!OPEN) {
       uint32_t* to = (uint32_t*)(a.tags_out + 16ull * s);
       for (int j = 0; j < 4; j++) to[j] = tag.w[j];
@@ -564,21 +590,22 @@ __global__ __launch_bounds__(256) void k_check_owner(const SegDesc* __restrict__
 // ---------------------------------------------------------------------------
 // Zero-fill of uncovered rows and of rejected segments.
 // ---------------------------------------------------------------------------
+// Zero-fill of uncovered rows and (open) of segments whose verdict is not OK.
+// The host cuts ranges into pieces of at most kZeroPieceBytes; a workgroup
+// takes whole pieces, so nothing loops over all ranges per thread.
 __global__ __launch_bounds__(256) void k_zero_ranges(uint8_t* out, const ZeroRange* __restrict__ rs, uint32_t n,
                                                      const int32_t* __restrict__ verdicts) {
-  const uint64_t gtid = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const uint64_t gsz = (uint64_t)gridDim.x * blockDim.x;
-  for (uint32_t i = 0; i < n; i++) {
+  for (uint32_t i = blockIdx.x; i < n; i += gridDim.x) {
     const ZeroRange z = rs[i];
     if (z.seg >= 0 && verdicts[z.seg] == kVerdictOk) continue;
     uint8_t* p = out + z.off;
     uint64_t head = (16u - ((uintptr_t)p & 15u)) & 15u;
     if (head > z.len) head = z.len;
-    for (uint64_t b = gtid; b < head; b += gsz) p[b] = 0;
+    for (uint64_t b = threadIdx.x; b < head; b += blockDim.x) p[b] = 0;
     const uint64_t mid = (z.len - head) / 16u;
     uint4* q = (uint4*)(p + head);
-    for (uint64_t k = gtid; k < mid; k += gsz) q[k] = make_uint4(0u, 0u, 0u, 0u);
-    for (uint64_t b = head + 16u * mid + gtid; b < z.len; b += gsz) p[b] = 0;
+    for (uint64_t k = threadIdx.x; k < mid; k += blockDim.x) q[k] = make_uint4(0u, 0u, 0u, 0u);
+    for (uint64_t b = head + 16u * mid + threadIdx.x; b < z.len; b += blockDim.x) p[b] = 0;
   }
 }
 
@@ -653,18 +680,32 @@ __global__ __launch_bounds__(256) void k_chunk_table(const SegDesc* __restrict__
   }
 }
 
+// Open through block tables: zero the chunks of requests whose verdict is not
+// OK.  A workgroup takes whole tiles of kTileBlocks blocks (the GCM kernel's
+// tiles, found through tile_base), so the work per workgroup is bounded.
 __global__ __launch_bounds__(256) void k_zero_chunks(const SegDesc* __restrict__ segs, uint32_t n,
+                                                     const uint32_t* __restrict__ tile_base, uint32_t n_tiles,
                                                      const int32_t* __restrict__ verdicts,
                                                      const uint64_t* __restrict__ chunk_off, uint8_t* pbase,
-                                                     uint64_t chunk_bytes) {
-  const uint64_t gtid = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const uint64_t gsz = (uint64_t)gridDim.x * blockDim.x;
-  const uint64_t per_chunk = chunk_bytes / 16;
-  for (uint32_t s = 0; s < n; s++) {
-    if (verdicts[s] == kVerdictOk) continue;
-    const uint64_t nblk = segs[s].len / 16, c0 = segs[s].chunk0;
-    for (uint64_t i = gtid; i < nblk; i += gsz)
-      *(uint4*)(pbase + chunk_off[c0 + i / per_chunk] + 16 * (i % per_chunk)) = make_uint4(0u, 0u, 0u, 0u);
+                                                     uint32_t chunk_shift) {
+  const uint64_t cmask = (1ull << chunk_shift) - 1;
+  for (uint32_t g = blockIdx.x; g < n_tiles; g += gridDim.x) {
+    uint32_t lo = 0, hi = n;  // tile_base[lo] <= g < tile_base[hi]
+    while (hi - lo > 1) {
+      const uint32_t mid = (lo + hi) >> 1;
+      if (tile_base[mid] <= g)
+        lo = mid;
+      else
+        hi = mid;
+    }
+    if (verdicts[lo] == kVerdictOk) continue;
+    const uint64_t m = segs[lo].nblocks, c0 = segs[lo].chunk0;
+    const uint64_t t = g - tile_base[lo];
+    // tiles are aligned to the end of the segment, as in k_gcm_tiles
+    const uint64_t end = m - t * (uint64_t)kTileBlocks;
+    const uint64_t begin = end > kTileBlocks ? end - kTileBlocks : 0;
+    for (uint64_t i = begin + threadIdx.x; i < end; i += blockDim.x)
+      *(uint4*)(pbase + chunk_off[c0 + (i >> chunk_shift)] + ((i & cmask) << 4)) = make_uint4(0u, 0u, 0u, 0u);
   }
 }
 
@@ -688,7 +729,7 @@ __global__ __launch_bounds__(64) void k_key_sched(const uint8_t* __restrict__ ke
   for (int i = 0; i < 4; i++) kt.h[4ull * u + i] = h[i];
 }
 
-constexpr uint32_t kPowersPerUser = kHPowers + kFinLanes + 1;
+constexpr uint32_t kPowersPerUser = kHPowers + kFinLanes + 1 + kHxLanes;
 
 __global__ __launch_bounds__(256) void k_key_powers(KeyTableDev kt) {
   const uint64_t idx = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -701,8 +742,11 @@ __global__ __launch_bounds__(256) void k_key_powers(KeyTableDev kt) {
   } else if (j < (uint32_t)(kHPowers + kFinLanes)) {
     const uint32_t l = j - kHPowers;
     st_u128(kt.pow_ht + u * kFinLanes + l, gf_pow(h, (uint64_t)l * kTileBlocks));
-  } else {
+  } else if (j == (uint32_t)(kHPowers + kFinLanes)) {
     st_u128(kt.pow_hlt + u, gf_pow(h, (uint64_t)kFinLanes * kTileBlocks));
+  } else {
+    const uint32_t k = j - (kHPowers + kFinLanes + 1);
+    st_u128(kt.pow_hxl + u * kHxLanes + k, gf_mul(h, gf_xpow_elem(64 + (int)k)));
   }
 }
 
@@ -792,6 +836,7 @@ hipError_t launch_gcm_finalize(const GcmArgs& a, bool open, hipStream_t s) {
 hipError_t launch_zero_ranges(uint8_t* out, const ZeroRange* r, uint32_t n, const int32_t* verdicts, uint32_t grid,
                               hipStream_t s) {
   if (n == 0) return hipSuccess;
+  if (grid > n) grid = n;
   hipLaunchKernelGGL(k_zero_ranges, dim3(grid), dim3(256), 0, s, out, r, n, verdicts);
   return hipGetLastError();
 }
@@ -820,12 +865,13 @@ hipError_t launch_chunk_table(const SegDesc* segs, uint32_t n_segs, const uint32
   return hipGetLastError();
 }
 
-hipError_t launch_zero_chunks(const SegDesc* segs, uint32_t n_segs, const int32_t* verdicts,
-                              const uint64_t* chunk_off, uint8_t* pbase, uint64_t chunk_bytes, uint32_t grid,
-                              hipStream_t s) {
-  if (n_segs == 0) return hipSuccess;
-  hipLaunchKernelGGL(k_zero_chunks, dim3(grid), dim3(256), 0, s, segs, n_segs, verdicts, chunk_off, pbase,
-                     chunk_bytes);
+hipError_t launch_zero_chunks(const SegDesc* segs, uint32_t n_segs, const uint32_t* tile_base, uint32_t n_tiles,
+                              const int32_t* verdicts, const uint64_t* chunk_off, uint8_t* pbase,
+                              uint32_t chunk_shift, uint32_t grid, hipStream_t s) {
+  if (n_segs == 0 || n_tiles == 0) return hipSuccess;
+  if (grid > n_tiles) grid = n_tiles;
+  hipLaunchKernelGGL(k_zero_chunks, dim3(grid), dim3(256), 0, s, segs, n_segs, tile_base, n_tiles, verdicts,
+                     chunk_off, pbase, chunk_shift);
   return hipGetLastError();
 }
 
