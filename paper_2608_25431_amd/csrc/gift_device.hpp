@@ -188,29 +188,45 @@ __device__ __forceinline__ u128 u128_xor(const u128& a, const u128& b) {
   return u128{{a.w[0] ^ b.w[0], a.w[1] ^ b.w[1], a.w[2] ^ b.w[2], a.w[3] ^ b.w[3]}};
 }
 
-// General product of two field elements: shift-and-add over the bits of x,
-// with y multiplied by x each step (V -> V >> 1, xor R = 0xE1 || 0^120 on
-// carry).  Computed on big-endian words so that "rightshift of the bit
-// string" is a plain 128-bit right shift.  ~1.4k VALU ops; used only outside
+// General product of two field elements (SP 800-38D Sec. 6.3 defines it bit
+// by bit).  Computed on big-endian words so that "rightshift of the bit
+// string" is a plain 128-bit right shift.  ~0.9k VALU ops; used only outside
 // the per-block loop.
 __device__ inline u128 gf_mul(const u128& x, const u128& y) {
-  uint32_t v0 = bswap32(y.w[0]), v1 = bswap32(y.w[1]), v2 = bswap32(y.w[2]), v3 = bswap32(y.w[3]);
+  // 8-bit comb: V_j = y * x^j for j < 8, then Horner over the bytes of x
+  // from the highest powers down, z <- z * x^8 xor sum_j x_(8n+j) V_j.  In
+  // the MSB-first word order a multiply by x is a right shift by one bit, and
+  // the bits x^128..x^135 that a shift by 8 pushes out fold back as
+  // x^m * (1 + x + x^2 + x^7), i.e. 0xE1 << (17 + k) for pushed-out bit k.
+  uint32_t V[8][4];
+  V[0][0] = bswap32(y.w[0]);
+  V[0][1] = bswap32(y.w[1]);
+  V[0][2] = bswap32(y.w[2]);
+  V[0][3] = bswap32(y.w[3]);
+#pragma unroll
+  for (int j = 1; j < 8; j++) {
+    const uint32_t carry = 0u - (V[j - 1][3] & 1u);
+    V[j][3] = __builtin_amdgcn_alignbit(V[j - 1][2], V[j - 1][3], 1);
+    V[j][2] = __builtin_amdgcn_alignbit(V[j - 1][1], V[j - 1][2], 1);
+    V[j][1] = __builtin_amdgcn_alignbit(V[j - 1][0], V[j - 1][1], 1);
+    V[j][0] = (V[j - 1][0] >> 1) ^ (0xE1000000u & carry);
+  }
   uint32_t z0 = 0, z1 = 0, z2 = 0, z3 = 0;
 #pragma unroll
-  for (int j = 0; j < 4; j++) {
-    uint32_t xw = bswap32(x.w[j]);
-#pragma unroll 8
-    for (int b = 31; b >= 0; b--) {
-      uint32_t m = 0u - ((xw >> b) & 1u);
-      z0 ^= v0 & m;
-      z1 ^= v1 & m;
-      z2 ^= v2 & m;
-      z3 ^= v3 & m;
-      uint32_t carry = 0u - (v3 & 1u);
-      v3 = __builtin_amdgcn_alignbit(v2, v3, 1);
-      v2 = __builtin_amdgcn_alignbit(v1, v2, 1);
-      v1 = __builtin_amdgcn_alignbit(v0, v1, 1);
-      v0 = (v0 >> 1) ^ (0xE1000000u & carry);
+  for (int n = 15; n >= 0; n--) {
+    const uint32_t t = z3 & 0xFFu;
+    z3 = __builtin_amdgcn_alignbit(z2, z3, 8);
+    z2 = __builtin_amdgcn_alignbit(z1, z2, 8);
+    z1 = __builtin_amdgcn_alignbit(z0, z1, 8);
+    z0 = xor3(xor3(z0 >> 8, t << 17, t << 22), t << 23, t << 24);
+    const uint32_t xw = x.w[n >> 2];
+#pragma unroll
+    for (int j = 0; j < 8; j++) {
+      const uint32_t m = 0u - ((xw >> (8 * (n & 3) + 7 - j)) & 1u);  // coefficient of x^(8n+j)
+      z0 ^= V[j][0] & m;
+      z1 ^= V[j][1] & m;
+      z2 ^= V[j][2] & m;
+      z3 ^= V[j][3] & m;
     }
   }
   return u128{{bswap32(z0), bswap32(z1), bswap32(z2), bswap32(z3)}};
