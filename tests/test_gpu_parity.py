@@ -228,6 +228,51 @@ def test_non_default_stream(kt3):
     assert host(out).tobytes() == o_out.tobytes() and host(tags)[:32].tobytes() == o_tags.tobytes()
 
 
+def test_two_threads_on_two_streams_share_a_key_table(kt3):
+    # calls from several host threads, each on its own stream, share one key
+    # table and the library's per-device staging ring
+    import threading
+    keys, nb, kt = kt3
+    n_rows, rb = 96, 65536  # 6 MiB per tensor: multi-tile segments
+    cases = []
+    for i in range(2):
+        cases.append((rng.integers(0, 256, n_rows * rb, dtype=np.uint8),
+                      [(0, 40, i, 100 + i), (40, 56, 2, 200 + i)]))
+    results, errors = [None, None], []
+
+    def work(i):
+        try:
+            data_np, table = cases[i]
+            s = torch.cuda.Stream()
+            outs = []
+            with torch.cuda.stream(s):
+                for _ in range(4):
+                    d = dev_u8(data_np)
+                    out, tags, _ = seal(d, n_rows, rb, table, kt, nb)
+                    back, ver = open_(out, n_rows, rb, table, kt, nb, tags)
+                    outs.append((out, tags, back, ver))
+            s.synchronize()
+            results[i] = [(o.cpu().numpy(), tg.cpu().numpy(), b.cpu().numpy(), v.cpu().numpy())
+                          for o, tg, b, v in outs]
+        except Exception as e:  # surfaced in the main thread
+            errors.append(e)
+
+    threads = [threading.Thread(target=work, args=(i,)) for i in range(2)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert not errors, errors
+    for i, (data_np, table) in enumerate(cases):
+        st, o_out, o_tags, _ = oracle.seal(data_np, n_rows, rb, table, keys, nb)
+        assert st == 0
+        for out, tags, back, ver in results[i]:
+            assert out.tobytes() == o_out.tobytes()
+            assert tags[:32].tobytes() == o_tags.tobytes()
+            assert back.tobytes() == data_np.tobytes()
+            assert ver[:2].tolist() == [gift.SEG_OK, gift.SEG_OK]
+
+
 # --------------------------------------------------------------------------
 # full-size configurations
 # --------------------------------------------------------------------------
