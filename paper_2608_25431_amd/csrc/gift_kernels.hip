@@ -266,16 +266,21 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
 
   for (uint32_t g = blockIdx.x; g < a.n_tiles; g += gridDim.x) {
     __syncthreads();  // previous tile finished with gtab, red and info
-    if (tid == 0) {
+    if (tid < 64) {
+      // 64-way search by wave 0 for the last segment with tile_base <= g:
+      // lane j probes lo + span*j/64, and the highest probe at or below g
+      // narrows [lo, hi) (about two dependent loads for a thousand segments)
       uint32_t lo = 0, hi = a.n_segs;  // tile_base[lo] <= g < tile_base[hi]
       while (hi - lo > 1) {
-        uint32_t mid = (lo + hi) >> 1;
-        if (tile_base[mid] <= g)
-          lo = mid;
-        else
-          hi = mid;
+        const uint64_t span = hi - lo;
+        const uint32_t pos = lo + (uint32_t)((span * tid) >> 6);
+        const uint64_t le = __ballot(tile_base[pos] <= g);  // lane 0 (pos = lo) always set
+        const uint32_t j = 63u - (uint32_t)__clzll(le);
+        const uint32_t nlo = lo + (uint32_t)((span * j) >> 6);
+        if (j < 63u) hi = lo + (uint32_t)((span * (j + 1)) >> 6);
+        lo = nlo;
       }
-      info[0] = lo;
+      if (tid == 0) info[0] = lo;
     }
     __syncthreads();
     const uint32_t s = __builtin_amdgcn_readfirstlane(info[0]);
