@@ -129,6 +129,56 @@ __device__ inline void aes256_encrypt_words(const uint32_t* __restrict__ rk, con
 #undef GIFT_SB
 }
 
+// The same cipher with its table passed in (typically a copy in LDS, where
+// per-lane lookups are cheap, unlike the constant segment): te0 as in
+// AesConst, and S(x) is byte 1 of te0[x].
+__device__ inline void aes256_encrypt_tab(const uint32_t* __restrict__ rk, const uint32_t in[4], uint32_t out[4],
+                                          const uint32_t* te0) {
+  uint32_t s0 = in[0] ^ rk[0], s1 = in[1] ^ rk[1], s2 = in[2] ^ rk[2], s3 = in[3] ^ rk[3];
+#define GIFT_TE(w, k) rotl32(te0[((w) >> (8 * (k))) & 0xffu], 8 * (k))
+  for (int r = 1; r < 14; r++) {
+    const uint32_t t0 = GIFT_TE(s0, 0) ^ GIFT_TE(s1, 1) ^ GIFT_TE(s2, 2) ^ GIFT_TE(s3, 3) ^ rk[4 * r + 0];
+    const uint32_t t1 = GIFT_TE(s1, 0) ^ GIFT_TE(s2, 1) ^ GIFT_TE(s3, 2) ^ GIFT_TE(s0, 3) ^ rk[4 * r + 1];
+    const uint32_t t2 = GIFT_TE(s2, 0) ^ GIFT_TE(s3, 1) ^ GIFT_TE(s0, 2) ^ GIFT_TE(s1, 3) ^ rk[4 * r + 2];
+    const uint32_t t3 = GIFT_TE(s3, 0) ^ GIFT_TE(s0, 1) ^ GIFT_TE(s1, 2) ^ GIFT_TE(s2, 3) ^ rk[4 * r + 3];
+    s0 = t0;
+    s1 = t1;
+    s2 = t2;
+    s3 = t3;
+  }
+#undef GIFT_TE
+#define GIFT_SB(w, k) (((te0[((w) >> (8 * (k))) & 0xffu] >> 8) & 0xffu) << (8 * (k)))
+  out[0] = (GIFT_SB(s0, 0) | GIFT_SB(s1, 1) | GIFT_SB(s2, 2) | GIFT_SB(s3, 3)) ^ rk[56];
+  out[1] = (GIFT_SB(s1, 0) | GIFT_SB(s2, 1) | GIFT_SB(s3, 2) | GIFT_SB(s0, 3)) ^ rk[57];
+  out[2] = (GIFT_SB(s2, 0) | GIFT_SB(s3, 1) | GIFT_SB(s0, 2) | GIFT_SB(s1, 3)) ^ rk[58];
+  out[3] = (GIFT_SB(s3, 0) | GIFT_SB(s0, 1) | GIFT_SB(s1, 2) | GIFT_SB(s2, 3)) ^ rk[59];
+#undef GIFT_SB
+}
+
+// Equivalent inverse cipher with td0 and the inverse S-box passed in.
+__device__ inline void aes256_decrypt_tab(const uint32_t* __restrict__ dk, const uint32_t in[4], uint32_t out[4],
+                                          const uint32_t* td0, const uint8_t* isb) {
+  uint32_t s0 = in[0] ^ dk[56], s1 = in[1] ^ dk[57], s2 = in[2] ^ dk[58], s3 = in[3] ^ dk[59];
+#define GIFT_TD(w, k) rotl32(td0[((w) >> (8 * (k))) & 0xffu], 8 * (k))
+  for (int r = 13; r >= 1; r--) {
+    const uint32_t t0 = GIFT_TD(s0, 0) ^ GIFT_TD(s3, 1) ^ GIFT_TD(s2, 2) ^ GIFT_TD(s1, 3) ^ dk[4 * r + 0];
+    const uint32_t t1 = GIFT_TD(s1, 0) ^ GIFT_TD(s0, 1) ^ GIFT_TD(s3, 2) ^ GIFT_TD(s2, 3) ^ dk[4 * r + 1];
+    const uint32_t t2 = GIFT_TD(s2, 0) ^ GIFT_TD(s1, 1) ^ GIFT_TD(s0, 2) ^ GIFT_TD(s3, 3) ^ dk[4 * r + 2];
+    const uint32_t t3 = GIFT_TD(s3, 0) ^ GIFT_TD(s2, 1) ^ GIFT_TD(s1, 2) ^ GIFT_TD(s0, 3) ^ dk[4 * r + 3];
+    s0 = t0;
+    s1 = t1;
+    s2 = t2;
+    s3 = t3;
+  }
+#undef GIFT_TD
+#define GIFT_ISB(w, k) ((uint32_t)isb[((w) >> (8 * (k))) & 0xffu] << (8 * (k)))
+  out[0] = (GIFT_ISB(s0, 0) | GIFT_ISB(s3, 1) | GIFT_ISB(s2, 2) | GIFT_ISB(s1, 3)) ^ dk[0];
+  out[1] = (GIFT_ISB(s1, 0) | GIFT_ISB(s0, 1) | GIFT_ISB(s3, 2) | GIFT_ISB(s2, 3)) ^ dk[1];
+  out[2] = (GIFT_ISB(s2, 0) | GIFT_ISB(s1, 1) | GIFT_ISB(s0, 2) | GIFT_ISB(s3, 3)) ^ dk[2];
+  out[3] = (GIFT_ISB(s3, 0) | GIFT_ISB(s2, 1) | GIFT_ISB(s1, 2) | GIFT_ISB(s0, 3)) ^ dk[3];
+#undef GIFT_ISB
+}
+
 // InvMixColumns of one column word (FIPS-197 Sec. 5.3.3), used to derive the
 // round keys of the equivalent inverse cipher (Sec. 5.3.5).
 __device__ inline uint32_t inv_mix_column(uint32_t w) {

@@ -185,17 +185,28 @@ gift_status check_segments(const gift_segment* segs, uint32_t n, uint64_t n_rows
   if (n > 1) {
     std::vector<std::pair<uint64_t, uint64_t>> v(n);
     for (uint32_t i = 0; i < n; i++) v[i] = {segs[i].row_begin, segs[i].row_count};
-    std::sort(v.begin(), v.end());
+    // tables usually arrive in row order: sort only when they do not
+    if (!std::is_sorted(v.begin(), v.end())) std::sort(v.begin(), v.end());
     for (uint32_t i = 1; i < n; i++)
       if (v[i].first < v[i - 1].first + v[i - 1].second)
         return fail(GIFT_E_OVERLAP, "segments overlap at row %llu", (unsigned long long)v[i].first);
     if (gcm) {
-      for (uint32_t i = 0; i < n; i++) v[i] = {segs[i].user, segs[i].iv_seq};
-      std::sort(v.begin(), v.end());
-      for (uint32_t i = 1; i < n; i++)
-        if (v[i] == v[i - 1])
-          return fail(GIFT_E_NONCE_REUSE, "two segments share user %llu and iv_seq %llu",
-                      (unsigned long long)v[i].first, (unsigned long long)v[i].second);
+      // a reuse needs a user that owns two segments; with every user once
+      // (a bitmap over the key set) there is nothing to sort
+      bool repeat = true;  // (a key set far larger than the table: just sort)
+      if ((uint64_t)n_users <= 64ull * n + 4096) {
+        std::vector<uint8_t> seen(n_users, 0);
+        repeat = false;
+        for (uint32_t i = 0; i < n && !repeat; i++) repeat = seen[segs[i].user]++ != 0;
+      }
+      if (repeat) {
+        for (uint32_t i = 0; i < n; i++) v[i] = {segs[i].user, segs[i].iv_seq};
+        std::sort(v.begin(), v.end());
+        for (uint32_t i = 1; i < n; i++)
+          if (v[i] == v[i - 1])
+            return fail(GIFT_E_NONCE_REUSE, "two segments share user %llu and iv_seq %llu",
+                        (unsigned long long)v[i].first, (unsigned long long)v[i].second);
+      }
     }
   }
   return GIFT_OK;
@@ -235,7 +246,7 @@ void build_plan(const gift_segment* segs, uint32_t n, uint64_t n_rows, uint64_t 
       P.n_tiles += (uint32_t)((nb + kTileBlocks - 1) / kTileBlocks);
     cover[i] = {s.row_begin, s.row_count};
   }
-  std::sort(cover.begin(), cover.end());
+  if (!std::is_sorted(cover.begin(), cover.end())) std::sort(cover.begin(), cover.end());
   uint64_t cur = 0;
   for (auto& c : cover) {
     if (c.first > cur) P.zr.push_back(ZeroRange{cur * row_bytes, (c.first - cur) * row_bytes, -1, {0, 0, 0}});
@@ -790,9 +801,13 @@ static gift_status run_tokens(bool decrypt, const gift_segment_table* st, uint64
     Staging* sg = staging_for(dev);
     e = sg ? sg->upload(d, P.descs.data(), sizeof(SegDesc) * n, stream) : hipErrorInvalidDevice;
   }
-  // uncovered tokens: zero output
-  if (e == hipSuccess) e = decrypt ? launch_wipe(tokens_out, 8ull * n_tokens, stream) : launch_wipe(blocks_out, 16ull * n_tokens, stream);
-  if (e == hipSuccess && decrypt && nonces_out) e = launch_wipe(nonces_out, 8ull * n_tokens, stream);
+  // uncovered tokens (rows no segment covers) get zero output: only when the
+  // plan has such gaps is the output cleared first, the token kernel then
+  // overwrites every covered entry
+  const bool gaps = !P.zr.empty();
+  if (e == hipSuccess && gaps)
+    e = decrypt ? launch_wipe(tokens_out, 8ull * n_tokens, stream) : launch_wipe(blocks_out, 16ull * n_tokens, stream);
+  if (e == hipSuccess && gaps && decrypt && nonces_out) e = launch_wipe(nonces_out, 8ull * n_tokens, stream);
   if (e == hipSuccess)
     e = launch_tokens(d, n, decrypt, tokens, nonces, blocks_in, blocks_out, tokens_out, nonces_out, eos_token, kt->dev,
                       stream);

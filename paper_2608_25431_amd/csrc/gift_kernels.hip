@@ -404,7 +404,7 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
 // Per-segment finalize of tiled segments: S = sum_t P_t H^(tT) xor H*L and
 // tag = E_K(J0) xor S.  One wave per segment; lane l folds tiles l, l+64, ...
 // H*L is a wave sum over the set bits of L (only its low 64 bits can be set)
-// of the products H*x^(64+k); E_K(J0) uses a T-table copy in LDS.
+// of the products H*x^(64+k); E_K(J0) reads a T-table copy in LDS.
 // ---------------------------------------------------------------------------
 template <bool OPEN>
 __global__ __launch_bounds__(kFinLanes) void k_finalize(GcmArgs a) {
@@ -438,28 +438,10 @@ __global__ __launch_bounds__(kFinLanes) void k_finalize(GcmArgs a) {
 #pragma unroll
   for (int j = 0; j < 4; j++) z.w[j] = wave_xor(z.w[j]);
   if (lane == 0) {
-    const uint32_t* rk = a.kt.rk + (size_t)user * 64u;
-    uint32_t s0 = sd.iv[0] ^ rk[0], s1 = sd.iv[1] ^ rk[1], s2 = sd.iv[2] ^ rk[2], s3 = 0x01000000u ^ rk[3];
-#define GIFT_TL(w, k) rotl32(te[((w) >> (8 * (k))) & 0xffu], 8 * (k))
-    for (int r = 1; r < 14; r++) {
-      const uint32_t t0 = GIFT_TL(s0, 0) ^ GIFT_TL(s1, 1) ^ GIFT_TL(s2, 2) ^ GIFT_TL(s3, 3) ^ rk[4 * r + 0];
-      const uint32_t t1 = GIFT_TL(s1, 0) ^ GIFT_TL(s2, 1) ^ GIFT_TL(s3, 2) ^ GIFT_TL(s0, 3) ^ rk[4 * r + 1];
-      const uint32_t t2 = GIFT_TL(s2, 0) ^ GIFT_TL(s3, 1) ^ GIFT_TL(s0, 2) ^ GIFT_TL(s1, 3) ^ rk[4 * r + 2];
-      const uint32_t t3 = GIFT_TL(s3, 0) ^ GIFT_TL(s0, 1) ^ GIFT_TL(s1, 2) ^ GIFT_TL(s2, 3) ^ rk[4 * r + 3];
-      s0 = t0;
-      s1 = t1;
-      s2 = t2;
-      s3 = t3;
-    }
-#undef GIFT_TL
-    // last round: S(x) is byte 1 of Te0[x]
-#define GIFT_SL(w, k) (((te[((w) >> (8 * (k))) & 0xffu] >> 8) & 0xffu) << (8 * (k)))
-    const uint32_t e0 = (GIFT_SL(s0, 0) | GIFT_SL(s1, 1) | GIFT_SL(s2, 2) | GIFT_SL(s3, 3)) ^ rk[56];
-    const uint32_t e1 = (GIFT_SL(s1, 0) | GIFT_SL(s2, 1) | GIFT_SL(s3, 2) | GIFT_SL(s0, 3)) ^ rk[57];
-    const uint32_t e2 = (GIFT_SL(s2, 0) | GIFT_SL(s3, 1) | GIFT_SL(s0, 2) | GIFT_SL(s1, 3)) ^ rk[58];
-    const uint32_t e3 = (GIFT_SL(s3, 0) | GIFT_SL(s0, 1) | GIFT_SL(s1, 2) | GIFT_SL(s2, 3)) ^ rk[59];
-#undef GIFT_SL
-    const u128 tag = u128{{e0 ^ z.w[0], e1 ^ z.w[1], e2 ^ z.w[2], e3 ^ z.w[3]}};
+    const uint32_t j0[4] = {sd.iv[0], sd.iv[1], sd.iv[2], 0x01000000u};
+    uint32_t e[4];
+    aes256_encrypt_tab(a.kt.rk + (size_t)user * 64u, j0, e, te);
+    const u128 tag = u128{{e[0] ^ z.w[0], e[1] ^ z.w[1], e[2] ^ z.w[2], e[3] ^ z.w[3]}};
     if (!OPEN) {
       uint32_t* to = (uint32_t*)(a.tags_out + 16ull * s);
       for (int j = 0; j < 4; j++) to[j] = tag.w[j];
@@ -480,6 +462,9 @@ __global__ __launch_bounds__(kFinLanes) void k_finalize(GcmArgs a) {
 // ---------------------------------------------------------------------------
 template <bool OPEN>
 __global__ __launch_bounds__(64) void k_small(GcmArgs a) {
+  __shared__ uint32_t te[256];
+  for (uint32_t i = threadIdx.x; i < 256u; i += 64u) te[i] = c_aes.te0[i];
+  __syncthreads();
   const uint32_t s = a.small_list[blockIdx.x];
   const uint32_t j = threadIdx.x;
   const SegDesc sd = a.segs[s];
@@ -502,7 +487,7 @@ __global__ __launch_bounds__(64) void k_small(GcmArgs a) {
     in = load_block(a.in + sd.byte_off + 16ull * j, n, aligned);
     const uint32_t cb[4] = {sd.iv[0], sd.iv[1], sd.iv[2], bswap32(2u + j)};
     uint32_t ks[4];
-    aes256_encrypt_words(rk, cb, ks, c_aes);
+    aes256_encrypt_tab(rk, cb, ks, te);
     o = mask_block(u128{{in.w[0] ^ ks[0], in.w[1] ^ ks[1], in.w[2] ^ ks[2], in.w[3] ^ ks[3]}}, n);
     const u128 x = OPEN ? in : o;
     z = gf_mul(x, ld_u128(a.kt.pow_h + (size_t)user * kHPowers + (m + 1 - j)));
@@ -515,7 +500,7 @@ __global__ __launch_bounds__(64) void k_small(GcmArgs a) {
   if (j == 0) {
     const uint32_t j0[4] = {sd.iv[0], sd.iv[1], sd.iv[2], 0x01000000u};
     uint32_t e[4];
-    aes256_encrypt_words(rk, j0, e, c_aes);
+    aes256_encrypt_tab(rk, j0, e, te);
     const u128 tag = u128{{e[0] ^ z.w[0], e[1] ^ z.w[1], e[2] ^ z.w[2], e[3] ^ z.w[3]}};
     if (!OPEN) {
       uint32_t* to = (uint32_t*)(a.tags_out + 16ull * s);
@@ -631,6 +616,13 @@ __global__ __launch_bounds__(64) void k_tokens(const SegDesc* __restrict__ segs,
                                                const uint8_t* __restrict__ blocks_in, uint8_t* __restrict__ blocks_out,
                                                uint64_t* __restrict__ tokens_out, uint64_t* __restrict__ nonces_out,
                                                uint64_t eos_token, KeyTableDev kt) {
+  __shared__ uint32_t tab[256];
+  __shared__ uint8_t isb[256];
+  for (uint32_t i = threadIdx.x; i < 256u; i += blockDim.x) {
+    tab[i] = DECRYPT ? c_aes.td0[i] : c_aes.te0[i];
+    isb[i] = c_aes.inv_sbox[i];
+  }
+  __syncthreads();
   for (uint32_t s = blockIdx.x; s < n_segs; s += gridDim.x) {
     const uint64_t rb = segs[s].row_begin, rc = segs[s].row_count;
     const uint32_t user = segs[s].user;
@@ -643,7 +635,7 @@ __global__ __launch_bounds__(64) void k_tokens(const SegDesc* __restrict__ segs,
           o[0] = o[1] = o[2] = o[3] = 0xFFFFFFFFu;
         } else {
           const uint32_t blk[4] = {(uint32_t)t, (uint32_t)(t >> 32), (uint32_t)n, (uint32_t)(n >> 32)};
-          aes256_encrypt_words(kt.rk + 64ull * user, blk, o, c_aes);
+          aes256_encrypt_tab(kt.rk + 64ull * user, blk, o, tab);
         }
         *(uint4*)(blocks_out + 16ull * r) = make_uint4(o[0], o[1], o[2], o[3]);
       } else {
@@ -655,7 +647,7 @@ __global__ __launch_bounds__(64) void k_tokens(const SegDesc* __restrict__ segs,
         } else {
           const uint32_t blk[4] = {b.x, b.y, b.z, b.w};
           uint32_t p[4];
-          aes256_decrypt_words(kt.dk + 64ull * user, blk, p, c_aes);
+          aes256_decrypt_tab(kt.dk + 64ull * user, blk, p, tab, isb);
           t = (uint64_t)p[0] | ((uint64_t)p[1] << 32);
           n = (uint64_t)p[2] | ((uint64_t)p[3] << 32);
         }
