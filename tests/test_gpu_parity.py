@@ -210,6 +210,57 @@ def test_validation_status_matches_oracle(kt3):
     assert status_of(gift.open, big, n_rows, rb, [(0, 1, 0, 0)], kt, nb, big, tags, None) == gift.E_INVALID
 
 
+def random_table(r, n_rows, n_users):
+    """A small segment table that is valid or breaks one rule at random."""
+    n = int(r.integers(0, 7))
+    table, used = [], set()
+    for _ in range(n):
+        rb_ = int(r.integers(0, n_rows))
+        rc = int(r.integers(1, n_rows - rb_ + 1))
+        table.append([rb_, rc, int(r.integers(0, n_users)), int(r.integers(0, 4)), 0])
+    if table and r.random() < 0.6:  # one defect
+        i = int(r.integers(0, len(table)))
+        kind = int(r.integers(0, 7))
+        if kind == 0:
+            table[i][1] = 0                                       # empty
+        elif kind == 1:
+            table[i][4] = 1                                       # reserved != 0
+        elif kind == 2:
+            table[i][2] = int(r.choice([gift.LABEL_PARAM, gift.LABEL_UNOWNED]))
+        elif kind == 3:
+            table[i][2] = n_users + int(r.integers(0, 3))         # user beyond the key set
+        elif kind == 4:
+            table[i][0] = n_rows + int(r.integers(0, 3))          # rows beyond the tensor
+        elif kind == 5:
+            table[i][1] = n_rows + 1 - table[i][0] + int(r.integers(0, 3))
+        else:
+            j = int(r.integers(0, len(table)))                    # a (user, iv_seq) twin
+            table[i][2], table[i][3] = table[j][2], table[j][3]
+    return [tuple(t) for t in table]
+
+
+def test_random_tables_status_and_output_match_oracle(kt3):
+    # overlapping rows, gaps, defects of every kind: the status is the
+    # oracle's, and when the call is valid so is every byte of the result
+    keys, nb, kt = kt3
+    r = np.random.default_rng(77)
+    n_ok = 0
+    for case in range(300):
+        n_rows, rb = int(r.integers(1, 9)), int(r.choice([4, 16, 20, 48]))
+        table = random_table(r, n_rows, 3)
+        data = r.integers(0, 256, n_rows * rb, dtype=np.uint8)
+        st_o, o_out, o_tags, o_ver = oracle.seal(data, n_rows, rb, table, keys, nb)
+        d = dev_u8(data)
+        st_g = status_of(seal, d, n_rows, rb, table, kt, nb)
+        assert st_g == st_o, (case, table)
+        if st_o == 0:
+            n_ok += 1
+            out, tags, _ = seal(d, n_rows, rb, table, kt, nb)
+            assert host(out).tobytes() == o_out.tobytes(), (case, table)
+            assert host(tags)[:16 * len(table)].tobytes() == o_tags.tobytes(), (case, table)
+    assert n_ok > 50
+
+
 def test_wrong_key_table_fails_every_segment(kt3):
     keys, nb, kt = kt3
     keys2, _ = keyset(3)
