@@ -145,7 +145,10 @@ gift_status gift_race_wait(gift_race h, uint32_t stream, uint32_t on_stream, uin
  * synchronisation, a blocking copy on that stream), and so is every kernel the
  * stream has waited on. */
 gift_status gift_race_sync(gift_race h, uint32_t stream);
-/* Every kernel launched so far is complete (device synchronisation). */
+/* Every kernel launched so far is complete (device synchronisation).  No
+ * recorded access can conflict with a later launch any more, so the per-range
+ * records are dropped here: memory stays bounded in a long-running server
+ * that synchronises the device now and then. */
 gift_status gift_race_sync_all(gift_race h);
 /* The range was freed: its records are dropped. */
 gift_status gift_race_release(gift_race h, gift_range r);

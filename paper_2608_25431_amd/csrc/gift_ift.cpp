@@ -74,6 +74,13 @@ struct gift_race_s {
     }
     return c;
   }
+  // Views recorded for kernels that are now complete are never needed again
+  // except the newest one, which still applies to later sequence numbers.
+  static void prune(Stream& st) {
+    size_t keep = 0;
+    while (keep + 1 < st.history.size() && st.history[keep + 1].first <= st.completed) keep++;
+    if (keep > 0) st.history.erase(st.history.begin(), st.history.begin() + (ptrdiff_t)keep);
+  }
   // has kernel a finished before the next kernel launched on `stream` starts?
   bool ordered(const Access& a, uint32_t stream) {
     if (a.stream == stream) return true;
@@ -409,12 +416,20 @@ gift_status gift_race_sync(gift_race h, uint32_t stream) {
     uint64_t& c = h->streams[kv.first].completed;
     c = std::max(c, kv.second);
   }
+  for (auto& kv : h->streams) gift_race_s::prune(kv.second);
   return GIFT_OK;
 }
 
 gift_status gift_race_sync_all(gift_race h) {
   if (!h) return GIFT_E_INVALID;
-  for (auto& kv : h->streams) kv.second.completed = kv.second.issued;
+  // every recorded access has finished, so none can conflict with a later
+  // launch: the records and the stream views are dropped (sequence numbers go on)
+  for (auto& kv : h->streams) {
+    kv.second.completed = kv.second.issued;
+    kv.second.view.clear();
+    kv.second.history.clear();
+  }
+  h->ivs.clear();
   return GIFT_OK;
 }
 
