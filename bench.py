@@ -303,8 +303,9 @@ def main():
                     help="run one plain 1 GiB device-to-device copy first (scales HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU: this build has no multi-GPU path (segments shard with no "
-              "exchange; see the design notes)", file=sys.stderr)
+        print("bench.py measures one GPU (--gpus 1). Segments are independent GCM messages: several GPUs "
+              "each seal the segments whose data they hold, with no exchange, so there is no multi-GPU run "
+              "to time here.", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
