@@ -675,7 +675,8 @@ gift_status gift_key_table_create(const uint8_t* keys, uint32_t n_users, hipStre
   const size_t o_dk = o_rk + align256(u * 64 * 4);
   const size_t o_h = o_dk + align256(u * 64 * 4);
   const size_t o_gt = o_h + align256(u * 16);
-  const size_t o_ph = o_gt + align256(u * 512 * 16);
+  const size_t o_gf = o_gt + align256(u * 512 * 16);
+  const size_t o_ph = o_gf + align256(u * 512 * 16);
   const size_t o_pt = o_ph + align256(u * kHPowers * 16);
   const size_t o_pl = o_pt + align256(u * kFinLanes * 16);
   const size_t o_px = o_pl + align256(u * 16);
@@ -698,6 +699,7 @@ gift_status gift_key_table_create(const uint8_t* keys, uint32_t n_users, hipStre
   kt->dev.dk = (uint32_t*)(mem + o_dk);
   kt->dev.h = (uint32_t*)(mem + o_h);
   kt->dev.gtab = (uint4*)(mem + o_gt);
+  kt->dev.gtab_fold = (uint4*)(mem + o_gf);
   kt->dev.pow_h = (uint4*)(mem + o_ph);
   kt->dev.pow_ht = (uint4*)(mem + o_pt);
   kt->dev.pow_hlt = (uint4*)(mem + o_pl);

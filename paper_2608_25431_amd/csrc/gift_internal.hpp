@@ -24,6 +24,10 @@ constexpr uint32_t kSmallMaxBlocks = 64;                   // segments up to 1 K
 constexpr int kHPowers = kThreads + 2;                     // H^0 .. H^(kThreads+1) per user
 constexpr int kHxLanes = 64;                               // H * x^(64+k), k < 64, per user
 constexpr int kFinLanes = 64;                              // lanes of the per-segment finalize
+// Tile end of the per-block kernel: one leader wave per SIMD folds the lane
+// partials of kThreads / 64 / kLeaders waves with W = H^(64 * kLeaders).
+constexpr int kLeaders = 4;
+static_assert(kThreads % (64 * kLeaders) == 0, "waves per leader");
 
 enum : uint32_t { kSegAligned = 1u, kSegSmall = 2u };
 
@@ -58,6 +62,7 @@ struct KeyTableDev {
   uint32_t* dk;      // [n_users][64] equivalent-inverse-cipher round keys (60 used)
   uint32_t* h;       // [n_users][4]  H = E_K(0^128)
   uint4* gtab;       // [n_users][32][16] 4-bit GHASH tables of M = H^kThreads
+  uint4* gtab_fold;  // [n_users][32][16] 4-bit GHASH tables of W = H^(64 * kLeaders)
   uint4* pow_h;      // [n_users][kHPowers] H^k
   uint4* pow_ht;     // [n_users][kFinLanes] H^(k * kTileBlocks)
   uint4* pow_hlt;    // [n_users] H^(kFinLanes * kTileBlocks)

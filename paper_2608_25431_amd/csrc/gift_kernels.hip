@@ -13,7 +13,9 @@
 // from the segment's last block contributes X*H^(d + 2) to the GHASH sum; a
 // tile t contributes P_t * H^(t*T) with P_t = sum of X*H^(d_t + 2) over its
 // own blocks (d_t: distance from the tile's end), and lane l of a full tile
-// ends at distance (1023 - l) from the tile's end.
+// ends at distance (1023 - l) from the tile's end.  At tile end one leader
+// wave per SIMD folds the lane partials of four waves with LDS tables of
+// H^256 and applies the remaining per-lane power with one generic multiply.
 #include <hip/hip_runtime.h>
 
 #include "gift_device.hpp"
@@ -26,11 +28,14 @@ __constant__ AesConst c_aes = make_aes_const();
 constexpr int32_t kVerdictOk = 0, kVerdictAuthFail = 1, kVerdictOwnerMixed = 2;
 
 // LDS layout of k_gcm_tiles (bytes).
-constexpr uint32_t kLdsGtab = 0;                    // 32 x 16 x 16 B GHASH tables
+constexpr uint32_t kLdsGtab = 0;                    // 32 x 16 x 16 B GHASH tables of M
 constexpr uint32_t kLdsAes = 8192;                  // T0/T1 (64 KiB) then T2/T3 (64 KiB)
-constexpr uint32_t kLdsRed = kLdsAes + 131072;      // one 16 B slot per wave
-constexpr uint32_t kLdsInfo = kLdsRed + 16 * (kThreads / 64);  // broadcast scratch
+constexpr uint32_t kLdsFold = kLdsAes + 131072;     // 32 x 16 x 16 B GHASH tables of W
+constexpr uint32_t kLdsStage = kLdsFold + 8192;     // lane partials of the waves that are not leaders
+constexpr uint32_t kLdsRed = kLdsStage + 16 * (kThreads - 64 * kLeaders);  // one 16 B slot per leader
+constexpr uint32_t kLdsInfo = kLdsRed + 16 * kLeaders;  // broadcast scratch
 constexpr uint32_t kLdsBytes = kLdsInfo + 16;
+static_assert(kLdsBytes <= 160u * 1024u, "LDS of a gfx950 workgroup");
 
 __device__ __forceinline__ uint32_t lds32(const uint8_t* base, uint32_t off) {
   return *(const uint32_t*)(base + off);
@@ -235,6 +240,20 @@ __device__ __forceinline__ u128 length_block(uint64_t len) {
   return u128{{0u, 0u, bswap32((uint32_t)(bits >> 32)), bswap32((uint32_t)bits)}};
 }
 
+// Tile end of a leader wave (see k_gcm_tiles): Horner over the staged lane
+// partials of its waves in W (LDS tables wt), one multiply by the lane's
+// power, then the wave sum into *red.  Kept out of line so that the main
+// loop's register allocation does not see it.
+__device__ __noinline__ void tile_fold(u128 v, const u128* stage, const uint8_t* wt, const uint4* hpow, u128* red,
+                                       uint32_t lane) {
+  constexpr int kFold = kThreads / 64 / kLeaders;
+  for (int i = 1; i < kFold; i++) v = ghash_step_lds(v, stage[64u * kLeaders * (i - 1)], wt);
+  u128 z = gf_mul(v, ld_u128(hpow));
+#pragma unroll
+  for (int j = 0; j < 4; j++) z.w[j] = wave_xor(z.w[j]);
+  if (lane == 0) *red = z;
+}
+
 // ---------------------------------------------------------------------------
 // Per-block kernel over 2 MiB tiles of the non-small segments.
 // ---------------------------------------------------------------------------
@@ -316,7 +335,11 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
 
     if (user != cur_user) {
       const uint4* src = a.kt.gtab + (size_t)user * 512u;
-      for (uint32_t i = tid; i < 512u; i += kThreads) ((uint4*)(smem + kLdsGtab))[i] = src[i];
+      const uint4* srcw = a.kt.gtab_fold + (size_t)user * 512u;
+      for (uint32_t i = tid; i < 512u; i += kThreads) {
+        ((uint4*)(smem + kLdsGtab))[i] = src[i];
+        ((uint4*)(smem + kLdsFold))[i] = srcw[i];
+      }
       cur_user = user;
       __syncthreads();
     }
@@ -384,17 +407,23 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
       y = ghash_step_lds(y, x, gt);
     }
 
-    // lane contribution y * H^(1023 - tid) times the H^2 that every block's
-    // GHASH term carries, then the workgroup sum
-    const u128 hp = ld_u128(a.kt.pow_h + (size_t)user * kHPowers + (kThreads + 1 - tid));
-    u128 z = gf_mul(y, hp);
-#pragma unroll
-    for (int j = 0; j < 4; j++) z.w[j] = wave_xor(z.w[j]);
-    if ((tid & 63u) == 0) red[tid >> 6] = z;
+    // Tile partial: lane tid contributes y * H^(kThreads + 1 - tid), its
+    // distance from the tile end plus the H^2 that every block's GHASH term
+    // carries.  Wave w = g + kLeaders*i (leader g, i < kFold) needs
+    // H^(64*kLeaders*(kFold - 1 - i)) * H^(64*kLeaders + 1 - 64*g - lane): leader
+    // g folds its waves by Horner in W = H^(64*kLeaders) from the LDS tables,
+    // then multiplies once by the per-lane power.
+    const uint32_t wave = tid >> 6, lane = tid & 63u;
+    u128* stage = (u128*)(smem + kLdsStage);
+    if (wave >= (uint32_t)kLeaders) stage[tid - 64u * kLeaders] = y;
+    __syncthreads();
+    if (wave < (uint32_t)kLeaders)
+      tile_fold(y, stage + (wave * 64u + lane), smem + kLdsFold,
+                a.kt.pow_h + (size_t)user * kHPowers + (64u * kLeaders + 1u - 64u * wave - lane), red + wave, lane);
     __syncthreads();
     if (tid == 0) {
       u128 p = red[0];
-      for (int w = 1; w < kThreads / 64; w++) p = u128_xor(p, red[w]);
+      for (int w = 1; w < kLeaders; w++) p = u128_xor(p, red[w]);
       st_u128(a.partials + g, p);
     }
   }
@@ -747,22 +776,25 @@ __global__ __launch_bounds__(256) void k_key_powers(KeyTableDev kt) {
   }
 }
 
-// Nibble tables of M = H^kThreads: entry [q][v] = (v placed at GCM bits
-// 4q..4q+3, MSB first) * M, built from the four products x^(4q+k) * M.
+// Nibble tables of M = H^kThreads (gtab) and W = H^(64 * kLeaders)
+// (gtab_fold): entry [q][v] = (v placed at GCM bits 4q..4q+3, MSB first) * M,
+// built from the four products x^(4q+k) * M.
 __global__ __launch_bounds__(256) void k_key_gtab(KeyTableDev kt) {
   const uint64_t idx = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const uint64_t u = idx / 32u;
+  const uint64_t u = idx / 64u;
   const int q = (int)(idx % 32u);
+  const bool fold = (idx % 64u) >= 32u;
   if (u >= kt.n_users) return;
   const u128 h = ld_u128((const uint4*)(kt.h + 4ull * u));
-  const u128 mm = gf_pow(h, (uint64_t)kThreads);
+  const u128 mm = gf_pow(h, fold ? (uint64_t)(64 * kLeaders) : (uint64_t)kThreads);
+  uint4* tab = (fold ? kt.gtab_fold : kt.gtab) + u * 512u;
   u128 b[4];
   for (int k = 0; k < 4; k++) b[k] = gf_mul(gf_xpow_elem(4 * q + k), mm);
   for (int v = 0; v < 16; v++) {
     u128 e = u128_zero();
     for (int k = 0; k < 4; k++)
       if (v & (8 >> k)) e = u128_xor(e, b[k]);
-    st_u128(kt.gtab + u * 512u + (uint64_t)q * 16u + v, e);
+    st_u128(tab + (uint64_t)q * 16u + v, e);
   }
 }
 
@@ -778,7 +810,7 @@ hipError_t launch_key_setup(const uint8_t* keys_dev, KeyTableDev kt, hipStream_t
   hipLaunchKernelGGL(k_key_powers, dim3(cdiv((uint64_t)kt.n_users * kPowersPerUser, 256)), dim3(256), 0, s, kt);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_key_gtab, dim3(cdiv((uint64_t)kt.n_users * 32u, 256)), dim3(256), 0, s, kt);
+  hipLaunchKernelGGL(k_key_gtab, dim3(cdiv((uint64_t)kt.n_users * 64u, 256)), dim3(256), 0, s, kt);
   return hipGetLastError();
 }
 
