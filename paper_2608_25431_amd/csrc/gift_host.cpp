@@ -19,6 +19,43 @@
 
 using namespace gift;
 
+namespace gift {
+
+// Longest tiles first, so that a work queue over them ends with short tiles:
+// a counting sort by the number of rows each tile runs (the kernel's tiles
+// are aligned to the segment end, so only a segment's first tile is partial).
+void tile_order(const SegDesc* descs, uint32_t n_segs, uint32_t n_tiles, uint32_t* order) {
+  std::vector<uint32_t> count(kRows + 2, 0);
+  auto rows_of = [](uint64_t m, uint32_t t) -> uint32_t {
+    const int64_t base = (int64_t)m - (int64_t)(t + 1) * (int64_t)kTileBlocks;
+    return base >= 0 ? (uint32_t)kRows : (uint32_t)kRows - (uint32_t)((uint64_t)(-base) / kThreads);
+  };
+  for (uint32_t i = 0; i < n_segs; i++) {
+    if (descs[i].flags & kSegSmall) continue;
+    const uint64_t m = descs[i].nblocks;
+    const uint32_t nt = (uint32_t)((m + kTileBlocks - 1) / kTileBlocks);
+    count[kRows] += nt - 1;
+    count[rows_of(m, nt - 1)]++;
+  }
+  // start of each row count's run, longest first
+  std::vector<uint32_t> pos(kRows + 2, 0);
+  uint32_t acc = 0;
+  for (int r = kRows; r >= 0; r--) {
+    pos[r] = acc;
+    acc += count[r];
+  }
+  (void)n_tiles;
+  uint32_t g = 0;
+  for (uint32_t i = 0; i < n_segs; i++) {
+    if (descs[i].flags & kSegSmall) continue;
+    const uint64_t m = descs[i].nblocks;
+    const uint32_t nt = (uint32_t)((m + kTileBlocks - 1) / kTileBlocks);
+    for (uint32_t t = 0; t < nt; t++, g++) order[pos[rows_of(m, t)]++] = g;
+  }
+}
+
+}  // namespace gift
+
 struct gift_key_table_s {
   int device;
   uint32_t n_users;
@@ -303,14 +340,16 @@ gift_status run_gcm(const gift_tensor* t, const gift_segment_table* st, gift_key
   Plan P;
   build_plan(st->segs, n, t->n_rows, t->row_bytes, nonce_base, t->data, out, OPEN, P);
 
-  // scratch: descs | zero ranges | tile_base | small_list | partials | verdicts
+  // scratch: descs | zero ranges | tile order | tile_base | small_list | partials | verdicts | queue head
   const size_t o_desc = 0;
   const size_t o_zr = o_desc + align256(sizeof(SegDesc) * n);
-  const size_t o_tb = o_zr + align256(sizeof(ZeroRange) * P.zr.size());
+  const size_t o_to = o_zr + align256(sizeof(ZeroRange) * P.zr.size());
+  const size_t o_tb = o_to + align256(4ull * P.n_tiles);
   const size_t o_sl = o_tb + align256(4ull * (n + 1));
   const size_t o_pt = o_sl + align256(4ull * (n ? n : 1));
   const size_t o_vd = o_pt + align256(16ull * (P.n_tiles ? P.n_tiles : 1));
-  const size_t bytes = o_vd + align256(4ull * (n ? n : 1));
+  const size_t o_qh = o_vd + align256(4ull * (n ? n : 1));
+  const size_t bytes = o_qh + 256;
   uint8_t* scratch = nullptr;
   hipError_t e = hipMallocAsync((void**)&scratch, bytes, stream);
   if (e != hipSuccess) return hip_fail(e, "hipMallocAsync(scratch)");
@@ -318,6 +357,7 @@ gift_status run_gcm(const gift_tensor* t, const gift_segment_table* st, gift_key
   std::vector<uint8_t> host(o_tb);
   if (n) memcpy(host.data() + o_desc, P.descs.data(), sizeof(SegDesc) * n);
   if (!P.zr.empty()) memcpy(host.data() + o_zr, P.zr.data(), sizeof(ZeroRange) * P.zr.size());
+  if (P.n_tiles) tile_order(P.descs.data(), n, P.n_tiles, (uint32_t*)(host.data() + o_to));
   Staging* sg = staging_for(dev);
   if (!sg) {
     (void)hipFreeAsync(scratch, stream);
@@ -342,7 +382,7 @@ gift_status run_gcm(const gift_tensor* t, const gift_segment_table* st, gift_key
         }
       }
       e = launch_expand(d_desc, n, (uint32_t*)(scratch + o_tb), (uint32_t*)(scratch + o_sl), verdicts,
-                        st->row_labels == nullptr, stream);
+                        st->row_labels == nullptr, (uint32_t*)(scratch + o_qh), stream);
       if (e != hipSuccess) {
         rs = hip_fail(e, "expand launch");
         break;
@@ -360,6 +400,8 @@ gift_status run_gcm(const gift_tensor* t, const gift_segment_table* st, gift_key
       a.n_tiles = P.n_tiles;
       a.n_small = P.n_small;
       a.partials = (uint4*)(scratch + o_pt);
+      a.tile_order = (const uint32_t*)(scratch + o_to);
+      a.tile_counter = (uint32_t*)(scratch + o_qh);
       a.verdicts = verdicts;
       a.tags_out = tags_out;
       a.tags_in = tags_in;
@@ -527,15 +569,17 @@ gift_status run_paged(const gift_paged_kv* kv, const gift_request* reqs, uint32_
   uint32_t shift = 0;
   while ((16ull << shift) < kv->chunk_bytes) shift++;
 
-  // scratch: descs | bids | tile_base | small_list | partials | verdicts | chunk offsets
+  // scratch: descs | bids | tile order | tile_base | small_list | partials | verdicts | chunk offsets | queue head
   const size_t o_desc = 0;
   const size_t o_bid = o_desc + align256(sizeof(SegDesc) * n);
-  const size_t o_tb = o_bid + align256(4ull * total_bids);
+  const size_t o_to = o_bid + align256(4ull * total_bids);
+  const size_t o_tb = o_to + align256(4ull * n_tiles);
   const size_t o_sl = o_tb + align256(4ull * (n + 1));
   const size_t o_pt = o_sl + align256(4ull * n);
   const size_t o_vd = o_pt + align256(16ull * (n_tiles ? n_tiles : 1));
   const size_t o_ck = o_vd + align256(4ull * n);
-  const size_t bytes = o_ck + align256(8ull * cpos);
+  const size_t o_qh = o_ck + align256(8ull * cpos);
+  const size_t bytes = o_qh + 256;
   uint8_t* scratch = nullptr;
   hipError_t e = hipMallocAsync((void**)&scratch, bytes, stream);
   if (e != hipSuccess) return hip_fail(e, "hipMallocAsync(scratch)");
@@ -548,6 +592,7 @@ gift_status run_paged(const gift_paged_kv* kv, const gift_request* reqs, uint32_
       bp += reqs[i].n_block_ids;
     }
   }
+  if (n_tiles) tile_order(descs.data(), n, n_tiles, (uint32_t*)(host.data() + o_to));
   Staging* sg = staging_for(dev);
   e = sg ? sg->upload(scratch, host.data(), o_tb, stream) : hipErrorInvalidDevice;
   if (e != hipSuccess) {
@@ -568,7 +613,7 @@ gift_status run_paged(const gift_paged_kv* kv, const gift_request* reqs, uint32_
       }
     }
     e = launch_expand(d_desc, n, (uint32_t*)(scratch + o_tb), (uint32_t*)(scratch + o_sl), verdicts, labels == nullptr,
-                      stream);
+                      (uint32_t*)(scratch + o_qh), stream);
     if (e == hipSuccess)
       e = launch_chunk_table(d_desc, n, d_bid, kv->n_layers, kv->n_parts, kv->layer_stride, kv->block_stride,
                              kv->part_stride, d_ck, stream);
@@ -589,6 +634,8 @@ gift_status run_paged(const gift_paged_kv* kv, const gift_request* reqs, uint32_
     a.n_tiles = n_tiles;
     a.n_small = 0;
     a.partials = (uint4*)(scratch + o_pt);
+    a.tile_order = (const uint32_t*)(scratch + o_to);
+    a.tile_counter = (uint32_t*)(scratch + o_qh);
     a.verdicts = verdicts;
     a.tags_out = tags_out;
     a.tags_in = tags_in;

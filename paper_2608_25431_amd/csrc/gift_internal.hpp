@@ -89,6 +89,8 @@ struct GcmArgs {
   uint32_t n_tiles;
   uint32_t n_small;
   uint4* partials;             // [n_tiles] GHASH partial of each tile
+  const uint32_t* tile_order;  // [n_tiles] tile ids in the order the workgroups claim them
+  uint32_t* tile_counter;      // work-queue head, zeroed by the expansion kernel
   int32_t* verdicts;           // [n_segs]
   uint8_t* tags_out;           // seal: [n_segs][16]
   const uint8_t* tags_in;      // open: [n_segs][16]
@@ -102,8 +104,12 @@ hipError_t launch_key_setup(const uint8_t* keys_dev, KeyTableDev kt, hipStream_t
 // rows are positions in the uploaded block tables)
 hipError_t launch_check_owner(const SegDesc* segs, uint32_t n_segs, const uint32_t* labels, const uint32_t* bids,
                               int32_t* verdicts, hipStream_t s);
+// Also zeroes *tile_counter, the work-queue head of the next tile kernel.
 hipError_t launch_expand(const SegDesc* segs, uint32_t n_segs, uint32_t* tile_base, uint32_t* small_list,
-                         int32_t* verdicts, bool init_verdicts, hipStream_t s);
+                         int32_t* verdicts, bool init_verdicts, uint32_t* tile_counter, hipStream_t s);
+// Tile ids (in tile_base numbering) longest first: full tiles, then each
+// segment's partial first tile by its number of rows.  order has n_tiles entries.
+void tile_order(const SegDesc* descs, uint32_t n_segs, uint32_t n_tiles, uint32_t* order);
 hipError_t launch_gcm_tiles(const GcmArgs& a, int mode, uint32_t grid, hipStream_t s);
 hipError_t launch_gcm_small(const GcmArgs& a, bool open, hipStream_t s);
 hipError_t launch_gcm_finalize(const GcmArgs& a, bool open, hipStream_t s);

@@ -283,25 +283,38 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
   const SegDesc* __restrict__ segs = a.segs;
   const uint32_t* __restrict__ tile_base = a.tile_base;
 
-  for (uint32_t g = blockIdx.x; g < a.n_tiles; g += gridDim.x) {
+  // Work queue over the host's tile order (longest tiles first): workgroup b
+  // takes entry b first, then entries gridDim.x + (queue claims).  Each claim
+  // is issued while the workgroup works on its current tile, so its latency
+  // stays off the critical path; every wave leaves the loop on the same claim.
+  uint32_t claim = blockIdx.x;  // lane 0 of wave 0 holds the next entry
+  for (;;) {
     __syncthreads();  // previous tile finished with gtab, red and info
     if (tid < 64) {
-      // 64-way search by wave 0 for the last segment with tile_base <= g:
-      // lane j probes lo + span*j/64, and the highest probe at or below g
+      const uint32_t k = __shfl(claim, 0, 64);
+      const uint32_t gq = k < a.n_tiles ? a.tile_order[k] : 0xFFFFFFFFu;
+      // 64-way search by wave 0 for the last segment with tile_base <= gq:
+      // lane j probes lo + span*j/64, and the highest probe at or below gq
       // narrows [lo, hi) (about two dependent loads for a thousand segments)
-      uint32_t lo = 0, hi = a.n_segs;  // tile_base[lo] <= g < tile_base[hi]
+      uint32_t lo = 0, hi = gq == 0xFFFFFFFFu ? 1u : a.n_segs;  // tile_base[lo] <= gq < tile_base[hi]
       while (hi - lo > 1) {
         const uint64_t span = hi - lo;
         const uint32_t pos = lo + (uint32_t)((span * tid) >> 6);
-        const uint64_t le = __ballot(tile_base[pos] <= g);  // lane 0 (pos = lo) always set
+        const uint64_t le = __ballot(tile_base[pos] <= gq);  // lane 0 (pos = lo) always set
         const uint32_t j = 63u - (uint32_t)__clzll(le);
         const uint32_t nlo = lo + (uint32_t)((span * j) >> 6);
         if (j < 63u) hi = lo + (uint32_t)((span * (j + 1)) >> 6);
         lo = nlo;
       }
-      if (tid == 0) info[0] = lo;
+      if (tid == 0) {
+        info[0] = lo;
+        info[1] = gq;
+        if (gq != 0xFFFFFFFFu) claim = gridDim.x + atomicAdd(a.tile_counter, 1u);
+      }
     }
     __syncthreads();
+    const uint32_t g = __builtin_amdgcn_readfirstlane(info[1]);
+    if (g == 0xFFFFFFFFu) break;
     const uint32_t s = __builtin_amdgcn_readfirstlane(info[0]);
     const SegDesc* sd = segs + s;
     const uint32_t user = sd->user;
@@ -553,9 +566,11 @@ __global__ __launch_bounds__(64) void k_small(GcmArgs a) {
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(1024) void k_expand(const SegDesc* __restrict__ segs, uint32_t n,
                                                  uint32_t* __restrict__ tile_base, uint32_t* __restrict__ small_list,
-                                                 int32_t* __restrict__ verdicts, int init_verdicts) {
+                                                 int32_t* __restrict__ verdicts, int init_verdicts,
+                                                 uint32_t* __restrict__ tile_counter) {
   __shared__ uint32_t sc_t[1024], sc_s[1024];
   const uint32_t tid = threadIdx.x;
+  if (tid == 0) *tile_counter = 0u;  // the tile kernel's work queue starts at entry 0
   uint32_t carry_t = 0, carry_s = 0;
   for (uint32_t b0 = 0; b0 < n; b0 += 1024) {
     const uint32_t i = b0 + tid;
@@ -823,9 +838,9 @@ hipError_t launch_check_owner(const SegDesc* segs, uint32_t n_segs, const uint32
 }
 
 hipError_t launch_expand(const SegDesc* segs, uint32_t n_segs, uint32_t* tile_base, uint32_t* small_list,
-                         int32_t* verdicts, bool init_verdicts, hipStream_t s) {
+                         int32_t* verdicts, bool init_verdicts, uint32_t* tile_counter, hipStream_t s) {
   hipLaunchKernelGGL(k_expand, dim3(1), dim3(1024), 0, s, segs, n_segs, tile_base, small_list, verdicts,
-                     init_verdicts ? 1 : 0);
+                     init_verdicts ? 1 : 0, tile_counter);
   return hipGetLastError();
 }
 
