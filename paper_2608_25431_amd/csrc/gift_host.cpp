@@ -24,7 +24,7 @@ namespace gift {
 // Longest tiles first, so that a work queue over them ends with short tiles:
 // a counting sort by the number of rows each tile runs (the kernel's tiles
 // are aligned to the segment end, so only a segment's first tile is partial).
-void tile_order(const SegDesc* descs, uint32_t n_segs, uint32_t n_tiles, uint32_t* order) {
+void tile_order(const SegDesc* descs, uint32_t n_segs, uint32_t n_tiles, TileEnt* order) {
   std::vector<uint32_t> count(kRows + 2, 0);
   auto rows_of = [](uint64_t m, uint32_t t) -> uint32_t {
     const int64_t base = (int64_t)m - (int64_t)(t + 1) * (int64_t)kTileBlocks;
@@ -50,7 +50,7 @@ void tile_order(const SegDesc* descs, uint32_t n_segs, uint32_t n_tiles, uint32_
     if (descs[i].flags & kSegSmall) continue;
     const uint64_t m = descs[i].nblocks;
     const uint32_t nt = (uint32_t)((m + kTileBlocks - 1) / kTileBlocks);
-    for (uint32_t t = 0; t < nt; t++, g++) order[pos[rows_of(m, t)]++] = g;
+    for (uint32_t t = 0; t < nt; t++, g++) order[pos[rows_of(m, t)]++] = TileEnt{g, i, t, 0u};
   }
 }
 
@@ -344,7 +344,7 @@ gift_status run_gcm(const gift_tensor* t, const gift_segment_table* st, gift_key
   const size_t o_desc = 0;
   const size_t o_zr = o_desc + align256(sizeof(SegDesc) * n);
   const size_t o_to = o_zr + align256(sizeof(ZeroRange) * P.zr.size());
-  const size_t o_tb = o_to + align256(4ull * P.n_tiles);
+  const size_t o_tb = o_to + align256(sizeof(TileEnt) * P.n_tiles);
   const size_t o_sl = o_tb + align256(4ull * (n + 1));
   const size_t o_pt = o_sl + align256(4ull * (n ? n : 1));
   const size_t o_vd = o_pt + align256(16ull * (P.n_tiles ? P.n_tiles : 1));
@@ -357,7 +357,7 @@ gift_status run_gcm(const gift_tensor* t, const gift_segment_table* st, gift_key
   std::vector<uint8_t> host(o_tb);
   if (n) memcpy(host.data() + o_desc, P.descs.data(), sizeof(SegDesc) * n);
   if (!P.zr.empty()) memcpy(host.data() + o_zr, P.zr.data(), sizeof(ZeroRange) * P.zr.size());
-  if (P.n_tiles) tile_order(P.descs.data(), n, P.n_tiles, (uint32_t*)(host.data() + o_to));
+  if (P.n_tiles) tile_order(P.descs.data(), n, P.n_tiles, (TileEnt*)(host.data() + o_to));
   Staging* sg = staging_for(dev);
   if (!sg) {
     (void)hipFreeAsync(scratch, stream);
@@ -400,7 +400,7 @@ gift_status run_gcm(const gift_tensor* t, const gift_segment_table* st, gift_key
       a.n_tiles = P.n_tiles;
       a.n_small = P.n_small;
       a.partials = (uint4*)(scratch + o_pt);
-      a.tile_order = (const uint32_t*)(scratch + o_to);
+      a.tile_order = (const TileEnt*)(scratch + o_to);
       a.tile_counter = (uint32_t*)(scratch + o_qh);
       a.verdicts = verdicts;
       a.tags_out = tags_out;
@@ -573,7 +573,7 @@ gift_status run_paged(const gift_paged_kv* kv, const gift_request* reqs, uint32_
   const size_t o_desc = 0;
   const size_t o_bid = o_desc + align256(sizeof(SegDesc) * n);
   const size_t o_to = o_bid + align256(4ull * total_bids);
-  const size_t o_tb = o_to + align256(4ull * n_tiles);
+  const size_t o_tb = o_to + align256(sizeof(TileEnt) * n_tiles);
   const size_t o_sl = o_tb + align256(4ull * (n + 1));
   const size_t o_pt = o_sl + align256(4ull * n);
   const size_t o_vd = o_pt + align256(16ull * (n_tiles ? n_tiles : 1));
@@ -592,7 +592,7 @@ gift_status run_paged(const gift_paged_kv* kv, const gift_request* reqs, uint32_
       bp += reqs[i].n_block_ids;
     }
   }
-  if (n_tiles) tile_order(descs.data(), n, n_tiles, (uint32_t*)(host.data() + o_to));
+  if (n_tiles) tile_order(descs.data(), n, n_tiles, (TileEnt*)(host.data() + o_to));
   Staging* sg = staging_for(dev);
   e = sg ? sg->upload(scratch, host.data(), o_tb, stream) : hipErrorInvalidDevice;
   if (e != hipSuccess) {
@@ -634,7 +634,7 @@ gift_status run_paged(const gift_paged_kv* kv, const gift_request* reqs, uint32_
     a.n_tiles = n_tiles;
     a.n_small = 0;
     a.partials = (uint4*)(scratch + o_pt);
-    a.tile_order = (const uint32_t*)(scratch + o_to);
+    a.tile_order = (const TileEnt*)(scratch + o_to);
     a.tile_counter = (uint32_t*)(scratch + o_qh);
     a.verdicts = verdicts;
     a.tags_out = tags_out;

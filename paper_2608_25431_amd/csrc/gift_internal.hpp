@@ -70,6 +70,14 @@ struct KeyTableDev {
   uint32_t n_users;
 };
 
+// One entry of the tile kernel's work queue: tile g (in tile_base numbering)
+// is tile t of segment s, counted from the segment's end.
+struct TileEnt {
+  uint32_t g, s, t, pad;
+};
+static_assert(sizeof(TileEnt) == 16, "TileEnt layout");
+constexpr uint32_t kNoTile = 0xFFFFFFFFu;
+
 // Addressing of k_gcm_tiles: contiguous tensor, or a paged cache on the
 // input side (seal: gather) or the output side (open: scatter).
 enum : int { kModeOpen = 1, kModeGather = 2, kModeScatter = 4 };
@@ -89,7 +97,7 @@ struct GcmArgs {
   uint32_t n_tiles;
   uint32_t n_small;
   uint4* partials;             // [n_tiles] GHASH partial of each tile
-  const uint32_t* tile_order;  // [n_tiles] tile ids in the order the workgroups claim them
+  const TileEnt* tile_order;   // [n_tiles] tiles in the order the workgroups claim them
   uint32_t* tile_counter;      // work-queue head, zeroed by the expansion kernel
   int32_t* verdicts;           // [n_segs]
   uint8_t* tags_out;           // seal: [n_segs][16]
@@ -107,9 +115,9 @@ hipError_t launch_check_owner(const SegDesc* segs, uint32_t n_segs, const uint32
 // Also zeroes *tile_counter, the work-queue head of the next tile kernel.
 hipError_t launch_expand(const SegDesc* segs, uint32_t n_segs, uint32_t* tile_base, uint32_t* small_list,
                          int32_t* verdicts, bool init_verdicts, uint32_t* tile_counter, hipStream_t s);
-// Tile ids (in tile_base numbering) longest first: full tiles, then each
-// segment's partial first tile by its number of rows.  order has n_tiles entries.
-void tile_order(const SegDesc* descs, uint32_t n_segs, uint32_t n_tiles, uint32_t* order);
+// Tiles longest first: full tiles, then each segment's partial first tile by
+// its number of rows.  order has n_tiles entries.
+void tile_order(const SegDesc* descs, uint32_t n_segs, uint32_t n_tiles, TileEnt* order);
 hipError_t launch_gcm_tiles(const GcmArgs& a, int mode, uint32_t grid, hipStream_t s);
 hipError_t launch_gcm_small(const GcmArgs& a, bool open, hipStream_t s);
 hipError_t launch_gcm_finalize(const GcmArgs& a, bool open, hipStream_t s);

@@ -241,17 +241,22 @@ __device__ __forceinline__ u128 length_block(uint64_t len) {
 }
 
 // Tile end of a leader wave (see k_gcm_tiles): Horner over the staged lane
-// partials of its waves in W (LDS tables wt), one multiply by the lane's
-// power, then the wave sum into *red.  Kept out of line so that the main
-// loop's register allocation does not see it.
-__device__ __noinline__ void tile_fold(u128 v, const u128* stage, const uint8_t* wt, const uint4* hpow, u128* red,
+// partials of its waves in W (LDS tables), one multiply by the lane's power
+// hp, then the wave sum into the leader's reduction slot.  Kept out of line,
+// so that the main loop's register allocation does not see it; the LDS
+// regions arrive as byte offsets, so every access is an LDS instruction.
+typedef __attribute__((address_space(3))) uint8_t lds_byte;
+__device__ __noinline__ void tile_fold(u128 v, uint32_t stage_off, uint32_t wt_off, u128 hp, uint32_t red_off,
                                        uint32_t lane) {
   constexpr int kFold = kThreads / 64 / kLeaders;
+  const u128* stage = (const u128*)(lds_byte*)(uintptr_t)stage_off;
+  const uint8_t* wt = (const uint8_t*)(lds_byte*)(uintptr_t)wt_off;
+#pragma unroll 1
   for (int i = 1; i < kFold; i++) v = ghash_step_lds(v, stage[64u * kLeaders * (i - 1)], wt);
-  u128 z = gf_mul(v, ld_u128(hpow));
+  u128 z = gf_mul(v, hp);
 #pragma unroll
   for (int j = 0; j < 4; j++) z.w[j] = wave_xor(z.w[j]);
-  if (lane == 0) *red = z;
+  if (lane == 0) *(u128*)(lds_byte*)(uintptr_t)red_off = z;
 }
 
 // ---------------------------------------------------------------------------
@@ -281,47 +286,36 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
   uint32_t cur_user = 0xFFFFFFFFu;
 
   const SegDesc* __restrict__ segs = a.segs;
-  const uint32_t* __restrict__ tile_base = a.tile_base;
 
   // Work queue over the host's tile order (longest tiles first): workgroup b
-  // takes entry b first, then entries gridDim.x + (queue claims).  Each claim
-  // is issued while the workgroup works on its current tile, so its latency
-  // stays off the critical path; every wave leaves the loop on the same claim.
-  uint32_t claim = blockIdx.x;  // lane 0 of wave 0 holds the next entry
+  // takes entry b first, then entries gridDim.x + (queue claims).  Thread 0
+  // issues each claim when a tile starts and loads the claimed entry once the
+  // tile's rows are done, so neither latency sits between two tiles; every
+  // wave leaves the loop on the same entry.
+  uint32_t claim = blockIdx.x;  // thread 0: the entry after the current one
+  TileEnt nx = TileEnt{kNoTile, 0u, 0u, 0u};
+  auto fetch_next = [&]() {
+    if (tid == 0) nx = claim < a.n_tiles ? a.tile_order[claim] : TileEnt{kNoTile, 0u, 0u, 0u};
+  };
+  fetch_next();
   for (;;) {
     __syncthreads();  // previous tile finished with gtab, red and info
-    if (tid < 64) {
-      const uint32_t k = __shfl(claim, 0, 64);
-      const uint32_t gq = k < a.n_tiles ? a.tile_order[k] : 0xFFFFFFFFu;
-      // 64-way search by wave 0 for the last segment with tile_base <= gq:
-      // lane j probes lo + span*j/64, and the highest probe at or below gq
-      // narrows [lo, hi) (about two dependent loads for a thousand segments)
-      uint32_t lo = 0, hi = gq == 0xFFFFFFFFu ? 1u : a.n_segs;  // tile_base[lo] <= gq < tile_base[hi]
-      while (hi - lo > 1) {
-        const uint64_t span = hi - lo;
-        const uint32_t pos = lo + (uint32_t)((span * tid) >> 6);
-        const uint64_t le = __ballot(tile_base[pos] <= gq);  // lane 0 (pos = lo) always set
-        const uint32_t j = 63u - (uint32_t)__clzll(le);
-        const uint32_t nlo = lo + (uint32_t)((span * j) >> 6);
-        if (j < 63u) hi = lo + (uint32_t)((span * (j + 1)) >> 6);
-        lo = nlo;
-      }
-      if (tid == 0) {
-        info[0] = lo;
-        info[1] = gq;
-        if (gq != 0xFFFFFFFFu) claim = gridDim.x + atomicAdd(a.tile_counter, 1u);
-      }
+    if (tid == 0) {
+      info[0] = nx.g;
+      info[1] = nx.s;
+      info[2] = nx.t;
+      if (nx.g != kNoTile) claim = gridDim.x + atomicAdd(a.tile_counter, 1u);
     }
     __syncthreads();
-    const uint32_t g = __builtin_amdgcn_readfirstlane(info[1]);
-    if (g == 0xFFFFFFFFu) break;
-    const uint32_t s = __builtin_amdgcn_readfirstlane(info[0]);
+    const uint32_t g = __builtin_amdgcn_readfirstlane(info[0]);
+    if (g == kNoTile) break;
+    const uint32_t s = __builtin_amdgcn_readfirstlane(info[1]);
+    const uint32_t t = __builtin_amdgcn_readfirstlane(info[2]);
     const SegDesc* sd = segs + s;
     const uint32_t user = sd->user;
     const uint32_t m = sd->nblocks;
     const uint64_t off = sd->byte_off, len = sd->len;
     const bool aligned = (sd->flags & kSegAligned) != 0;
-    const uint32_t t = g - tile_base[s];
     const int32_t verdict = a.verdicts[s];
     const int64_t base = (int64_t)m - (int64_t)(t + 1) * (int64_t)kTileBlocks;  // block index of virtual slot 0
     const int r_start = base < 0 ? (int)((uint64_t)(-base) / kThreads) : 0;
@@ -343,6 +337,7 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
           store_block(dst, u128_zero(), rem >= 16 ? 16u : (uint32_t)rem, aligned);
         }
       }
+      fetch_next();
       continue;
     }
 
@@ -426,13 +421,21 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
     // H^(64*kLeaders*(kFold - 1 - i)) * H^(64*kLeaders + 1 - 64*g - lane): leader
     // g folds its waves by Horner in W = H^(64*kLeaders) from the LDS tables,
     // then multiplies once by the per-lane power.
+    fetch_next();  // its load overlaps the tile end
     const uint32_t wave = tid >> 6, lane = tid & 63u;
     u128* stage = (u128*)(smem + kLdsStage);
+    // the leaders fetch their lane's power before the barrier, so the load
+    // overlaps the wait for the other waves
+    u128 hp = u128_zero();
+    if (wave < (uint32_t)kLeaders)
+      hp = ld_u128(a.kt.pow_h + (size_t)user * kHPowers + (64u * kLeaders + 1u - 64u * wave - lane));
     if (wave >= (uint32_t)kLeaders) stage[tid - 64u * kLeaders] = y;
     __syncthreads();
-    if (wave < (uint32_t)kLeaders)
-      tile_fold(y, stage + (wave * 64u + lane), smem + kLdsFold,
-                a.kt.pow_h + (size_t)user * kHPowers + (64u * kLeaders + 1u - 64u * wave - lane), red + wave, lane);
+    if (wave < (uint32_t)kLeaders) {
+      const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_byte*)smem;
+      tile_fold(y, lds0 + kLdsStage + 16u * (wave * 64u + lane), lds0 + kLdsFold, hp, lds0 + kLdsRed + 16u * wave,
+                lane);
+    }
     __syncthreads();
     if (tid == 0) {
       u128 p = red[0];
