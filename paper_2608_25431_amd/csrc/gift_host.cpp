@@ -189,6 +189,175 @@ Staging* staging_for(int dev) {
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
+// Device scratch of the calls (descriptors, tile queue, partials, ...),
+// cached per (device, stream) instead of allocated and freed on every call.
+// Work on one stream runs in order, so the buffer of an earlier call on the
+// same stream can serve the next call at once: its first use there (the
+// descriptor upload) runs behind everything the earlier call enqueued.  A
+// lease holds the entry's lock until its call has enqueued all its work, so
+// two host threads on one stream cannot interleave their uses of the buffer.
+// The event recorded when a lease ends guards the rare cases where a buffer
+// is replaced (it is too small) or handed to another stream: the host waits
+// for its last use first.  When every entry of the device is busy on other
+// streams, a call falls back to stream-ordered allocation.
+struct ScratchEntry {
+  std::mutex mu;
+  bool bound = false;  // stream is valid
+  hipStream_t stream = nullptr;
+  uint8_t* ptr = nullptr;
+  size_t cap = 0;
+  hipEvent_t done = nullptr;
+  bool recorded = false;  // done marks the last use of ptr
+  bool unsure = false;    // a use is not covered by done: synchronise the device first
+};
+
+constexpr int kScratchEntries = 16;
+
+struct ScratchTable {
+  std::mutex mu;
+  ScratchEntry e[kScratchEntries];
+};
+
+ScratchTable* scratch_table(int dev) {
+  // never destroyed: device memory outlives static destruction order
+  static ScratchTable* t[kMaxDevices] = {nullptr};
+  static std::mutex mu;
+  if (dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> g(mu);
+  if (!t[dev]) t[dev] = new ScratchTable;
+  return t[dev];
+}
+
+class ScratchLease {
+ public:
+  ScratchLease() = default;
+  ScratchLease(const ScratchLease&) = delete;
+  ScratchLease& operator=(const ScratchLease&) = delete;
+  ~ScratchLease() { (void)release(); }
+
+  // A buffer of at least `bytes` for work enqueued on `s` by this call.
+  hipError_t acquire(int dev, hipStream_t s, size_t bytes) {
+    s_ = s;
+    ScratchTable* tab = scratch_table(dev);
+    if (!tab) return hipErrorInvalidDevice;
+    for (int attempt = 0; attempt < 4 && !e_; attempt++) {
+      ScratchEntry* mine = nullptr;
+      {
+        std::lock_guard<std::mutex> g(tab->mu);
+        for (ScratchEntry& x : tab->e)
+          if (x.bound && x.stream == s) mine = &x;
+        if (!mine) {
+          // an unbound entry, else one that no call holds (its stream's
+          // last use must finish before the buffer changes hands)
+          for (ScratchEntry& x : tab->e)
+            if (!x.bound && x.mu.try_lock()) {
+              e_ = &x;
+              break;
+            }
+          for (int i = 0; i < kScratchEntries && !e_; i++)
+            if (tab->e[i].mu.try_lock()) e_ = &tab->e[i];
+          if (e_) {
+            lk_ = std::unique_lock<std::mutex>(e_->mu, std::adopt_lock);
+            e_->bound = true;
+            e_->stream = s;
+          }
+        }
+      }
+      if (e_) {
+        // taken over from another stream (or fresh): its last use there
+        // must finish before this call's work may touch the buffer
+        hipError_t w = settle(*e_);
+        if (w != hipSuccess) return w;
+      }
+      if (mine) {
+        std::unique_lock<std::mutex> l(mine->mu);
+        if (mine->bound && mine->stream == s) {  // still ours after the wait
+          e_ = mine;
+          lk_ = std::move(l);
+        }
+      } else if (!e_) {
+        break;  // every entry is busy on another stream
+      }
+    }
+    if (!e_) {
+      hipError_t r = hipMallocAsync((void**)&ptr, bytes, s);
+      owned_ = r == hipSuccess;
+      return r;
+    }
+    if (e_->cap < bytes) {
+      hipError_t w = settle(*e_);
+      if (w != hipSuccess) return w;
+      if (e_->ptr) {
+        w = hipFree(e_->ptr);
+        e_->ptr = nullptr;
+        e_->cap = 0;
+        if (w != hipSuccess) return w;
+      }
+      const size_t cap = std::max(bytes, (size_t)1 << 20);
+      w = hipMalloc((void**)&e_->ptr, cap);
+      if (w != hipSuccess) {
+        e_->ptr = nullptr;
+        return w;
+      }
+      e_->cap = cap;
+    }
+    if (!e_->done) {
+      hipError_t w = hipEventCreateWithFlags(&e_->done, hipEventDisableTiming);
+      if (w != hipSuccess) {
+        e_->done = nullptr;
+        return w;
+      }
+    }
+    ptr = e_->ptr;
+    return hipSuccess;
+  }
+
+  // Ends the call's use of the buffer: after its last enqueued work.
+  hipError_t release() {
+    hipError_t r = hipSuccess;
+    if (owned_) {
+      r = hipFreeAsync(ptr, s_);
+      owned_ = false;
+    } else if (e_) {
+      if (ptr) {
+        r = hipEventRecord(e_->done, s_);
+        e_->recorded = r == hipSuccess;
+        e_->unsure = r != hipSuccess;
+      }
+      lk_.unlock();
+      e_ = nullptr;
+    }
+    ptr = nullptr;
+    return r;
+  }
+
+  uint8_t* ptr = nullptr;
+
+ private:
+  // waits until no enqueued work uses the entry's buffer
+  static hipError_t settle(ScratchEntry& x) {
+    if (x.unsure) {
+      hipError_t w = hipDeviceSynchronize();
+      if (w != hipSuccess) return w;
+      x.unsure = false;
+      x.recorded = false;
+    }
+    if (x.recorded) {
+      hipError_t w = hipEventSynchronize(x.done);
+      if (w != hipSuccess) return w;
+      x.recorded = false;
+    }
+    return hipSuccess;
+  }
+
+  ScratchEntry* e_ = nullptr;
+  std::unique_lock<std::mutex> lk_;
+  hipStream_t s_ = nullptr;
+  bool owned_ = false;
+};
+
+
+
 struct Plan {
   std::vector<SegDesc> descs;
   std::vector<ZeroRange> zr;
@@ -350,24 +519,19 @@ gift_status run_gcm(const gift_tensor* t, const gift_segment_table* st, gift_key
   const size_t o_vd = o_pt + align256(16ull * (P.n_tiles ? P.n_tiles : 1));
   const size_t o_qh = o_vd + align256(4ull * (n ? n : 1));
   const size_t bytes = o_qh + 256;
-  uint8_t* scratch = nullptr;
-  hipError_t e = hipMallocAsync((void**)&scratch, bytes, stream);
-  if (e != hipSuccess) return hip_fail(e, "hipMallocAsync(scratch)");
+  ScratchLease lease;
+  hipError_t e = lease.acquire(dev, stream, bytes);
+  if (e != hipSuccess) return hip_fail(e, "device scratch");
+  uint8_t* scratch = lease.ptr;
 
   std::vector<uint8_t> host(o_tb);
   if (n) memcpy(host.data() + o_desc, P.descs.data(), sizeof(SegDesc) * n);
   if (!P.zr.empty()) memcpy(host.data() + o_zr, P.zr.data(), sizeof(ZeroRange) * P.zr.size());
   if (P.n_tiles) tile_order(P.descs.data(), n, P.n_tiles, (TileEnt*)(host.data() + o_to));
   Staging* sg = staging_for(dev);
-  if (!sg) {
-    (void)hipFreeAsync(scratch, stream);
-    return fail(GIFT_E_INVALID, "device index %d unsupported", dev);
-  }
+  if (!sg) return fail(GIFT_E_INVALID, "device index %d unsupported", dev);
   e = sg->upload(scratch, host.data(), o_tb, stream);
-  if (e != hipSuccess) {
-    (void)hipFreeAsync(scratch, stream);
-    return hip_fail(e, "staging upload");
-  }
+  if (e != hipSuccess) return hip_fail(e, "staging upload");
 
   const SegDesc* d_desc = (const SegDesc*)(scratch + o_desc);
   int32_t* verdicts = st->verdicts ? st->verdicts : (int32_t*)(scratch + o_vd);
@@ -441,8 +605,8 @@ gift_status run_gcm(const gift_tensor* t, const gift_segment_table* st, gift_key
       }
     }
   } while (0);
-  e = hipFreeAsync(scratch, stream);
-  if (rs == GIFT_OK && e != hipSuccess) rs = hip_fail(e, "hipFreeAsync(scratch)");
+  e = lease.release();
+  if (rs == GIFT_OK && e != hipSuccess) rs = hip_fail(e, "device scratch release");
   return rs;
 }
 
@@ -580,9 +744,10 @@ gift_status run_paged(const gift_paged_kv* kv, const gift_request* reqs, uint32_
   const size_t o_ck = o_vd + align256(4ull * n);
   const size_t o_qh = o_ck + align256(8ull * cpos);
   const size_t bytes = o_qh + 256;
-  uint8_t* scratch = nullptr;
-  hipError_t e = hipMallocAsync((void**)&scratch, bytes, stream);
-  if (e != hipSuccess) return hip_fail(e, "hipMallocAsync(scratch)");
+  ScratchLease lease;
+  hipError_t e = lease.acquire(dev, stream, bytes);
+  if (e != hipSuccess) return hip_fail(e, "device scratch");
+  uint8_t* scratch = lease.ptr;
   std::vector<uint8_t> host(o_tb);
   memcpy(host.data() + o_desc, descs.data(), sizeof(SegDesc) * n);
   {
@@ -595,10 +760,7 @@ gift_status run_paged(const gift_paged_kv* kv, const gift_request* reqs, uint32_
   if (n_tiles) tile_order(descs.data(), n, n_tiles, (TileEnt*)(host.data() + o_to));
   Staging* sg = staging_for(dev);
   e = sg ? sg->upload(scratch, host.data(), o_tb, stream) : hipErrorInvalidDevice;
-  if (e != hipSuccess) {
-    (void)hipFreeAsync(scratch, stream);
-    return hip_fail(e, "staging upload");
-  }
+  if (e != hipSuccess) return hip_fail(e, "staging upload");
   const SegDesc* d_desc = (const SegDesc*)(scratch + o_desc);
   const uint32_t* d_bid = (const uint32_t*)(scratch + o_bid);
   uint64_t* d_ck = (uint64_t*)(scratch + o_ck);
@@ -659,8 +821,8 @@ gift_status run_paged(const gift_paged_kv* kv, const gift_request* reqs, uint32_
     }
   } while (0);
   g_prof_before = g_prof_after = nullptr;
-  e = hipFreeAsync(scratch, stream);
-  if (rs == GIFT_OK && e != hipSuccess) rs = hip_fail(e, "hipFreeAsync(scratch)");
+  e = lease.release();
+  if (rs == GIFT_OK && e != hipSuccess) rs = hip_fail(e, "device scratch release");
   return rs;
 }
 
@@ -809,16 +971,17 @@ gift_status gift_check_owner(const gift_segment_table* st, const uint32_t* label
   if ((sv = current_device(&dev)) != GIFT_OK) return sv;
   Plan P;
   build_plan(st->segs, n, n_rows, 1, nullptr, nullptr, nullptr, false, P);
-  SegDesc* d = nullptr;
   const size_t bytes = sizeof(SegDesc) * n;
-  hipError_t e = hipMallocAsync((void**)&d, bytes, stream);
-  if (e != hipSuccess) return hip_fail(e, "hipMallocAsync(descs)");
+  ScratchLease lease;
+  hipError_t e = lease.acquire(dev, stream, bytes);
+  if (e != hipSuccess) return hip_fail(e, "device scratch");
+  SegDesc* d = (SegDesc*)lease.ptr;
   Staging* sg = staging_for(dev);
   e = sg ? sg->upload(d, P.descs.data(), bytes, stream) : hipErrorInvalidDevice;
   if (e == hipSuccess) e = launch_check_owner(d, n, labels, nullptr, st->verdicts, stream);
-  hipError_t e2 = hipFreeAsync(d, stream);
+  hipError_t e2 = lease.release();
   if (e != hipSuccess) return hip_fail(e, "check_owner");
-  if (e2 != hipSuccess) return hip_fail(e2, "hipFreeAsync(descs)");
+  if (e2 != hipSuccess) return hip_fail(e2, "device scratch release");
   return GIFT_OK;
 }
 
@@ -844,9 +1007,11 @@ static gift_status run_tokens(bool decrypt, const gift_segment_table* st, uint64
   build_plan(st->segs, n, n_tokens, 1, nullptr, nullptr, nullptr, false, P);
   SegDesc* d = nullptr;
   hipError_t e = hipSuccess;
+  ScratchLease lease;
   if (n > 0) {
-    e = hipMallocAsync((void**)&d, sizeof(SegDesc) * n, stream);
-    if (e != hipSuccess) return hip_fail(e, "hipMallocAsync(descs)");
+    e = lease.acquire(dev, stream, sizeof(SegDesc) * n);
+    if (e != hipSuccess) return hip_fail(e, "device scratch");
+    d = (SegDesc*)lease.ptr;
     Staging* sg = staging_for(dev);
     e = sg ? sg->upload(d, P.descs.data(), sizeof(SegDesc) * n, stream) : hipErrorInvalidDevice;
   }
@@ -860,9 +1025,9 @@ static gift_status run_tokens(bool decrypt, const gift_segment_table* st, uint64
   if (e == hipSuccess)
     e = launch_tokens(d, n, decrypt, tokens, nonces, blocks_in, blocks_out, tokens_out, nonces_out, eos_token, kt->dev,
                       stream);
-  hipError_t e2 = d ? hipFreeAsync(d, stream) : hipSuccess;
+  hipError_t e2 = lease.release();
   if (e != hipSuccess) return hip_fail(e, "token kernels");
-  if (e2 != hipSuccess) return hip_fail(e2, "hipFreeAsync(descs)");
+  if (e2 != hipSuccess) return hip_fail(e2, "device scratch release");
   return GIFT_OK;
 }
 

@@ -334,6 +334,68 @@ def test_two_threads_on_two_streams_share_a_key_table(kt3):
             assert ver[:2].tolist() == [gift.SEG_OK, gift.SEG_OK]
 
 
+def test_scratch_reuse_across_streams_threads_and_sizes(kt3):
+    # the library keeps each stream's device scratch between calls: more
+    # streams than it caches (buffers change hands), two host threads on one
+    # stream, and growing then shrinking tables on one stream
+    import threading
+    keys, nb, kt = kt3
+    cases = []
+    for i in range(24):
+        n_segs = [1, 3, 40, 700][i % 4]
+        rb = 64 if n_segs > 3 else 4096 + 48 * i
+        n_rows = n_segs * (2 if rb == 64 else 5)
+        data_np = rng.integers(0, 256, n_rows * rb, dtype=np.uint8)
+        per = n_rows // n_segs
+        table = [(k * per, per, (k + i) % 3, 1000 * i + k) for k in range(n_segs)]
+        st, o_out, o_tags, _ = oracle.seal(data_np, n_rows, rb, table, keys, nb)
+        assert st == 0
+        cases.append((data_np, n_rows, rb, table, o_out, o_tags))
+
+    def check(i, out, tags, back, ver):
+        data_np, n_rows, rb, table, o_out, o_tags = cases[i]
+        n = len(table)
+        assert host(out).tobytes() == o_out.tobytes(), i
+        assert host(tags)[:16 * n].tobytes() == o_tags.tobytes(), i
+        assert host(back).tobytes() == data_np.tobytes(), i
+        assert (host(ver)[:n] == gift.SEG_OK).all(), i
+
+    def run(i, stream):
+        data_np, n_rows, rb, table, _, _ = cases[i]
+        with torch.cuda.stream(stream):
+            d = dev_u8(data_np)
+            out, tags, _ = seal(d, n_rows, rb, table, kt, nb)
+            back, ver = open_(out, n_rows, rb, table, kt, nb, tags)
+        return out, tags, back, ver
+
+    streams = [torch.cuda.Stream() for _ in range(20)]
+    res = [run(i, streams[i % 20]) for i in range(24)]
+    torch.cuda.synchronize()
+    for i, r in enumerate(res):
+        check(i, *r)
+
+    shared = torch.cuda.Stream()
+    got, errors = {}, []
+
+    def work(t):
+        try:
+            for i in range(t, 24, 2):
+                got[i] = run(i, shared)
+        except Exception as e:  # surfaced in the main thread
+            errors.append(e)
+
+    threads = [threading.Thread(target=work, args=(t,)) for t in range(2)]
+    for th in threads:
+        th.start()
+    for th in threads:
+        th.join()
+    assert not errors, errors
+    torch.cuda.synchronize()
+    for i, r in got.items():
+        check(i, *r)
+    assert len(got) == 24
+
+
 # --------------------------------------------------------------------------
 # full-size configurations
 # --------------------------------------------------------------------------
