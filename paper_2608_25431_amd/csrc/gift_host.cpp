@@ -99,9 +99,11 @@ int device_cus(int dev) {
   return cus[dev];
 }
 
-// Pinned host staging ring per device: descriptors are copied here and
-// uploaded with one async copy; a slot is reused only after the event
-// recorded behind its copy has completed.
+// Pinned host staging ring per device: descriptors are copied here and read
+// into device scratch by one small kernel on the call's stream (a DMA copy
+// would make the compute queue wait for the copy engine, ~30 us per call); a
+// slot is reused only after the event recorded behind that kernel has
+// completed.
 class Staging {
  public:
   hipError_t upload(void* dst, const void* src, size_t bytes, hipStream_t s) {
@@ -118,11 +120,14 @@ class Staging {
       return e != hipSuccess ? e : e2;
     }
     if (base_ == nullptr) {
-      hipError_t e = hipHostMalloc((void**)&base_, kCap, hipHostMallocDefault);
+      hipError_t e = hipHostMalloc((void**)&base_, kCap, hipHostMallocMapped);
       if (e != hipSuccess) {
         base_ = nullptr;
         return e;
       }
+      // the ring's address on the device, for the copy kernel; without one
+      // the uploads take the DMA copy
+      if (hipHostGetDevicePointer((void**)&dbase_, base_, 0) != hipSuccess) dbase_ = nullptr;
     }
     size_t need = (bytes + 255) & ~(size_t)255;
     if (head_ + need > kCap) head_ = 0;
@@ -145,7 +150,8 @@ class Staging {
       }
     }
     memcpy(base_ + head_, src, bytes);
-    hipError_t e = hipMemcpyAsync(dst, base_ + head_, bytes, hipMemcpyHostToDevice, s);
+    hipError_t e = (dbase_ && !(bytes & 15u)) ? launch_copy_in(dst, dbase_ + head_, bytes, s)
+                                               : hipMemcpyAsync(dst, base_ + head_, bytes, hipMemcpyHostToDevice, s);
     if (e != hipSuccess) return e;
     hipEvent_t ev;
     if (!free_ev_.empty()) {
@@ -177,6 +183,7 @@ class Staging {
   };
   std::mutex mu_;
   uint8_t* base_ = nullptr;
+  uint8_t* dbase_ = nullptr;  // base_ as the device addresses it
   size_t head_ = 0;
   std::vector<Slot> live_;
   std::vector<hipEvent_t> free_ev_;

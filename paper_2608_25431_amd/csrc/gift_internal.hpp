@@ -124,6 +124,9 @@ hipError_t launch_gcm_finalize(const GcmArgs& a, bool open, hipStream_t s);
 hipError_t launch_zero_ranges(uint8_t* out, const ZeroRange* r, uint32_t n, const int32_t* verdicts, uint32_t grid,
                               hipStream_t s);
 hipError_t launch_wipe(void* p, size_t bytes, hipStream_t s);
+// Copies bytes (a multiple of 16, both addresses 16-byte aligned) from pinned,
+// device-accessible host memory into device memory, as a kernel on s.
+hipError_t launch_copy_in(void* dst, const void* src_host, size_t bytes, hipStream_t s);
 // Paged calls: chunk offsets from the block tables (segment rows index bids),
 // and zeroing of every chunk of segments whose verdict is not OK.
 hipError_t launch_chunk_table(const SegDesc* segs, uint32_t n_segs, const uint32_t* bids, uint32_t n_layers,

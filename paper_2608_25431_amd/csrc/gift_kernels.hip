@@ -651,6 +651,14 @@ __global__ __launch_bounds__(256) void k_wipe(uint8_t* p, size_t bytes) {
   for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < bytes; i += gsz) p[i] = 0;
 }
 
+// A call's descriptors, read straight from the pinned host staging ring into
+// device scratch by a kernel on the call's stream: no DMA engine has to
+// synchronise with the compute queue between the upload and the kernels.
+__global__ __launch_bounds__(256) void k_copy_in(uint4* __restrict__ dst, const uint4* __restrict__ src, size_t n16) {
+  const size_t gsz = (size_t)gridDim.x * blockDim.x;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += gsz) dst[i] = src[i];
+}
+
 // ---------------------------------------------------------------------------
 // Per-token encryption (token || nonce as one block under the owner's key,
 // the end-of-sequence token as the all-0xFF block).  One workgroup per
@@ -919,6 +927,16 @@ hipError_t launch_zero_chunks(const SegDesc* segs, uint32_t n_segs, const uint32
   if (grid > n_tiles) grid = n_tiles;
   hipLaunchKernelGGL(k_zero_chunks, dim3(grid), dim3(256), 0, s, segs, n_segs, tile_base, n_tiles, verdicts,
                      chunk_off, pbase, chunk_shift);
+  return hipGetLastError();
+}
+
+hipError_t launch_copy_in(void* dst, const void* src_host, size_t bytes, hipStream_t s) {
+  if (bytes == 0) return hipSuccess;
+  if ((bytes | (uintptr_t)dst | (uintptr_t)src_host) & 15u) return hipErrorInvalidValue;
+  const size_t n16 = bytes / 16;
+  uint32_t grid = cdiv(n16, 256u);
+  if (grid > 64u) grid = 64u;
+  hipLaunchKernelGGL(k_copy_in, dim3(grid), dim3(256), 0, s, (uint4*)dst, (const uint4*)src_host, n16);
   return hipGetLastError();
 }
 
