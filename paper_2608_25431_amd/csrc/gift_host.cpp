@@ -54,6 +54,20 @@ void tile_order(const SegDesc* descs, uint32_t n_segs, uint32_t n_tiles, TileEnt
   }
 }
 
+// tile_base (n + 1 entries: first tile of each segment; small segments have
+// none) and the list of small segments, as the kernels read them.
+void tile_tables(const SegDesc* descs, uint32_t n, uint32_t* tile_base, uint32_t* small_list) {
+  uint32_t t = 0, k = 0;
+  for (uint32_t i = 0; i < n; i++) {
+    tile_base[i] = t;
+    if (descs[i].flags & kSegSmall)
+      small_list[k++] = i;
+    else
+      t += (uint32_t)(((uint64_t)descs[i].nblocks + kTileBlocks - 1) / kTileBlocks);
+  }
+  tile_base[n] = t;
+}
+
 }  // namespace gift
 
 struct gift_key_table_s {
@@ -99,16 +113,21 @@ int device_cus(int dev) {
   return cus[dev];
 }
 
-// Pinned host staging ring per device: descriptors are copied here and read
-// into device scratch by one small kernel on the call's stream (a DMA copy
-// would make the compute queue wait for the copy engine, ~30 us per call); a
-// slot is reused only after the event recorded behind that kernel has
+// Pinned host staging ring per device.  A call's descriptors are copied
+// here and read into device scratch by the call's first kernel (a DMA copy
+// would make the compute queue wait for the copy engine, ~30 us per call);
+// a slot is reused only after the event recorded behind that kernel has
 // completed.
 class Staging {
  public:
-  hipError_t upload(void* dst, const void* src, size_t bytes, hipStream_t s) {
+  // Copies bytes into the ring, then consume(src) enqueues on s the kernel
+  // that reads them: src is the copy's device address, or nullptr when the
+  // bytes were DMA-copied to dst instead (no device address for the ring, or
+  // a table too large for it).
+  template <class F>
+  hipError_t upload(void* dst, const void* src, size_t bytes, hipStream_t s, F&& consume) {
     std::lock_guard<std::mutex> g(mu_);
-    if (bytes == 0) return hipSuccess;
+    if (bytes == 0) return consume((const void*)nullptr);
     if (bytes > kCap / 2) {  // rare: very large tables take a private synchronous path
       void* tmp = nullptr;
       hipError_t e = hipHostMalloc(&tmp, bytes, hipHostMallocDefault);
@@ -117,7 +136,8 @@ class Staging {
       e = hipMemcpyAsync(dst, tmp, bytes, hipMemcpyHostToDevice, s);
       hipError_t e2 = hipStreamSynchronize(s);
       (void)hipHostFree(tmp);
-      return e != hipSuccess ? e : e2;
+      if (e == hipSuccess) e = e2;
+      return e != hipSuccess ? e : consume((const void*)nullptr);
     }
     if (base_ == nullptr) {
       hipError_t e = hipHostMalloc((void**)&base_, kCap, hipHostMallocMapped);
@@ -125,8 +145,6 @@ class Staging {
         base_ = nullptr;
         return e;
       }
-      // the ring's address on the device, for the copy kernel; without one
-      // the uploads take the DMA copy
       if (hipHostGetDevicePointer((void**)&dbase_, base_, 0) != hipSuccess) dbase_ = nullptr;
     }
     size_t need = (bytes + 255) & ~(size_t)255;
@@ -150,9 +168,17 @@ class Staging {
       }
     }
     memcpy(base_ + head_, src, bytes);
-    hipError_t e = (dbase_ && !(bytes & 15u)) ? launch_copy_in(dst, dbase_ + head_, bytes, s)
-                                               : hipMemcpyAsync(dst, base_ + head_, bytes, hipMemcpyHostToDevice, s);
-    if (e != hipSuccess) return e;
+    hipError_t e;
+    if (dbase_ && !(bytes & 15u)) {
+      e = consume((const void*)(dbase_ + head_));
+    } else {
+      e = hipMemcpyAsync(dst, base_ + head_, bytes, hipMemcpyHostToDevice, s);
+      if (e == hipSuccess) e = consume((const void*)nullptr);
+    }
+    if (e != hipSuccess) {
+      (void)hipStreamSynchronize(s);  // the slot may still be read: let it drain
+      return e;
+    }
     hipEvent_t ev;
     if (!free_ev_.empty()) {
       ev = free_ev_.back();
@@ -183,7 +209,7 @@ class Staging {
   };
   std::mutex mu_;
   uint8_t* base_ = nullptr;
-  uint8_t* dbase_ = nullptr;  // base_ as the device addresses it
+  uint8_t* dbase_ = nullptr;  // base_ as the device addresses it (mapped pinned memory)
   size_t head_ = 0;
   std::vector<Slot> live_;
   std::vector<hipEvent_t> free_ev_;
@@ -516,48 +542,40 @@ gift_status run_gcm(const gift_tensor* t, const gift_segment_table* st, gift_key
   Plan P;
   build_plan(st->segs, n, t->n_rows, t->row_bytes, nonce_base, t->data, out, OPEN, P);
 
-  // scratch: descs | zero ranges | tile order | tile_base | small_list | partials | verdicts | queue head
+  // scratch: the staged tables (descs | zero ranges | tile queue | tile_base |
+  // small list | queue head), then partials | verdicts
   const size_t o_desc = 0;
   const size_t o_zr = o_desc + align256(sizeof(SegDesc) * n);
   const size_t o_to = o_zr + align256(sizeof(ZeroRange) * P.zr.size());
   const size_t o_tb = o_to + align256(sizeof(TileEnt) * P.n_tiles);
   const size_t o_sl = o_tb + align256(4ull * (n + 1));
-  const size_t o_pt = o_sl + align256(4ull * (n ? n : 1));
+  const size_t o_qh = o_sl + align256(4ull * (n ? n : 1));
+  const size_t o_pt = o_qh + 256;  // end of the staged tables
   const size_t o_vd = o_pt + align256(16ull * (P.n_tiles ? P.n_tiles : 1));
-  const size_t o_qh = o_vd + align256(4ull * (n ? n : 1));
-  const size_t bytes = o_qh + 256;
+  const size_t bytes = o_vd + align256(4ull * (n ? n : 1));
   ScratchLease lease;
   hipError_t e = lease.acquire(dev, stream, bytes);
   if (e != hipSuccess) return hip_fail(e, "device scratch");
   uint8_t* scratch = lease.ptr;
 
-  std::vector<uint8_t> host(o_tb);
+  std::vector<uint8_t> host(o_pt);  // zero-filled: the queue head starts at 0
   if (n) memcpy(host.data() + o_desc, P.descs.data(), sizeof(SegDesc) * n);
   if (!P.zr.empty()) memcpy(host.data() + o_zr, P.zr.data(), sizeof(ZeroRange) * P.zr.size());
   if (P.n_tiles) tile_order(P.descs.data(), n, P.n_tiles, (TileEnt*)(host.data() + o_to));
+  tile_tables(P.descs.data(), n, (uint32_t*)(host.data() + o_tb), (uint32_t*)(host.data() + o_sl));
+  int32_t* verdicts = st->verdicts ? st->verdicts : (int32_t*)(scratch + o_vd);
   Staging* sg = staging_for(dev);
   if (!sg) return fail(GIFT_E_INVALID, "device index %d unsupported", dev);
-  e = sg->upload(scratch, host.data(), o_tb, stream);
+  // the prologue copies the tables and settles the verdicts (owner check)
+  e = sg->upload(scratch, host.data(), o_pt, stream, [&](const void* src) {
+    return launch_prologue(scratch, src, o_pt, n, kNoBids, st->row_labels, n ? verdicts : nullptr, stream);
+  });
   if (e != hipSuccess) return hip_fail(e, "staging upload");
 
   const SegDesc* d_desc = (const SegDesc*)(scratch + o_desc);
-  int32_t* verdicts = st->verdicts ? st->verdicts : (int32_t*)(scratch + o_vd);
   gift_status rs = GIFT_OK;
   do {
     if (n > 0) {
-      if (st->row_labels) {
-        e = launch_check_owner(d_desc, n, st->row_labels, nullptr, verdicts, stream);
-        if (e != hipSuccess) {
-          rs = hip_fail(e, "check_owner launch");
-          break;
-        }
-      }
-      e = launch_expand(d_desc, n, (uint32_t*)(scratch + o_tb), (uint32_t*)(scratch + o_sl), verdicts,
-                        st->row_labels == nullptr, (uint32_t*)(scratch + o_qh), stream);
-      if (e != hipSuccess) {
-        rs = hip_fail(e, "expand launch");
-        break;
-      }
       GcmArgs a;
       a.in = (const uint8_t*)t->data;
       a.out = (uint8_t*)out;
@@ -740,22 +758,23 @@ gift_status run_paged(const gift_paged_kv* kv, const gift_request* reqs, uint32_
   uint32_t shift = 0;
   while ((16ull << shift) < kv->chunk_bytes) shift++;
 
-  // scratch: descs | bids | tile order | tile_base | small_list | partials | verdicts | chunk offsets | queue head
+  // scratch: the staged tables (descs | block ids | tile queue | tile_base |
+  // small list | queue head), then partials | verdicts | chunk offsets
   const size_t o_desc = 0;
   const size_t o_bid = o_desc + align256(sizeof(SegDesc) * n);
   const size_t o_to = o_bid + align256(4ull * total_bids);
   const size_t o_tb = o_to + align256(sizeof(TileEnt) * n_tiles);
   const size_t o_sl = o_tb + align256(4ull * (n + 1));
-  const size_t o_pt = o_sl + align256(4ull * n);
+  const size_t o_qh = o_sl + align256(4ull * n);
+  const size_t o_pt = o_qh + 256;  // end of the staged tables
   const size_t o_vd = o_pt + align256(16ull * (n_tiles ? n_tiles : 1));
   const size_t o_ck = o_vd + align256(4ull * n);
-  const size_t o_qh = o_ck + align256(8ull * cpos);
-  const size_t bytes = o_qh + 256;
+  const size_t bytes = o_ck + align256(8ull * cpos);
   ScratchLease lease;
   hipError_t e = lease.acquire(dev, stream, bytes);
   if (e != hipSuccess) return hip_fail(e, "device scratch");
   uint8_t* scratch = lease.ptr;
-  std::vector<uint8_t> host(o_tb);
+  std::vector<uint8_t> host(o_pt);  // zero-filled: the queue head starts at 0
   memcpy(host.data() + o_desc, descs.data(), sizeof(SegDesc) * n);
   {
     uint32_t* bp = (uint32_t*)(host.data() + o_bid);
@@ -765,27 +784,23 @@ gift_status run_paged(const gift_paged_kv* kv, const gift_request* reqs, uint32_
     }
   }
   if (n_tiles) tile_order(descs.data(), n, n_tiles, (TileEnt*)(host.data() + o_to));
+  tile_tables(descs.data(), n, (uint32_t*)(host.data() + o_tb), (uint32_t*)(host.data() + o_sl));
+  int32_t* verdicts = verdicts_user ? verdicts_user : (int32_t*)(scratch + o_vd);
   Staging* sg = staging_for(dev);
-  e = sg ? sg->upload(scratch, host.data(), o_tb, stream) : hipErrorInvalidDevice;
+  // the prologue copies the tables and settles the verdicts (owner check by block id)
+  e = sg ? sg->upload(scratch, host.data(), o_pt, stream,
+                      [&](const void* src) {
+                        return launch_prologue(scratch, src, o_pt, n, o_bid, labels, verdicts, stream);
+                      })
+         : hipErrorInvalidDevice;
   if (e != hipSuccess) return hip_fail(e, "staging upload");
   const SegDesc* d_desc = (const SegDesc*)(scratch + o_desc);
   const uint32_t* d_bid = (const uint32_t*)(scratch + o_bid);
   uint64_t* d_ck = (uint64_t*)(scratch + o_ck);
-  int32_t* verdicts = verdicts_user ? verdicts_user : (int32_t*)(scratch + o_vd);
   gift_status rs = GIFT_OK;
   do {
-    if (labels) {
-      e = launch_check_owner(d_desc, n, labels, d_bid, verdicts, stream);
-      if (e != hipSuccess) {
-        rs = hip_fail(e, "check_owner launch");
-        break;
-      }
-    }
-    e = launch_expand(d_desc, n, (uint32_t*)(scratch + o_tb), (uint32_t*)(scratch + o_sl), verdicts, labels == nullptr,
-                      (uint32_t*)(scratch + o_qh), stream);
-    if (e == hipSuccess)
-      e = launch_chunk_table(d_desc, n, d_bid, kv->n_layers, kv->n_parts, kv->layer_stride, kv->block_stride,
-                             kv->part_stride, d_ck, stream);
+    e = launch_chunk_table(d_desc, n, d_bid, kv->n_layers, kv->n_parts, kv->layer_stride, kv->block_stride,
+                           kv->part_stride, d_ck, stream);
     if (e != hipSuccess) {
       rs = hip_fail(e, "paged expansion");
       break;
@@ -984,8 +999,11 @@ gift_status gift_check_owner(const gift_segment_table* st, const uint32_t* label
   if (e != hipSuccess) return hip_fail(e, "device scratch");
   SegDesc* d = (SegDesc*)lease.ptr;
   Staging* sg = staging_for(dev);
-  e = sg ? sg->upload(d, P.descs.data(), bytes, stream) : hipErrorInvalidDevice;
-  if (e == hipSuccess) e = launch_check_owner(d, n, labels, nullptr, st->verdicts, stream);
+  e = sg ? sg->upload(d, P.descs.data(), bytes, stream,
+                      [&](const void* src) {
+                        return launch_prologue(d, src, bytes, n, kNoBids, labels, st->verdicts, stream);
+                      })
+         : hipErrorInvalidDevice;
   hipError_t e2 = lease.release();
   if (e != hipSuccess) return hip_fail(e, "check_owner");
   if (e2 != hipSuccess) return hip_fail(e2, "device scratch release");
@@ -1020,7 +1038,12 @@ static gift_status run_tokens(bool decrypt, const gift_segment_table* st, uint64
     if (e != hipSuccess) return hip_fail(e, "device scratch");
     d = (SegDesc*)lease.ptr;
     Staging* sg = staging_for(dev);
-    e = sg ? sg->upload(d, P.descs.data(), sizeof(SegDesc) * n, stream) : hipErrorInvalidDevice;
+    const size_t bytes = sizeof(SegDesc) * n;
+    e = sg ? sg->upload(d, P.descs.data(), bytes, stream,
+                        [&](const void* src) {
+                          return launch_prologue(d, src, bytes, n, kNoBids, nullptr, nullptr, stream);
+                        })
+           : hipErrorInvalidDevice;
   }
   // uncovered tokens (rows no segment covers) get zero output: only when the
   // plan has such gaps is the output cleared first, the token kernel then

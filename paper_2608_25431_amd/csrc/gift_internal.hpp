@@ -108,13 +108,15 @@ struct GcmArgs {
 // Launch wrappers (gift_kernels.hip).  All enqueue on `s` and return the
 // launch status.
 hipError_t launch_key_setup(const uint8_t* keys_dev, KeyTableDev kt, hipStream_t s);
-// labels are indexed by row, or by bids[row] when bids is not NULL (paged:
-// rows are positions in the uploaded block tables)
-hipError_t launch_check_owner(const SegDesc* segs, uint32_t n_segs, const uint32_t* labels, const uint32_t* bids,
-                              int32_t* verdicts, hipStream_t s);
-// Also zeroes *tile_counter, the work-queue head of the next tile kernel.
-hipError_t launch_expand(const SegDesc* segs, uint32_t n_segs, uint32_t* tile_base, uint32_t* small_list,
-                         int32_t* verdicts, bool init_verdicts, uint32_t* tile_counter, hipStream_t s);
+// First kernel of a call.  Copies bytes of staged tables from src (the
+// mapped host ring; nullptr: they are in dst already) to dst, and, when
+// verdicts is not NULL, writes each segment's first verdict: the owner check
+// against labels (indexed by row, or by the block ids at byte bids_off of the
+// tables for paged calls) or OK without labels.  The descriptors sit at byte 0
+// of the tables.
+constexpr uint64_t kNoBids = ~0ull;
+hipError_t launch_prologue(void* dst, const void* src, size_t bytes, uint32_t n_segs, uint64_t bids_off,
+                           const uint32_t* labels, int32_t* verdicts, hipStream_t s);
 // Tiles longest first: full tiles, then each segment's partial first tile by
 // its number of rows.  order has n_tiles entries.
 void tile_order(const SegDesc* descs, uint32_t n_segs, uint32_t n_tiles, TileEnt* order);
@@ -124,9 +126,6 @@ hipError_t launch_gcm_finalize(const GcmArgs& a, bool open, hipStream_t s);
 hipError_t launch_zero_ranges(uint8_t* out, const ZeroRange* r, uint32_t n, const int32_t* verdicts, uint32_t grid,
                               hipStream_t s);
 hipError_t launch_wipe(void* p, size_t bytes, hipStream_t s);
-// Copies bytes (a multiple of 16, both addresses 16-byte aligned) from pinned,
-// device-accessible host memory into device memory, as a kernel on s.
-hipError_t launch_copy_in(void* dst, const void* src_host, size_t bytes, hipStream_t s);
 // Paged calls: chunk offsets from the block tables (segment rows index bids),
 // and zeroing of every chunk of segments whose verdict is not OK.
 hipError_t launch_chunk_table(const SegDesc* segs, uint32_t n_segs, const uint32_t* bids, uint32_t n_layers,

@@ -564,62 +564,29 @@ __global__ __launch_bounds__(64) void k_small(GcmArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Segment-table expansion: per-segment tile counts -> exclusive prefix
-// (tile_base), and the list of small segments.  One workgroup.
+// First kernel of a call.  It copies the call's staged tables (descriptors,
+// tile queue, tile_base, small list, zeroed queue head, ...) from the mapped
+// host ring into device scratch, and settles every segment's first verdict:
+// with labels, the owner check (OWNER_MIXED iff some row label differs from
+// the segment's user; the sentinels never equal a user), else OK.  The check
+// reads descriptors and block ids where the copy reads them, so the two parts
+// never wait on each other.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(1024) void k_expand(const SegDesc* __restrict__ segs, uint32_t n,
-                                                 uint32_t* __restrict__ tile_base, uint32_t* __restrict__ small_list,
-                                                 int32_t* __restrict__ verdicts, int init_verdicts,
-                                                 uint32_t* __restrict__ tile_counter) {
-  __shared__ uint32_t sc_t[1024], sc_s[1024];
-  const uint32_t tid = threadIdx.x;
-  if (tid == 0) *tile_counter = 0u;  // the tile kernel's work queue starts at entry 0
-  uint32_t carry_t = 0, carry_s = 0;
-  for (uint32_t b0 = 0; b0 < n; b0 += 1024) {
-    const uint32_t i = b0 + tid;
-    uint32_t nt = 0, sm = 0;
-    if (i < n) {
-      if (segs[i].flags & kSegSmall)
-        sm = 1;
-      else
-        nt = (uint32_t)(((uint64_t)segs[i].nblocks + kTileBlocks - 1) / kTileBlocks);
-      if (init_verdicts) verdicts[i] = kVerdictOk;
-    }
-    sc_t[tid] = nt;
-    sc_s[tid] = sm;
-    __syncthreads();
-    for (uint32_t o = 1; o < 1024; o <<= 1) {
-      const uint32_t vt = tid >= o ? sc_t[tid - o] : 0u, vs = tid >= o ? sc_s[tid - o] : 0u;
-      __syncthreads();
-      sc_t[tid] += vt;
-      sc_s[tid] += vs;
-      __syncthreads();
-    }
-    if (i < n) {
-      tile_base[i] = carry_t + sc_t[tid] - nt;
-      if (sm) small_list[carry_s + sc_s[tid] - sm] = i;
-    }
-    carry_t += sc_t[1023];
-    carry_s += sc_s[1023];
-    __syncthreads();
-  }
-  if (tid == 0) tile_base[n] = carry_t;
-}
-
-// ---------------------------------------------------------------------------
-// Owner-label check: verdict OWNER_MIXED iff some row label differs from the
-// segment's user (the sentinels never equal a user).
-// ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void k_check_owner(const SegDesc* __restrict__ segs, uint32_t n,
-                                                     const uint32_t* __restrict__ labels,
-                                                     const uint32_t* __restrict__ bids,
-                                                     int32_t* __restrict__ verdicts) {
+__global__ __launch_bounds__(256) void k_prologue(uint4* __restrict__ dst, const uint4* __restrict__ src, size_t n16,
+                                                  const SegDesc* __restrict__ segs, uint32_t n,
+                                                  const uint32_t* __restrict__ labels,
+                                                  const uint32_t* __restrict__ bids, int32_t* __restrict__ verdicts) {
+  const size_t gsz = (size_t)gridDim.x * blockDim.x;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += gsz) dst[i] = src[i];
+  if (!verdicts) return;
   for (uint32_t s = blockIdx.x; s < n; s += gridDim.x) {
-    const uint64_t rb = segs[s].row_begin, rc = segs[s].row_count;
-    const uint32_t user = segs[s].user;
     int bad = 0;
-    for (uint64_t r = threadIdx.x; r < rc; r += blockDim.x) bad |= labels[bids ? bids[rb + r] : rb + r] != user;
-    bad = __syncthreads_or(bad);
+    if (labels) {
+      const uint64_t rb = segs[s].row_begin, rc = segs[s].row_count;
+      const uint32_t user = segs[s].user;
+      for (uint64_t r = threadIdx.x; r < rc; r += blockDim.x) bad |= labels[bids ? bids[rb + r] : rb + r] != user;
+      bad = __syncthreads_or(bad);
+    }
     if (threadIdx.x == 0) verdicts[s] = bad ? kVerdictOwnerMixed : kVerdictOk;
   }
 }
@@ -651,13 +618,6 @@ __global__ __launch_bounds__(256) void k_wipe(uint8_t* p, size_t bytes) {
   for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < bytes; i += gsz) p[i] = 0;
 }
 
-// A call's descriptors, read straight from the pinned host staging ring into
-// device scratch by a kernel on the call's stream: no DMA engine has to
-// synchronise with the compute queue between the upload and the kernels.
-__global__ __launch_bounds__(256) void k_copy_in(uint4* __restrict__ dst, const uint4* __restrict__ src, size_t n16) {
-  const size_t gsz = (size_t)gridDim.x * blockDim.x;
-  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += gsz) dst[i] = src[i];
-}
 
 // ---------------------------------------------------------------------------
 // Per-token encryption (token || nonce as one block under the owner's key,
@@ -840,20 +800,7 @@ hipError_t launch_key_setup(const uint8_t* keys_dev, KeyTableDev kt, hipStream_t
   return hipGetLastError();
 }
 
-hipError_t launch_check_owner(const SegDesc* segs, uint32_t n_segs, const uint32_t* labels, const uint32_t* bids,
-                              int32_t* verdicts, hipStream_t s) {
-  if (n_segs == 0) return hipSuccess;
-  const uint32_t grid = n_segs < 65535u ? n_segs : 65535u;
-  hipLaunchKernelGGL(k_check_owner, dim3(grid), dim3(256), 0, s, segs, n_segs, labels, bids, verdicts);
-  return hipGetLastError();
-}
 
-hipError_t launch_expand(const SegDesc* segs, uint32_t n_segs, uint32_t* tile_base, uint32_t* small_list,
-                         int32_t* verdicts, bool init_verdicts, uint32_t* tile_counter, hipStream_t s) {
-  hipLaunchKernelGGL(k_expand, dim3(1), dim3(1024), 0, s, segs, n_segs, tile_base, small_list, verdicts,
-                     init_verdicts ? 1 : 0, tile_counter);
-  return hipGetLastError();
-}
 
 hipError_t launch_gcm_tiles(const GcmArgs& a, int mode, uint32_t grid, hipStream_t s) {
   if (a.n_tiles == 0) return hipSuccess;
@@ -930,13 +877,21 @@ hipError_t launch_zero_chunks(const SegDesc* segs, uint32_t n_segs, const uint32
   return hipGetLastError();
 }
 
-hipError_t launch_copy_in(void* dst, const void* src_host, size_t bytes, hipStream_t s) {
-  if (bytes == 0) return hipSuccess;
-  if ((bytes | (uintptr_t)dst | (uintptr_t)src_host) & 15u) return hipErrorInvalidValue;
-  const size_t n16 = bytes / 16;
-  uint32_t grid = cdiv(n16, 256u);
-  if (grid > 64u) grid = 64u;
-  hipLaunchKernelGGL(k_copy_in, dim3(grid), dim3(256), 0, s, (uint4*)dst, (const uint4*)src_host, n16);
+
+hipError_t launch_prologue(void* dst, const void* src, size_t bytes, uint32_t n_segs, uint64_t bids_off,
+                           const uint32_t* labels, int32_t* verdicts, hipStream_t s) {
+  if (bytes & 15u) return hipErrorInvalidValue;
+  const size_t n16 = src ? bytes / 16 : 0;
+  if (n16 == 0 && !verdicts) return hipSuccess;
+  if (n16 && (((uintptr_t)dst | (uintptr_t)src) & 15u)) return hipErrorInvalidValue;
+  const uint8_t* rd = src ? (const uint8_t*)src : (const uint8_t*)dst;  // where the tables are readable now
+  uint64_t grid = cdiv(n16, 256u);
+  if (verdicts && n_segs > grid) grid = n_segs;
+  if (grid > 1024u) grid = 1024u;
+  if (grid == 0) grid = 1;
+  hipLaunchKernelGGL(k_prologue, dim3((uint32_t)grid), dim3(256), 0, s, (uint4*)dst, (const uint4*)src, n16,
+                     (const SegDesc*)rd, n_segs, labels,
+                     bids_off == kNoBids ? (const uint32_t*)nullptr : (const uint32_t*)(rd + bids_off), verdicts);
   return hipGetLastError();
 }
 
