@@ -50,7 +50,7 @@ void tile_order(const SegDesc* descs, uint32_t n_segs, uint32_t n_tiles, TileEnt
     if (descs[i].flags & kSegSmall) continue;
     const uint64_t m = descs[i].nblocks;
     const uint32_t nt = (uint32_t)((m + kTileBlocks - 1) / kTileBlocks);
-    for (uint32_t t = 0; t < nt; t++, g++) order[pos[rows_of(m, t)]++] = TileEnt{g, i, t, 0u};
+    for (uint32_t t = 0; t < nt; t++, g++) order[pos[rows_of(m, t)]++] = TileEnt{g, i, t, descs[i].user};
   }
 }
 

@@ -71,9 +71,10 @@ struct KeyTableDev {
 };
 
 // One entry of the tile kernel's work queue: tile g (in tile_base numbering)
-// is tile t of segment s, counted from the segment's end.
+// is tile t of segment s, counted from the segment's end; user is the
+// segment's user.
 struct TileEnt {
-  uint32_t g, s, t, pad;
+  uint32_t g, s, t, user;
 };
 static_assert(sizeof(TileEnt) == 16, "TileEnt layout");
 constexpr uint32_t kNoTile = 0xFFFFFFFFu;

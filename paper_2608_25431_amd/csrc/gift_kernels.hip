@@ -33,8 +33,18 @@ constexpr uint32_t kLdsAes = 8192;                  // T0/T1 (64 KiB) then T2/T3
 constexpr uint32_t kLdsFold = kLdsAes + 131072;     // 32 x 16 x 16 B GHASH tables of W
 constexpr uint32_t kLdsStage = kLdsFold + 8192;     // lane partials of the waves that are not leaders
 constexpr uint32_t kLdsRed = kLdsStage + 16 * (kThreads - 64 * kLeaders);  // one 16 B slot per leader
-constexpr uint32_t kLdsInfo = kLdsRed + 16 * kLeaders;  // broadcast scratch
-constexpr uint32_t kLdsBytes = kLdsInfo + 16;
+constexpr uint32_t kLdsInfo = kLdsRed + 16 * kLeaders;  // TileInfo of the current tile
+
+// The current tile's record in LDS, staged by the prefetch waves.
+struct TileInfo {
+  uint32_t g, s, t, user;  // queue entry
+  int32_t verdict;
+  uint32_t next_k;  // queue entry claimed for the next tile
+  uint32_t pad[2];
+  SegDesc desc;
+  uint32_t rk[64];  // round keys (60 used)
+};
+constexpr uint32_t kLdsBytes = kLdsInfo + sizeof(TileInfo);
 static_assert(kLdsBytes <= 160u * 1024u, "LDS of a gfx950 workgroup");
 
 __device__ __forceinline__ uint32_t lds32(const uint8_t* base, uint32_t off) {
@@ -270,7 +280,6 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
   const uint32_t tid = threadIdx.x;
   uint8_t* tt = smem + kLdsAes;
   const uint8_t* gt = smem + kLdsGtab;
-  uint32_t* info = (uint32_t*)(smem + kLdsInfo);
   u128* red = (u128*)(smem + kLdsRed);
 
   // Replicated T-tables: word w = region*16384 + x*64 + slot holds
@@ -283,50 +292,79 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
     ((uint32_t*)tt)[w] = (v << sh) | (v >> ((32u - sh) & 31u));
   }
   const uint32_t L = ((tid & 31u) << 2) | 0x10000u;  // this lane's table copy
-  uint32_t cur_user = 0xFFFFFFFFu;
-
-  const SegDesc* __restrict__ segs = a.segs;
+  uint32_t cur_user = 0xFFFFFFFFu;  // user whose GHASH tables are in LDS
+  TileInfo* ti = (TileInfo*)(smem + kLdsInfo);
 
   // Work queue over the host's tile order (longest tiles first): workgroup b
-  // takes entry b first, then entries gridDim.x + (queue claims).  Thread 0
-  // issues each claim when a tile starts and loads the claimed entry once the
-  // tile's rows are done, so neither latency sits between two tiles; every
-  // wave leaves the loop on the same entry.
-  uint32_t claim = blockIdx.x;  // thread 0: the entry after the current one
-  TileEnt nx = TileEnt{kNoTile, 0u, 0u, 0u};
-  auto fetch_next = [&]() {
-    if (tid == 0) nx = claim < a.n_tiles ? a.tile_order[claim] : TileEnt{kNoTile, 0u, 0u, 0u};
-  };
-  fetch_next();
-  for (;;) {
-    __syncthreads();  // previous tile finished with gtab, red and info
-    if (tid == 0) {
-      info[0] = nx.g;
-      info[1] = nx.s;
-      info[2] = nx.t;
-      if (nx.g != kNoTile) claim = gridDim.x + atomicAdd(a.tile_counter, 1u);
+  // takes entry b first, then entries gridDim.x + (queue claims); the claim
+  // is issued when a tile starts.  While the leader waves fold a tile's GHASH
+  // partials, the other waves (the prefetch waves) load the next tile's
+  // entry, descriptor, verdict, round keys and, for a new user, the tables of
+  // M into LDS (nothing reads them then) and the tables of W into registers
+  // (the fold still reads W), so no global-memory latency sits between two
+  // tiles.  Every wave leaves the loop on the same entry.
+  constexpr uint32_t kPf0 = 64u * kLeaders;  // first thread of the prefetch waves
+  static_assert(kThreads - kPf0 > 592u, "prefetch roles");
+  uint32_t claim = 0;  // thread kPf0: queue entry of the next tile
+  bool pf_tabs = false;  // this thread holds entry j of the next user's W tables
+  uint4 pf_w = make_uint4(0u, 0u, 0u, 0u);
+  // thread kPf0 + j: j < 512 tables; 512 + i descriptor word i (i < 16);
+  // 528 + i round-key word i (i < 64); 592 entry and verdict
+  auto prefetch = [&](uint32_t k) {
+    const uint32_t j = tid - kPf0;
+    const TileEnt e = k < a.n_tiles ? a.tile_order[k] : TileEnt{kNoTile, 0u, 0u, 0u};
+    pf_tabs = false;
+    if (j == 592u) {
+      ti->g = e.g;
+      ti->s = e.s;
+      ti->t = e.t;
+      ti->user = e.user;
     }
-    __syncthreads();
-    const uint32_t g = __builtin_amdgcn_readfirstlane(info[0]);
+    if (e.g == kNoTile) return;
+    const uint32_t u = e.user;
+    if (j < 512u) {
+      if (u != cur_user) {
+        pf_tabs = true;
+        ((uint4*)(smem + kLdsGtab))[j] = a.kt.gtab[(size_t)u * 512u + j];
+        pf_w = a.kt.gtab_fold[(size_t)u * 512u + j];
+      }
+    } else if (j < 528u) {
+      ((uint32_t*)&ti->desc)[j - 512u] = ((const uint32_t*)(a.segs + e.s))[j - 512u];
+    } else if (j < 592u) {
+      ti->rk[j - 528u] = a.kt.rk[(size_t)u * 64u + (j - 528u)];
+    } else if (j == 592u) {
+      ti->verdict = a.verdicts[e.s];
+    }
+  };
+  auto commit = [&]() {
+    if (pf_tabs) ((uint4*)(smem + kLdsFold))[tid - kPf0] = pf_w;
+  };
+  if (tid >= kPf0) prefetch(blockIdx.x);
+
+  for (;;) {
+    commit();
+    __syncthreads();  // the tile's record and tables are in LDS; the previous tile is done with them
+    const uint32_t g = __builtin_amdgcn_readfirstlane(ti->g);
     if (g == kNoTile) break;
-    const uint32_t s = __builtin_amdgcn_readfirstlane(info[1]);
-    const uint32_t t = __builtin_amdgcn_readfirstlane(info[2]);
-    const SegDesc* sd = segs + s;
-    const uint32_t user = sd->user;
-    const uint32_t m = sd->nblocks;
-    const uint64_t off = sd->byte_off, len = sd->len;
-    const bool aligned = (sd->flags & kSegAligned) != 0;
-    const int32_t verdict = a.verdicts[s];
+    if (tid == kPf0) claim = gridDim.x + atomicAdd(a.tile_counter, 1u);
+    const uint32_t t = __builtin_amdgcn_readfirstlane(ti->t);
+    const uint32_t user = __builtin_amdgcn_readfirstlane(ti->user);
+    const int32_t verdict = (int32_t)__builtin_amdgcn_readfirstlane((uint32_t)ti->verdict);
+    cur_user = user;
+    const uint32_t m = __builtin_amdgcn_readfirstlane(ti->desc.nblocks);
+    const uint64_t off = ti->desc.byte_off, len = ti->desc.len;
+    const bool aligned = (__builtin_amdgcn_readfirstlane(ti->desc.flags) & kSegAligned) != 0;
     const int64_t base = (int64_t)m - (int64_t)(t + 1) * (int64_t)kTileBlocks;  // block index of virtual slot 0
     const int r_start = base < 0 ? (int)((uint64_t)(-base) / kThreads) : 0;
 
     // paged side: block i of the segment lives in chunk i >> shift
-    const uint64_t chunk0 = sd->chunk0;
+    const uint64_t chunk0 = ti->desc.chunk0;
     const uint64_t cmask = (1ull << a.chunk_shift) - 1;
     auto paged = [&](uint64_t i) -> uint8_t* {
       return a.pbase + a.chunk_off[chunk0 + (i >> a.chunk_shift)] + ((i & cmask) << 4);
     };
 
+    u128 y = u128_zero();
     if (verdict != kVerdictOk) {
       // rejected before this call's data is touched: release zeros only
       for (int r = r_start; r < kRows; r++) {
@@ -337,83 +375,69 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
           store_block(dst, u128_zero(), rem >= 16 ? 16u : (uint32_t)rem, aligned);
         }
       }
-      fetch_next();
-      continue;
-    }
+    } else {
+      // Tile-uniform values live in SGPRs: the kernel also stores to global
+      // memory, so the compiler cannot prove these loads unclobbered and would
+      // otherwise keep all 60 round-key words in VGPRs.
+      uint32_t rk[60];
+  #pragma unroll
+      for (int i = 0; i < 60; i++) rk[i] = __builtin_amdgcn_readfirstlane(ti->rk[i]);
+      const uint32_t k0 = __builtin_amdgcn_readfirstlane(ti->desc.iv[0]) ^ rk[0];
+      const uint32_t k1 = __builtin_amdgcn_readfirstlane(ti->desc.iv[1]) ^ rk[1];
+      const uint32_t k2 = __builtin_amdgcn_readfirstlane(ti->desc.iv[2]) ^ rk[2];
 
-    if (user != cur_user) {
-      const uint4* src = a.kt.gtab + (size_t)user * 512u;
-      const uint4* srcw = a.kt.gtab_fold + (size_t)user * 512u;
-      for (uint32_t i = tid; i < 512u; i += kThreads) {
-        ((uint4*)(smem + kLdsGtab))[i] = src[i];
-        ((uint4*)(smem + kLdsFold))[i] = srcw[i];
-      }
-      cur_user = user;
-      __syncthreads();
-    }
+      CtrCache cc;
+      const uint32_t c0 = 2u + (uint32_t)(base + (int64_t)tid);  // counter of this lane in row 0, mod 2^32
+      ctr_cache_init(cc, k0, k1, k2, c0, rk, tt, L);
 
-    // Tile-uniform values live in SGPRs: the kernel also stores to global
-    // memory, so the compiler cannot prove these loads unclobbered and would
-    // otherwise keep all 60 round-key words in VGPRs.
-    uint32_t rk[60];
-    const uint32_t* rkp = a.kt.rk + (size_t)user * 64u;
-#pragma unroll
-    for (int i = 0; i < 60; i++) rk[i] = __builtin_amdgcn_readfirstlane(rkp[i]);
-    const uint32_t k0 = __builtin_amdgcn_readfirstlane(sd->iv[0]) ^ rk[0];
-    const uint32_t k1 = __builtin_amdgcn_readfirstlane(sd->iv[1]) ^ rk[1];
-    const uint32_t k2 = __builtin_amdgcn_readfirstlane(sd->iv[2]) ^ rk[2];
+      // rows where every lane holds a whole block and the segment is 16-byte
+      // aligned take the branch-free path
+      const int r_full = base < 0 ? (int)(((uint64_t)(-base) + kThreads - 1) / kThreads) : 0;
+      const int r_end_full = (t == 0 && (len & 15u)) ? kRows - 1 : kRows;
 
-    CtrCache cc;
-    const uint32_t c0 = 2u + (uint32_t)(base + (int64_t)tid);  // counter of this lane in row 0, mod 2^32
-    ctr_cache_init(cc, k0, k1, k2, c0, rk, tt, L);
-
-    // rows where every lane holds a whole block and the segment is 16-byte
-    // aligned take the branch-free path
-    const int r_full = base < 0 ? (int)(((uint64_t)(-base) + kThreads - 1) / kThreads) : 0;
-    const int r_end_full = (t == 0 && (len & 15u)) ? kRows - 1 : kRows;
-
-    u128 y = u128_zero();
-    for (int r = r_start; r < kRows; r++) {
-      // the whole-block rows load their input before the AES rounds, so the
-      // HBM latency overlaps the keystream
-      const bool fast = aligned && r >= r_full && r < r_end_full;
-      const uint8_t* src = nullptr;
-      uint8_t* dst = nullptr;
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (fast) {
-        // every lane's block index is >= 0 in these rows; pointer arithmetic
-        // (not integers) keeps the global address space for the compiler
-        const uint64_t i0 = (uint64_t)(base + (int64_t)r * kThreads + tid);
-        src = GATHER ? paged(i0) : a.in + off + 16ull * i0;
-        dst = SCATTER ? paged(i0) : a.out + off + 16ull * i0;
-        v = *(const uint4*)src;
-      }
-      uint32_t x0, x1, x2, x3;
-      ctr_rounds12(cc, c0 + (uint32_t)kThreads * (uint32_t)r, x0, x1, x2, x3, rk, tt, L);
-      aes_rounds_lds<3>(x0, x1, x2, x3, rk, tt, L);
-      u128 x;
-      if (fast) {
-        const uint4 o = make_uint4(v.x ^ x0, v.y ^ x1, v.z ^ x2, v.w ^ x3);
-        *(uint4*)dst = o;
-        x = OPEN ? u128{{v.x, v.y, v.z, v.w}} : u128{{o.x, o.y, o.z, o.w}};
-      } else {
-        x = u128_zero();
-        const int64_t i0 = base + (int64_t)r * kThreads + tid;
-        if (i0 >= 0) {
-          const uint64_t boff = off + 16ull * (uint64_t)i0;
-          const uint64_t rem = len - 16ull * (uint64_t)i0;
-          const uint32_t n = rem >= 16 ? 16u : (uint32_t)rem;
-          const u128 in = load_block(GATHER ? paged((uint64_t)i0) : a.in + boff, n, aligned);
-          const u128 o = mask_block(u128{{in.w[0] ^ x0, in.w[1] ^ x1, in.w[2] ^ x2, in.w[3] ^ x3}}, n);
-          store_block(SCATTER ? paged((uint64_t)i0) : a.out + boff, o, n, aligned);
-          x = OPEN ? in : o;
+      for (int r = r_start; r < kRows; r++) {
+        // the whole-block rows load their input before the AES rounds, so the
+        // HBM latency overlaps the keystream
+        const bool fast = aligned && r >= r_full && r < r_end_full;
+        const uint8_t* src = nullptr;
+        uint8_t* dst = nullptr;
+        uint4 v = make_uint4(0, 0, 0, 0);
+        if (fast) {
+          // every lane's block index is >= 0 in these rows; pointer arithmetic
+          // (not integers) keeps the global address space for the compiler
+          const uint64_t i0 = (uint64_t)(base + (int64_t)r * kThreads + tid);
+          src = GATHER ? paged(i0) : a.in + off + 16ull * i0;
+          dst = SCATTER ? paged(i0) : a.out + off + 16ull * i0;
+          v = *(const uint4*)src;
         }
+        uint32_t x0, x1, x2, x3;
+        ctr_rounds12(cc, c0 + (uint32_t)kThreads * (uint32_t)r, x0, x1, x2, x3, rk, tt, L);
+        aes_rounds_lds<3>(x0, x1, x2, x3, rk, tt, L);
+        u128 x;
+        if (fast) {
+          const uint4 o = make_uint4(v.x ^ x0, v.y ^ x1, v.z ^ x2, v.w ^ x3);
+          *(uint4*)dst = o;
+          x = OPEN ? u128{{v.x, v.y, v.z, v.w}} : u128{{o.x, o.y, o.z, o.w}};
+        } else {
+          x = u128_zero();
+          const int64_t i0 = base + (int64_t)r * kThreads + tid;
+          if (i0 >= 0) {
+            const uint64_t boff = off + 16ull * (uint64_t)i0;
+            const uint64_t rem = len - 16ull * (uint64_t)i0;
+            const uint32_t n = rem >= 16 ? 16u : (uint32_t)rem;
+            const u128 in = load_block(GATHER ? paged((uint64_t)i0) : a.in + boff, n, aligned);
+            const u128 o = mask_block(u128{{in.w[0] ^ x0, in.w[1] ^ x1, in.w[2] ^ x2, in.w[3] ^ x3}}, n);
+            store_block(SCATTER ? paged((uint64_t)i0) : a.out + boff, o, n, aligned);
+            x = OPEN ? in : o;
+          }
+        }
+        // GHASH table reads at a priority between the AES issue and combine
+        // phases; the next AES round sets its own
+        __builtin_amdgcn_s_setprio(1);
+        y = ghash_step_lds(y, x, gt);
       }
-      // GHASH table reads at a priority between the AES issue and combine
-      // phases; the next AES round sets its own
-      __builtin_amdgcn_s_setprio(1);
-      y = ghash_step_lds(y, x, gt);
-    }
+
+    }  // verdict OK
 
     // Tile partial: lane tid contributes y * H^(kThreads + 1 - tid), its
     // distance from the tile end plus the H^2 that every block's GHASH term
@@ -421,23 +445,26 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
     // H^(64*kLeaders*(kFold - 1 - i)) * H^(64*kLeaders + 1 - 64*g - lane): leader
     // g folds its waves by Horner in W = H^(64*kLeaders) from the LDS tables,
     // then multiplies once by the per-lane power.
-    fetch_next();  // its load overlaps the tile end
+    const bool fold = verdict == kVerdictOk;
     const uint32_t wave = tid >> 6, lane = tid & 63u;
     u128* stage = (u128*)(smem + kLdsStage);
+    if (tid == kPf0) ti->next_k = claim;
     // the leaders fetch their lane's power before the barrier, so the load
     // overlaps the wait for the other waves
     u128 hp = u128_zero();
-    if (wave < (uint32_t)kLeaders)
+    if (fold && wave < (uint32_t)kLeaders)
       hp = ld_u128(a.kt.pow_h + (size_t)user * kHPowers + (64u * kLeaders + 1u - 64u * wave - lane));
-    if (wave >= (uint32_t)kLeaders) stage[tid - 64u * kLeaders] = y;
+    if (fold && wave >= (uint32_t)kLeaders) stage[tid - kPf0] = y;
     __syncthreads();
-    if (wave < (uint32_t)kLeaders) {
+    if (wave >= (uint32_t)kLeaders) {
+      prefetch(ti->next_k);  // overlaps the fold
+    } else if (fold) {
       const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_byte*)smem;
       tile_fold(y, lds0 + kLdsStage + 16u * (wave * 64u + lane), lds0 + kLdsFold, hp, lds0 + kLdsRed + 16u * wave,
                 lane);
     }
     __syncthreads();
-    if (tid == 0) {
+    if (fold && tid == 0) {
       u128 p = red[0];
       for (int w = 1; w < kLeaders; w++) p = u128_xor(p, red[w]);
       st_u128(a.partials + g, p);
