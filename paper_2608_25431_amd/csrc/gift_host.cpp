@@ -396,6 +396,7 @@ struct Plan {
   std::vector<ZeroRange> zr;
   uint32_t n_tiles = 0;
   uint32_t n_small = 0;
+  uint32_t n_multi = 0;
 };
 
 enum class Check { kOwner, kGcm, kBlock };
@@ -478,11 +479,13 @@ void build_plan(const gift_segment* segs, uint32_t n, uint64_t n_rows, uint64_t 
     }
     const bool aligned = ((((uintptr_t)in + d.byte_off) | ((uintptr_t)out + d.byte_off)) & 15u) == 0;
     const bool small = nb <= kSmallMaxBlocks;
-    d.flags = (aligned ? kSegAligned : 0u) | (small ? kSegSmall : 0u);
+    const bool one = !small && nb <= kTileBlocks;
+    d.flags = (aligned ? kSegAligned : 0u) | (small ? kSegSmall : 0u) | (one ? kSegOneTile : 0u);
     if (small)
       P.n_small++;
     else
       P.n_tiles += (uint32_t)((nb + kTileBlocks - 1) / kTileBlocks);
+    if (!small && !one) P.n_multi++;
     cover[i] = {s.row_begin, s.row_count};
   }
   if (!std::is_sorted(cover.begin(), cover.end())) std::sort(cover.begin(), cover.end());
@@ -543,7 +546,7 @@ gift_status run_gcm(const gift_tensor* t, const gift_segment_table* st, gift_key
   build_plan(st->segs, n, t->n_rows, t->row_bytes, nonce_base, t->data, out, OPEN, P);
 
   // scratch: the staged tables (descs | zero ranges | tile queue | tile_base |
-  // small list | queue head), then partials | verdicts
+  // small list | queue head), then partials | verdicts | one-tile tag masks
   const size_t o_desc = 0;
   const size_t o_zr = o_desc + align256(sizeof(SegDesc) * n);
   const size_t o_to = o_zr + align256(sizeof(ZeroRange) * P.zr.size());
@@ -552,7 +555,8 @@ gift_status run_gcm(const gift_tensor* t, const gift_segment_table* st, gift_key
   const size_t o_qh = o_sl + align256(4ull * (n ? n : 1));
   const size_t o_pt = o_qh + 256;  // end of the staged tables
   const size_t o_vd = o_pt + align256(16ull * (P.n_tiles ? P.n_tiles : 1));
-  const size_t bytes = o_vd + align256(4ull * (n ? n : 1));
+  const size_t o_fn = o_vd + align256(4ull * (n ? n : 1));
+  const size_t bytes = o_fn + align256(16ull * (n ? n : 1));
   ScratchLease lease;
   hipError_t e = lease.acquire(dev, stream, bytes);
   if (e != hipSuccess) return hip_fail(e, "device scratch");
@@ -568,7 +572,8 @@ gift_status run_gcm(const gift_tensor* t, const gift_segment_table* st, gift_key
   if (!sg) return fail(GIFT_E_INVALID, "device index %d unsupported", dev);
   // the prologue copies the tables and settles the verdicts (owner check)
   e = sg->upload(scratch, host.data(), o_pt, stream, [&](const void* src) {
-    return launch_prologue(scratch, src, o_pt, n, kNoBids, st->row_labels, n ? verdicts : nullptr, stream);
+    return launch_prologue(scratch, src, o_pt, n, kNoBids, st->row_labels, n ? verdicts : nullptr, &kt->dev,
+                           (uint4*)(scratch + o_fn), stream);
   });
   if (e != hipSuccess) return hip_fail(e, "staging upload");
 
@@ -576,7 +581,7 @@ gift_status run_gcm(const gift_tensor* t, const gift_segment_table* st, gift_key
   gift_status rs = GIFT_OK;
   do {
     if (n > 0) {
-      GcmArgs a;
+      GcmArgs a{};  // zero-initialised: no field is left undefined
       a.in = (const uint8_t*)t->data;
       a.out = (uint8_t*)out;
       a.chunk_off = nullptr;
@@ -588,7 +593,9 @@ gift_status run_gcm(const gift_tensor* t, const gift_segment_table* st, gift_key
       a.small_list = (const uint32_t*)(scratch + o_sl);
       a.n_tiles = P.n_tiles;
       a.n_small = P.n_small;
+      a.n_multi = P.n_multi;
       a.partials = (uint4*)(scratch + o_pt);
+      a.fin = (const uint4*)(scratch + o_fn);
       a.tile_order = (const TileEnt*)(scratch + o_to);
       a.tile_counter = (uint32_t*)(scratch + o_qh);
       a.verdicts = verdicts;
@@ -731,7 +738,7 @@ gift_status run_paged(const gift_paged_kv* kv, const gift_request* reqs, uint32_
   // descriptors: rows = positions in the uploaded block-id array
   std::vector<SegDesc> descs(n);
   uint64_t boff = 0, bpos = 0, cpos = 0;
-  uint32_t n_tiles = 0;
+  uint32_t n_tiles = 0, n_multi = 0;
   for (uint32_t i = 0; i < n; i++) {
     const gift_request& r = reqs[i];
     SegDesc& d = descs[i];
@@ -742,7 +749,8 @@ gift_status run_paged(const gift_paged_kv* kv, const gift_request* reqs, uint32_
     d.row_count = r.n_block_ids;
     d.user = r.user;
     d.nblocks = (uint32_t)(d.len / 16);
-    d.flags = kSegAligned;
+    d.flags = kSegAligned | (d.nblocks <= kTileBlocks ? kSegOneTile : 0u);
+    if (d.nblocks > kTileBlocks) n_multi++;
     d.chunk0 = cpos;
     uint8_t iv[12];
     memcpy(iv, nonce_base + 12ull * r.user, 12);
@@ -759,7 +767,8 @@ gift_status run_paged(const gift_paged_kv* kv, const gift_request* reqs, uint32_
   while ((16ull << shift) < kv->chunk_bytes) shift++;
 
   // scratch: the staged tables (descs | block ids | tile queue | tile_base |
-  // small list | queue head), then partials | verdicts | chunk offsets
+  // small list | queue head), then partials | verdicts | chunk offsets |
+  // one-tile tag masks
   const size_t o_desc = 0;
   const size_t o_bid = o_desc + align256(sizeof(SegDesc) * n);
   const size_t o_to = o_bid + align256(4ull * total_bids);
@@ -769,7 +778,8 @@ gift_status run_paged(const gift_paged_kv* kv, const gift_request* reqs, uint32_
   const size_t o_pt = o_qh + 256;  // end of the staged tables
   const size_t o_vd = o_pt + align256(16ull * (n_tiles ? n_tiles : 1));
   const size_t o_ck = o_vd + align256(4ull * n);
-  const size_t bytes = o_ck + align256(8ull * cpos);
+  const size_t o_fn = o_ck + align256(8ull * cpos);
+  const size_t bytes = o_fn + align256(16ull * (n ? n : 1));
   ScratchLease lease;
   hipError_t e = lease.acquire(dev, stream, bytes);
   if (e != hipSuccess) return hip_fail(e, "device scratch");
@@ -790,7 +800,8 @@ gift_status run_paged(const gift_paged_kv* kv, const gift_request* reqs, uint32_
   // the prologue copies the tables and settles the verdicts (owner check by block id)
   e = sg ? sg->upload(scratch, host.data(), o_pt, stream,
                       [&](const void* src) {
-                        return launch_prologue(scratch, src, o_pt, n, o_bid, labels, verdicts, stream);
+                        return launch_prologue(scratch, src, o_pt, n, o_bid, labels, verdicts, &kt->dev,
+                                               (uint4*)(scratch + o_fn), stream);
                       })
          : hipErrorInvalidDevice;
   if (e != hipSuccess) return hip_fail(e, "staging upload");
@@ -805,7 +816,7 @@ gift_status run_paged(const gift_paged_kv* kv, const gift_request* reqs, uint32_
       rs = hip_fail(e, "paged expansion");
       break;
     }
-    GcmArgs a;
+    GcmArgs a{};  // zero-initialised: no field is left undefined
     a.in = (const uint8_t*)in;
     a.out = (uint8_t*)out;
     a.chunk_off = d_ck;
@@ -816,8 +827,10 @@ gift_status run_paged(const gift_paged_kv* kv, const gift_request* reqs, uint32_
     a.tile_base = (const uint32_t*)(scratch + o_tb);
     a.small_list = (const uint32_t*)(scratch + o_sl);
     a.n_tiles = n_tiles;
+    a.n_multi = n_multi;
     a.n_small = 0;
     a.partials = (uint4*)(scratch + o_pt);
+    a.fin = (const uint4*)(scratch + o_fn);
     a.tile_order = (const TileEnt*)(scratch + o_to);
     a.tile_counter = (uint32_t*)(scratch + o_qh);
     a.verdicts = verdicts;
@@ -1001,7 +1014,8 @@ gift_status gift_check_owner(const gift_segment_table* st, const uint32_t* label
   Staging* sg = staging_for(dev);
   e = sg ? sg->upload(d, P.descs.data(), bytes, stream,
                       [&](const void* src) {
-                        return launch_prologue(d, src, bytes, n, kNoBids, labels, st->verdicts, stream);
+                        return launch_prologue(d, src, bytes, n, kNoBids, labels, st->verdicts, nullptr, nullptr,
+                                               stream);
                       })
          : hipErrorInvalidDevice;
   hipError_t e2 = lease.release();
@@ -1041,7 +1055,8 @@ static gift_status run_tokens(bool decrypt, const gift_segment_table* st, uint64
     const size_t bytes = sizeof(SegDesc) * n;
     e = sg ? sg->upload(d, P.descs.data(), bytes, stream,
                         [&](const void* src) {
-                          return launch_prologue(d, src, bytes, n, kNoBids, nullptr, nullptr, stream);
+                          return launch_prologue(d, src, bytes, n, kNoBids, nullptr, nullptr, nullptr, nullptr,
+                                                 stream);
                         })
            : hipErrorInvalidDevice;
   }

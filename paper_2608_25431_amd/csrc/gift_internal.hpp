@@ -29,7 +29,9 @@ constexpr int kFinLanes = 64;                              // lanes of the per-s
 constexpr int kLeaders = 4;
 static_assert(kThreads % (64 * kLeaders) == 0, "waves per leader");
 
-enum : uint32_t { kSegAligned = 1u, kSegSmall = 2u };
+// kSegOneTile: a tiled segment of at most kTileBlocks blocks; the tile kernel
+// writes its tag (open: its verdict) itself and the finalize pass skips it.
+enum : uint32_t { kSegAligned = 1u, kSegSmall = 2u, kSegOneTile = 4u };
 
 // Device descriptor of one segment (64 B), built on the host.
 struct SegDesc {
@@ -97,7 +99,9 @@ struct GcmArgs {
   const uint32_t* small_list;  // [n_small] indices of small segments
   uint32_t n_tiles;
   uint32_t n_small;
+  uint32_t n_multi;            // segments of more than one tile (the finalize pass)
   uint4* partials;             // [n_tiles] GHASH partial of each tile
+  const uint4* fin;            // [n_segs] E_K(J0) xor H*L of one-tile segments (from the prologue)
   const TileEnt* tile_order;   // [n_tiles] tiles in the order the workgroups claim them
   uint32_t* tile_counter;      // work-queue head, zeroed by the expansion kernel
   int32_t* verdicts;           // [n_segs]
@@ -113,11 +117,13 @@ hipError_t launch_key_setup(const uint8_t* keys_dev, KeyTableDev kt, hipStream_t
 // mapped host ring; nullptr: they are in dst already) to dst, and, when
 // verdicts is not NULL, writes each segment's first verdict: the owner check
 // against labels (indexed by row, or by the block ids at byte bids_off of the
-// tables for paged calls) or OK without labels.  The descriptors sit at byte 0
-// of the tables.
+// tables for paged calls) or OK without labels.  With a key table it also
+// writes fin[s] = E_K(J0) xor H*L of every one-tile segment s.  The
+// descriptors sit at byte 0 of the tables.
 constexpr uint64_t kNoBids = ~0ull;
 hipError_t launch_prologue(void* dst, const void* src, size_t bytes, uint32_t n_segs, uint64_t bids_off,
-                           const uint32_t* labels, int32_t* verdicts, hipStream_t s);
+                           const uint32_t* labels, int32_t* verdicts, const KeyTableDev* kt, uint4* fin,
+                           hipStream_t s);
 // Tiles longest first: full tiles, then each segment's partial first tile by
 // its number of rows.  order has n_tiles entries.
 void tile_order(const SegDesc* descs, uint32_t n_segs, uint32_t n_tiles, TileEnt* order);

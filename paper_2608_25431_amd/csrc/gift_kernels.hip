@@ -32,8 +32,9 @@ constexpr uint32_t kLdsGtab = 0;                    // 32 x 16 x 16 B GHASH tabl
 constexpr uint32_t kLdsAes = 8192;                  // T0/T1 (64 KiB) then T2/T3 (64 KiB)
 constexpr uint32_t kLdsFold = kLdsAes + 131072;     // 32 x 16 x 16 B GHASH tables of W
 constexpr uint32_t kLdsStage = kLdsFold + 8192;     // lane partials of the waves that are not leaders
-constexpr uint32_t kLdsRed = kLdsStage + 16 * (kThreads - 64 * kLeaders);  // one 16 B slot per leader
-constexpr uint32_t kLdsInfo = kLdsRed + 16 * kLeaders;  // TileInfo of the current tile
+// one 16 B slot per leader, then E_K(J0) xor H*L of a one-tile segment
+constexpr uint32_t kLdsRed = kLdsStage + 16 * (kThreads - 64 * kLeaders);
+constexpr uint32_t kLdsInfo = kLdsRed + 16 * (kLeaders + 1);  // TileInfo of the current tile
 
 // The current tile's record in LDS, staged by the prefetch waves.
 struct TileInfo {
@@ -41,6 +42,7 @@ struct TileInfo {
   int32_t verdict;
   uint32_t next_k;  // queue entry claimed for the next tile
   uint32_t pad[2];
+  uint4 fin;  // one-tile segment: E_K(J0) xor H*L from the prologue
   SegDesc desc;
   uint32_t rk[64];  // round keys (60 used)
 };
@@ -252,11 +254,11 @@ __device__ __forceinline__ u128 length_block(uint64_t len) {
 
 // Tile end of a leader wave (see k_gcm_tiles): Horner over the staged lane
 // partials of its waves in W (LDS tables), one multiply by the lane's power
-// hp, then the wave sum into the leader's reduction slot.  Kept out of line,
-// so that the main loop's register allocation does not see it; the LDS
-// regions arrive as byte offsets, so every access is an LDS instruction.
+// hp, then the wave sum into the leader's reduction slot.  The LDS regions
+// arrive as byte offsets in the LDS address space, so every access is an LDS
+// instruction.
 typedef __attribute__((address_space(3))) uint8_t lds_byte;
-__device__ __noinline__ void tile_fold(u128 v, uint32_t stage_off, uint32_t wt_off, u128 hp, uint32_t red_off,
+__device__ __forceinline__ void tile_fold(u128 v, uint32_t stage_off, uint32_t wt_off, u128 hp, uint32_t red_off,
                                        uint32_t lane) {
   constexpr int kFold = kThreads / 64 / kLeaders;
   const u128* stage = (const u128*)(lds_byte*)(uintptr_t)stage_off;
@@ -304,12 +306,12 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
   // (the fold still reads W), so no global-memory latency sits between two
   // tiles.  Every wave leaves the loop on the same entry.
   constexpr uint32_t kPf0 = 64u * kLeaders;  // first thread of the prefetch waves
-  static_assert(kThreads - kPf0 > 592u, "prefetch roles");
+  static_assert(kThreads - kPf0 > 593u, "prefetch roles");
   uint32_t claim = 0;  // thread kPf0: queue entry of the next tile
   bool pf_tabs = false;  // this thread holds entry j of the next user's W tables
   uint4 pf_w = make_uint4(0u, 0u, 0u, 0u);
   // thread kPf0 + j: j < 512 tables; 512 + i descriptor word i (i < 16);
-  // 528 + i round-key word i (i < 64); 592 entry and verdict
+  // 528 + i round-key word i (i < 64); 592 entry and verdict; 593 fin
   auto prefetch = [&](uint32_t k) {
     const uint32_t j = tid - kPf0;
     const TileEnt e = k < a.n_tiles ? a.tile_order[k] : TileEnt{kNoTile, 0u, 0u, 0u};
@@ -334,6 +336,8 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
       ti->rk[j - 528u] = a.kt.rk[(size_t)u * 64u + (j - 528u)];
     } else if (j == 592u) {
       ti->verdict = a.verdicts[e.s];
+    } else if (j == 593u) {
+      ti->fin = a.fin[e.s];  // meaningful for one-tile segments only
     }
   };
   auto commit = [&]() {
@@ -347,13 +351,17 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
     const uint32_t g = __builtin_amdgcn_readfirstlane(ti->g);
     if (g == kNoTile) break;
     if (tid == kPf0) claim = gridDim.x + atomicAdd(a.tile_counter, 1u);
+    const uint32_t s = __builtin_amdgcn_readfirstlane(ti->s);
     const uint32_t t = __builtin_amdgcn_readfirstlane(ti->t);
     const uint32_t user = __builtin_amdgcn_readfirstlane(ti->user);
     const int32_t verdict = (int32_t)__builtin_amdgcn_readfirstlane((uint32_t)ti->verdict);
     cur_user = user;
     const uint32_t m = __builtin_amdgcn_readfirstlane(ti->desc.nblocks);
     const uint64_t off = ti->desc.byte_off, len = ti->desc.len;
-    const bool aligned = (__builtin_amdgcn_readfirstlane(ti->desc.flags) & kSegAligned) != 0;
+    const uint32_t flags = __builtin_amdgcn_readfirstlane(ti->desc.flags);
+    const bool aligned = (flags & kSegAligned) != 0;
+    const bool one = (flags & kSegOneTile) != 0;
+    if (one && tid == 0) red[kLeaders] = u128{{ti->fin.x, ti->fin.y, ti->fin.z, ti->fin.w}};  // for the tile end
     const int64_t base = (int64_t)m - (int64_t)(t + 1) * (int64_t)kTileBlocks;  // block index of virtual slot 0
     const int r_start = base < 0 ? (int)((uint64_t)(-base) / kThreads) : 0;
 
@@ -363,6 +371,16 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
     auto paged = [&](uint64_t i) -> uint8_t* {
       return a.pbase + a.chunk_off[chunk0 + (i >> a.chunk_shift)] + ((i & cmask) << 4);
     };
+
+    // Tile-uniform values live in SGPRs: the kernel also stores to global
+    // memory, so the compiler cannot prove these loads unclobbered and would
+    // otherwise keep all 60 round-key words in VGPRs.
+    uint32_t rk[60];
+#pragma unroll
+    for (int i = 0; i < 60; i++) rk[i] = __builtin_amdgcn_readfirstlane(ti->rk[i]);
+    const uint32_t k0 = __builtin_amdgcn_readfirstlane(ti->desc.iv[0]) ^ rk[0];
+    const uint32_t k1 = __builtin_amdgcn_readfirstlane(ti->desc.iv[1]) ^ rk[1];
+    const uint32_t k2 = __builtin_amdgcn_readfirstlane(ti->desc.iv[2]) ^ rk[2];
 
     u128 y = u128_zero();
     if (verdict != kVerdictOk) {
@@ -376,16 +394,6 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
         }
       }
     } else {
-      // Tile-uniform values live in SGPRs: the kernel also stores to global
-      // memory, so the compiler cannot prove these loads unclobbered and would
-      // otherwise keep all 60 round-key words in VGPRs.
-      uint32_t rk[60];
-  #pragma unroll
-      for (int i = 0; i < 60; i++) rk[i] = __builtin_amdgcn_readfirstlane(ti->rk[i]);
-      const uint32_t k0 = __builtin_amdgcn_readfirstlane(ti->desc.iv[0]) ^ rk[0];
-      const uint32_t k1 = __builtin_amdgcn_readfirstlane(ti->desc.iv[1]) ^ rk[1];
-      const uint32_t k2 = __builtin_amdgcn_readfirstlane(ti->desc.iv[2]) ^ rk[2];
-
       CtrCache cc;
       const uint32_t c0 = 2u + (uint32_t)(base + (int64_t)tid);  // counter of this lane in row 0, mod 2^32
       ctr_cache_init(cc, k0, k1, k2, c0, rk, tt, L);
@@ -464,10 +472,29 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
                 lane);
     }
     __syncthreads();
-    if (fold && tid == 0) {
-      u128 p = red[0];
-      for (int w = 1; w < kLeaders; w++) p = u128_xor(p, red[w]);
-      st_u128(a.partials + g, p);
+    if (tid == 0) {
+      if (fold) {
+        u128 p = red[0];
+        for (int w = 1; w < kLeaders; w++) p = u128_xor(p, red[w]);
+        if (!one) {
+          st_u128(a.partials + g, p);
+        } else {
+          // S = P_0 xor H*L, tag = E_K(J0) xor S (the finalize pass skips this segment)
+          const u128 tag = u128_xor(p, red[kLeaders]);
+          if (!OPEN) {
+            uint32_t* to = (uint32_t*)(a.tags_out + 16ull * s);
+            for (int j = 0; j < 4; j++) to[j] = tag.w[j];
+          } else {
+            const uint32_t* tin = (const uint32_t*)(a.tags_in + 16ull * s);
+            uint32_t diff = 0;
+            for (int j = 0; j < 4; j++) diff |= tin[j] ^ tag.w[j];
+            a.verdicts[s] = diff ? kVerdictAuthFail : kVerdictOk;
+          }
+        }
+      } else if (one && !OPEN) {
+        uint32_t* to = (uint32_t*)(a.tags_out + 16ull * s);  // rejected: zero tag
+        for (int j = 0; j < 4; j++) to[j] = 0u;
+      }
     }
   }
 }
@@ -485,7 +512,7 @@ __global__ __launch_bounds__(kFinLanes) void k_finalize(GcmArgs a) {
   for (uint32_t i = lane; i < 256u; i += kFinLanes) te[i] = c_aes.te0[i];
   __syncthreads();
   const SegDesc sd = a.segs[s];
-  if (sd.flags & kSegSmall) return;
+  if (sd.flags & (kSegSmall | kSegOneTile)) return;
   const int32_t verdict = a.verdicts[s];
   if (verdict != kVerdictOk) {
     if (!OPEN && lane < 4) ((uint32_t*)(a.tags_out + 16ull * s))[lane] = 0u;
@@ -602,11 +629,33 @@ __global__ __launch_bounds__(64) void k_small(GcmArgs a) {
 __global__ __launch_bounds__(256) void k_prologue(uint4* __restrict__ dst, const uint4* __restrict__ src, size_t n16,
                                                   const SegDesc* __restrict__ segs, uint32_t n,
                                                   const uint32_t* __restrict__ labels,
-                                                  const uint32_t* __restrict__ bids, int32_t* __restrict__ verdicts) {
+                                                  const uint32_t* __restrict__ bids, int32_t* __restrict__ verdicts,
+                                                  KeyTableDev kt, uint4* __restrict__ fin) {
+  __shared__ uint32_t te[256];
   const size_t gsz = (size_t)gridDim.x * blockDim.x;
   for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += gsz) dst[i] = src[i];
   if (!verdicts) return;
+  if (fin) {
+    for (uint32_t i = threadIdx.x; i < 256u; i += blockDim.x) te[i] = c_aes.te0[i];
+    __syncthreads();
+  }
   for (uint32_t s = blockIdx.x; s < n; s += gridDim.x) {
+    if (fin && threadIdx.x < 64u && (segs[s].flags & kSegOneTile)) {
+      // GCM a one-tile segment needs besides its tile: E_K(J0) xor H*L,
+      // J0 = IV || BE32(1), H*L a wave sum over the set bits of the length
+      // block (only its low 64 bits can be set) of the products H*x^(64+k)
+      const uint32_t lane = threadIdx.x, user = segs[s].user;
+      u128 z = u128_zero();
+      if (((segs[s].len * 8ull) >> (63 - lane)) & 1ull) z = ld_u128(kt.pow_hxl + (size_t)user * kHxLanes + lane);
+#pragma unroll
+      for (int j = 0; j < 4; j++) z.w[j] = wave_xor(z.w[j]);
+      if (lane == 0) {
+        const uint32_t j0[4] = {segs[s].iv[0], segs[s].iv[1], segs[s].iv[2], 0x01000000u};
+        uint32_t e[4];
+        aes256_encrypt_tab(kt.rk + (size_t)user * 64u, j0, e, te);
+        fin[s] = make_uint4(e[0] ^ z.w[0], e[1] ^ z.w[1], e[2] ^ z.w[2], e[3] ^ z.w[3]);
+      }
+    }
     int bad = 0;
     if (labels) {
       const uint64_t rb = segs[s].row_begin, rc = segs[s].row_count;
@@ -854,7 +903,7 @@ hipError_t launch_gcm_small(const GcmArgs& a, bool open, hipStream_t s) {
 }
 
 hipError_t launch_gcm_finalize(const GcmArgs& a, bool open, hipStream_t s) {
-  if (a.n_tiles == 0) return hipSuccess;
+  if (a.n_multi == 0) return hipSuccess;
   if (open)
     hipLaunchKernelGGL(k_finalize<true>, dim3(a.n_segs), dim3(kFinLanes), 0, s, a);
   else
@@ -906,7 +955,8 @@ hipError_t launch_zero_chunks(const SegDesc* segs, uint32_t n_segs, const uint32
 
 
 hipError_t launch_prologue(void* dst, const void* src, size_t bytes, uint32_t n_segs, uint64_t bids_off,
-                           const uint32_t* labels, int32_t* verdicts, hipStream_t s) {
+                           const uint32_t* labels, int32_t* verdicts, const KeyTableDev* kt, uint4* fin,
+                           hipStream_t s) {
   if (bytes & 15u) return hipErrorInvalidValue;
   const size_t n16 = src ? bytes / 16 : 0;
   if (n16 == 0 && !verdicts) return hipSuccess;
@@ -918,7 +968,8 @@ hipError_t launch_prologue(void* dst, const void* src, size_t bytes, uint32_t n_
   if (grid == 0) grid = 1;
   hipLaunchKernelGGL(k_prologue, dim3((uint32_t)grid), dim3(256), 0, s, (uint4*)dst, (const uint4*)src, n16,
                      (const SegDesc*)rd, n_segs, labels,
-                     bids_off == kNoBids ? (const uint32_t*)nullptr : (const uint32_t*)(rd + bids_off), verdicts);
+                     bids_off == kNoBids ? (const uint32_t*)nullptr : (const uint32_t*)(rd + bids_off), verdicts,
+                     kt ? *kt : KeyTableDev{}, kt ? fin : nullptr);
   return hipGetLastError();
 }
 
