@@ -18,7 +18,11 @@
  *   current device; "host" pointers are ordinary host memory that the call
  *   reads before it returns (the caller may reuse it right away).  The
  *   caller owns every buffer it passes.  The library owns the key-table
- *   handle and stream-ordered scratch that it frees on the same stream.
+ *   handle, one pinned host staging ring per device (8 MiB) and device
+ *   scratch kept per (device, stream) for later calls (at most 16 buffers
+ *   per device, each as large as the largest call on its stream needed; held
+ *   until the process ends).  Calls on one stream reuse its buffer in stream
+ *   order; a buffer moves to another stream only after its last use.
  * - Errors: a call returns GIFT_OK or a negative gift_status.  Argument
  *   errors are detected on the host before anything is enqueued; when a call
  *   returns an error no GPU work was enqueued and no output was touched.

@@ -254,11 +254,12 @@ __device__ __forceinline__ u128 length_block(uint64_t len) {
 
 // Tile end of a leader wave (see k_gcm_tiles): Horner over the staged lane
 // partials of its waves in W (LDS tables), one multiply by the lane's power
-// hp, then the wave sum into the leader's reduction slot.  The LDS regions
-// arrive as byte offsets in the LDS address space, so every access is an LDS
-// instruction.
+// hp, then the wave sum into the leader's reduction slot.  Kept out of line,
+// so that the main loop's register allocation does not see it (inlined, the
+// kernel spills twice as many registers); the LDS regions arrive as byte
+// offsets in the LDS address space, so every access is an LDS instruction.
 typedef __attribute__((address_space(3))) uint8_t lds_byte;
-__device__ __forceinline__ void tile_fold(u128 v, uint32_t stage_off, uint32_t wt_off, u128 hp, uint32_t red_off,
+__device__ __noinline__ void tile_fold(u128 v, uint32_t stage_off, uint32_t wt_off, u128 hp, uint32_t red_off,
                                        uint32_t lane) {
   constexpr int kFold = kThreads / 64 / kLeaders;
   const u128* stage = (const u128*)(lds_byte*)(uintptr_t)stage_off;
