@@ -21,21 +21,38 @@ using namespace gift;
 
 namespace gift {
 
-// Longest tiles first, so that a work queue over them ends with short tiles:
-// a counting sort by the number of rows each tile runs (the kernel's tiles
+// Longest pieces first, so that a work queue over them ends with short work:
+// a counting sort by the number of rows each entry runs (the kernel's tiles
 // are aligned to the segment end, so only a segment's first tile is partial).
-void tile_order(const SegDesc* descs, uint32_t n_segs, uint32_t n_tiles, TileEnt* order) {
-  std::vector<uint32_t> count(kRows + 2, 0);
+// The tail also gets the pieces of up to `split` whole tiles of segments
+// longer than one tile, each cut into kRows / kPieceRows row ranges: the
+// workgroups run at slightly different speeds, and with whole tiles at the
+// end the fast ones would run out of work a tile's time before the slow ones.
+uint32_t tile_order(const SegDesc* descs, uint32_t n_segs, uint32_t n_tiles, uint32_t split, TileEnt* order) {
+  constexpr uint32_t kPieces = kRows / kPieceRows;
+  static_assert(kRows % kPieceRows == 0 && kPieceRows > 0, "pieces of a tile");
   auto rows_of = [](uint64_t m, uint32_t t) -> uint32_t {
     const int64_t base = (int64_t)m - (int64_t)(t + 1) * (int64_t)kTileBlocks;
     return base >= 0 ? (uint32_t)kRows : (uint32_t)kRows - (uint32_t)((uint64_t)(-base) / kThreads);
   };
+  auto pack = [](uint32_t t, uint32_t r0, uint32_t r1) { return t | (r0 << 16) | (r1 << 24); };
+  std::vector<uint32_t> count(kRows + 2, 0);
+  std::vector<uint8_t> cut(n_tiles, 0);
+  uint32_t n_cut = 0, g = 0;
   for (uint32_t i = 0; i < n_segs; i++) {
     if (descs[i].flags & kSegSmall) continue;
     const uint64_t m = descs[i].nblocks;
     const uint32_t nt = (uint32_t)((m + kTileBlocks - 1) / kTileBlocks);
-    count[kRows] += nt - 1;
-    count[rows_of(m, nt - 1)]++;
+    for (uint32_t t = 0; t < nt; t++, g++) {
+      const uint32_t r = rows_of(m, t);
+      if (nt > 1 && r == (uint32_t)kRows && n_cut < split) {
+        cut[g] = 1;
+        n_cut++;
+        count[kPieceRows] += kPieces;
+      } else {
+        count[r]++;
+      }
+    }
   }
   // start of each row count's run, longest first
   std::vector<uint32_t> pos(kRows + 2, 0);
@@ -44,14 +61,21 @@ void tile_order(const SegDesc* descs, uint32_t n_segs, uint32_t n_tiles, TileEnt
     pos[r] = acc;
     acc += count[r];
   }
-  (void)n_tiles;
-  uint32_t g = 0;
+  g = 0;
   for (uint32_t i = 0; i < n_segs; i++) {
     if (descs[i].flags & kSegSmall) continue;
     const uint64_t m = descs[i].nblocks;
     const uint32_t nt = (uint32_t)((m + kTileBlocks - 1) / kTileBlocks);
-    for (uint32_t t = 0; t < nt; t++, g++) order[pos[rows_of(m, t)]++] = TileEnt{g, i, t, descs[i].user};
+    for (uint32_t t = 0; t < nt; t++, g++) {
+      if (cut[g]) {
+        for (uint32_t q = 0; q < kPieces; q++)
+          order[pos[kPieceRows]++] = TileEnt{g, i, pack(t, q * kPieceRows, (q + 1) * kPieceRows), descs[i].user};
+      } else {
+        order[pos[rows_of(m, t)]++] = TileEnt{g, i, pack(t, 0, kRows), descs[i].user};
+      }
+    }
   }
+  return n_tiles + n_cut * (kPieces - 1);
 }
 
 // tile_base (n + 1 entries: first tile of each segment; small segments have
@@ -550,7 +574,9 @@ gift_status run_gcm(const gift_tensor* t, const gift_segment_table* st, gift_key
   const size_t o_desc = 0;
   const size_t o_zr = o_desc + align256(sizeof(SegDesc) * n);
   const size_t o_to = o_zr + align256(sizeof(ZeroRange) * P.zr.size());
-  const size_t o_tb = o_to + align256(sizeof(TileEnt) * P.n_tiles);
+  // the queue's tail splits about one whole tile per CU into pieces
+  const uint32_t split = P.n_multi ? (uint32_t)device_cus(dev) : 0u;
+  const size_t o_tb = o_to + align256(sizeof(TileEnt) * ((size_t)P.n_tiles + (uint64_t)(kRows / kPieceRows - 1) * split));
   const size_t o_sl = o_tb + align256(4ull * (n + 1));
   const size_t o_qh = o_sl + align256(4ull * (n ? n : 1));
   const size_t o_pt = o_qh + 256;  // end of the staged tables
@@ -565,7 +591,8 @@ gift_status run_gcm(const gift_tensor* t, const gift_segment_table* st, gift_key
   std::vector<uint8_t> host(o_pt);  // zero-filled: the queue head starts at 0
   if (n) memcpy(host.data() + o_desc, P.descs.data(), sizeof(SegDesc) * n);
   if (!P.zr.empty()) memcpy(host.data() + o_zr, P.zr.data(), sizeof(ZeroRange) * P.zr.size());
-  if (P.n_tiles) tile_order(P.descs.data(), n, P.n_tiles, (TileEnt*)(host.data() + o_to));
+  const uint32_t n_ents = P.n_tiles ? tile_order(P.descs.data(), n, P.n_tiles, split, (TileEnt*)(host.data() + o_to)) : 0u;
+  const bool pieces = n_ents > P.n_tiles;  // some tile is split: its partial is an XOR of pieces
   tile_tables(P.descs.data(), n, (uint32_t*)(host.data() + o_tb), (uint32_t*)(host.data() + o_sl));
   int32_t* verdicts = st->verdicts ? st->verdicts : (int32_t*)(scratch + o_vd);
   Staging* sg = staging_for(dev);
@@ -573,7 +600,7 @@ gift_status run_gcm(const gift_tensor* t, const gift_segment_table* st, gift_key
   // the prologue copies the tables and settles the verdicts (owner check)
   e = sg->upload(scratch, host.data(), o_pt, stream, [&](const void* src) {
     return launch_prologue(scratch, src, o_pt, n, kNoBids, st->row_labels, n ? verdicts : nullptr, &kt->dev,
-                           (uint4*)(scratch + o_fn), stream);
+                           (uint4*)(scratch + o_fn), (uint4*)(scratch + o_pt), pieces ? P.n_tiles : 0u, stream);
   });
   if (e != hipSuccess) return hip_fail(e, "staging upload");
 
@@ -592,6 +619,7 @@ gift_status run_gcm(const gift_tensor* t, const gift_segment_table* st, gift_key
       a.tile_base = (const uint32_t*)(scratch + o_tb);
       a.small_list = (const uint32_t*)(scratch + o_sl);
       a.n_tiles = P.n_tiles;
+      a.n_ents = n_ents;
       a.n_small = P.n_small;
       a.n_multi = P.n_multi;
       a.partials = (uint4*)(scratch + o_pt);
@@ -772,7 +800,9 @@ gift_status run_paged(const gift_paged_kv* kv, const gift_request* reqs, uint32_
   const size_t o_desc = 0;
   const size_t o_bid = o_desc + align256(sizeof(SegDesc) * n);
   const size_t o_to = o_bid + align256(4ull * total_bids);
-  const size_t o_tb = o_to + align256(sizeof(TileEnt) * n_tiles);
+  // the queue's tail splits about one whole tile per CU into pieces
+  const uint32_t split = n_multi ? (uint32_t)device_cus(dev) : 0u;
+  const size_t o_tb = o_to + align256(sizeof(TileEnt) * ((size_t)n_tiles + (uint64_t)(kRows / kPieceRows - 1) * split));
   const size_t o_sl = o_tb + align256(4ull * (n + 1));
   const size_t o_qh = o_sl + align256(4ull * n);
   const size_t o_pt = o_qh + 256;  // end of the staged tables
@@ -793,7 +823,8 @@ gift_status run_paged(const gift_paged_kv* kv, const gift_request* reqs, uint32_
       bp += reqs[i].n_block_ids;
     }
   }
-  if (n_tiles) tile_order(descs.data(), n, n_tiles, (TileEnt*)(host.data() + o_to));
+  const uint32_t n_ents = n_tiles ? tile_order(descs.data(), n, n_tiles, split, (TileEnt*)(host.data() + o_to)) : 0u;
+  const bool pieces = n_ents > n_tiles;  // some tile is split: its partial is an XOR of pieces
   tile_tables(descs.data(), n, (uint32_t*)(host.data() + o_tb), (uint32_t*)(host.data() + o_sl));
   int32_t* verdicts = verdicts_user ? verdicts_user : (int32_t*)(scratch + o_vd);
   Staging* sg = staging_for(dev);
@@ -801,7 +832,8 @@ gift_status run_paged(const gift_paged_kv* kv, const gift_request* reqs, uint32_
   e = sg ? sg->upload(scratch, host.data(), o_pt, stream,
                       [&](const void* src) {
                         return launch_prologue(scratch, src, o_pt, n, o_bid, labels, verdicts, &kt->dev,
-                                               (uint4*)(scratch + o_fn), stream);
+                                               (uint4*)(scratch + o_fn), (uint4*)(scratch + o_pt),
+                                               pieces ? n_tiles : 0u, stream);
                       })
          : hipErrorInvalidDevice;
   if (e != hipSuccess) return hip_fail(e, "staging upload");
@@ -827,6 +859,7 @@ gift_status run_paged(const gift_paged_kv* kv, const gift_request* reqs, uint32_
     a.tile_base = (const uint32_t*)(scratch + o_tb);
     a.small_list = (const uint32_t*)(scratch + o_sl);
     a.n_tiles = n_tiles;
+    a.n_ents = n_ents;
     a.n_multi = n_multi;
     a.n_small = 0;
     a.partials = (uint4*)(scratch + o_pt);
@@ -924,7 +957,8 @@ gift_status gift_key_table_create(const uint8_t* keys, uint32_t n_users, hipStre
   const size_t o_pt = o_ph + align256(u * kHPowers * 16);
   const size_t o_pl = o_pt + align256(u * kFinLanes * 16);
   const size_t o_px = o_pl + align256(u * 16);
-  const size_t bytes = o_px + align256(u * kHxLanes * 16);
+  const size_t o_pr = o_px + align256(u * kHxLanes * 16);
+  const size_t bytes = o_pr + align256(u * kRows * 16);
   uint8_t* mem = nullptr;
   hipError_t e = hipMalloc((void**)&mem, bytes);
   if (e != hipSuccess) return hip_fail(e, "hipMalloc(key table)");
@@ -948,6 +982,7 @@ gift_status gift_key_table_create(const uint8_t* keys, uint32_t n_users, hipStre
   kt->dev.pow_ht = (uint4*)(mem + o_pt);
   kt->dev.pow_hlt = (uint4*)(mem + o_pl);
   kt->dev.pow_hxl = (uint4*)(mem + o_px);
+  kt->dev.pow_hr = (uint4*)(mem + o_pr);
   kt->dev.n_users = n_users;
   // The copy reads the caller's buffer; synchronising before return means no
   // copy of the keys outlives the call on the host side of the library.
@@ -1015,7 +1050,7 @@ gift_status gift_check_owner(const gift_segment_table* st, const uint32_t* label
   e = sg ? sg->upload(d, P.descs.data(), bytes, stream,
                       [&](const void* src) {
                         return launch_prologue(d, src, bytes, n, kNoBids, labels, st->verdicts, nullptr, nullptr,
-                                               stream);
+                                               nullptr, 0u, stream);
                       })
          : hipErrorInvalidDevice;
   hipError_t e2 = lease.release();
@@ -1056,7 +1091,7 @@ static gift_status run_tokens(bool decrypt, const gift_segment_table* st, uint64
     e = sg ? sg->upload(d, P.descs.data(), bytes, stream,
                         [&](const void* src) {
                           return launch_prologue(d, src, bytes, n, kNoBids, nullptr, nullptr, nullptr, nullptr,
-                                                 stream);
+                                                 nullptr, 0u, stream);
                         })
            : hipErrorInvalidDevice;
   }

@@ -69,16 +69,22 @@ struct KeyTableDev {
   uint4* pow_ht;     // [n_users][kFinLanes] H^(k * kTileBlocks)
   uint4* pow_hlt;    // [n_users] H^(kFinLanes * kTileBlocks)
   uint4* pow_hxl;    // [n_users][kHxLanes] H * x^(64+k): the products H * L needs
+  uint4* pow_hr;     // [n_users][kRows] H^(k * kThreads): a tile piece ending k rows before its tile's end
   uint32_t n_users;
 };
 
-// One entry of the tile kernel's work queue: tile g (in tile_base numbering)
-// is tile t of segment s, counted from the segment's end; user is the
-// segment's user.
+// One entry of the tile kernel's work queue: rows [r0, r1) of tile g (in
+// tile_base numbering), which is tile t of segment s counted from the
+// segment's end; user is the segment's user.  trow packs t (bits 0-15), r0
+// (16-23) and r1 (24-31).  A whole tile has r0 = 0, r1 = kRows; the queue's
+// tail splits some tiles into pieces of rows, so that workgroups that run
+// faster take more of the last work.
 struct TileEnt {
-  uint32_t g, s, t, user;
+  uint32_t g, s, trow, user;
 };
 static_assert(sizeof(TileEnt) == 16, "TileEnt layout");
+static_assert(kRows <= 255, "rows fit a byte of TileEnt::trow");
+constexpr int kPieceRows = kRows / 4;  // rows of one piece of a split tile
 constexpr uint32_t kNoTile = 0xFFFFFFFFu;
 
 // Addressing of k_gcm_tiles: contiguous tensor, or a paged cache on the
@@ -98,6 +104,7 @@ struct GcmArgs {
   const uint32_t* tile_base;   // [n_segs + 1] first tile of each segment (small ones: 0 tiles)
   const uint32_t* small_list;  // [n_small] indices of small segments
   uint32_t n_tiles;
+  uint32_t n_ents;             // entries of the work queue (tiles, some split into pieces)
   uint32_t n_small;
   uint32_t n_multi;            // segments of more than one tile (the finalize pass)
   uint4* partials;             // [n_tiles] GHASH partial of each tile
@@ -118,15 +125,20 @@ hipError_t launch_key_setup(const uint8_t* keys_dev, KeyTableDev kt, hipStream_t
 // verdicts is not NULL, writes each segment's first verdict: the owner check
 // against labels (indexed by row, or by the block ids at byte bids_off of the
 // tables for paged calls) or OK without labels.  With a key table it also
-// writes fin[s] = E_K(J0) xor H*L of every one-tile segment s.  The
+// writes fin[s] = E_K(J0) xor H*L of every one-tile segment s and zeroes the
+// n_zero tile partials at zero (the tile kernel XORs pieces into them).  The
 // descriptors sit at byte 0 of the tables.
 constexpr uint64_t kNoBids = ~0ull;
 hipError_t launch_prologue(void* dst, const void* src, size_t bytes, uint32_t n_segs, uint64_t bids_off,
                            const uint32_t* labels, int32_t* verdicts, const KeyTableDev* kt, uint4* fin,
-                           hipStream_t s);
-// Tiles longest first: full tiles, then each segment's partial first tile by
-// its number of rows.  order has n_tiles entries.
-void tile_order(const SegDesc* descs, uint32_t n_segs, uint32_t n_tiles, TileEnt* order);
+                           uint4* zero, uint32_t n_zero, hipStream_t s);
+// The work queue, longest pieces first: whole tiles, then by number of rows
+// the segments' partial first tiles and the pieces of split tiles.  Up to
+// `split` whole tiles of segments longer than one tile are split into
+// kRows / kPieceRows pieces.  Returns the number of entries written to order
+// (n_tiles + kRows / kPieceRows - 1 per split tile; order must have room for
+// n_tiles + (kRows / kPieceRows - 1) * split).
+uint32_t tile_order(const SegDesc* descs, uint32_t n_segs, uint32_t n_tiles, uint32_t split, TileEnt* order);
 hipError_t launch_gcm_tiles(const GcmArgs& a, int mode, uint32_t grid, hipStream_t s);
 hipError_t launch_gcm_small(const GcmArgs& a, bool open, hipStream_t s);
 hipError_t launch_gcm_finalize(const GcmArgs& a, bool open, hipStream_t s);

@@ -38,7 +38,7 @@ constexpr uint32_t kLdsInfo = kLdsRed + 16 * (kLeaders + 1);  // TileInfo of the
 
 // The current tile's record in LDS, staged by the prefetch waves.
 struct TileInfo {
-  uint32_t g, s, t, user;  // queue entry
+  uint32_t g, s, trow, user;  // queue entry
   int32_t verdict;
   uint32_t next_k;  // queue entry claimed for the next tile
   uint32_t pad[2];
@@ -315,12 +315,12 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
   // 528 + i round-key word i (i < 64); 592 entry and verdict; 593 fin
   auto prefetch = [&](uint32_t k) {
     const uint32_t j = tid - kPf0;
-    const TileEnt e = k < a.n_tiles ? a.tile_order[k] : TileEnt{kNoTile, 0u, 0u, 0u};
+    const TileEnt e = k < a.n_ents ? a.tile_order[k] : TileEnt{kNoTile, 0u, 0u, 0u};
     pf_tabs = false;
     if (j == 592u) {
       ti->g = e.g;
       ti->s = e.s;
-      ti->t = e.t;
+      ti->trow = e.trow;
       ti->user = e.user;
     }
     if (e.g == kNoTile) return;
@@ -353,7 +353,9 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
     if (g == kNoTile) break;
     if (tid == kPf0) claim = gridDim.x + atomicAdd(a.tile_counter, 1u);
     const uint32_t s = __builtin_amdgcn_readfirstlane(ti->s);
-    const uint32_t t = __builtin_amdgcn_readfirstlane(ti->t);
+    const uint32_t trow = __builtin_amdgcn_readfirstlane(ti->trow);
+    const uint32_t t = trow & 0xFFFFu;                                      // tile of the segment
+    const int r0 = (int)((trow >> 16) & 0xFFu), r1 = (int)(trow >> 24);  // its rows in this entry
     const uint32_t user = __builtin_amdgcn_readfirstlane(ti->user);
     const int32_t verdict = (int32_t)__builtin_amdgcn_readfirstlane((uint32_t)ti->verdict);
     cur_user = user;
@@ -365,6 +367,7 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
     if (one && tid == 0) red[kLeaders] = u128{{ti->fin.x, ti->fin.y, ti->fin.z, ti->fin.w}};  // for the tile end
     const int64_t base = (int64_t)m - (int64_t)(t + 1) * (int64_t)kTileBlocks;  // block index of virtual slot 0
     const int r_start = base < 0 ? (int)((uint64_t)(-base) / kThreads) : 0;
+    const int r_lo = r_start > r0 ? r_start : r0;
 
     // paged side: block i of the segment lives in chunk i >> shift
     const uint64_t chunk0 = ti->desc.chunk0;
@@ -386,7 +389,7 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
     u128 y = u128_zero();
     if (verdict != kVerdictOk) {
       // rejected before this call's data is touched: release zeros only
-      for (int r = r_start; r < kRows; r++) {
+      for (int r = r_lo; r < r1; r++) {
         const int64_t i0 = base + (int64_t)r * kThreads + tid;
         if (i0 >= 0) {
           const uint64_t rem = len - 16ull * (uint64_t)i0;
@@ -402,9 +405,9 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
       // rows where every lane holds a whole block and the segment is 16-byte
       // aligned take the branch-free path
       const int r_full = base < 0 ? (int)(((uint64_t)(-base) + kThreads - 1) / kThreads) : 0;
-      const int r_end_full = (t == 0 && (len & 15u)) ? kRows - 1 : kRows;
+      const int r_end_full = (t == 0 && (len & 15u)) ? r1 - (r1 == kRows ? 1 : 0) : r1;
 
-      for (int r = r_start; r < kRows; r++) {
+      for (int r = r_lo; r < r1; r++) {
         // the whole-block rows load their input before the AES rounds, so the
         // HBM latency overlaps the keystream
         const bool fast = aligned && r >= r_full && r < r_end_full;
@@ -477,9 +480,17 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
       if (fold) {
         u128 p = red[0];
         for (int w = 1; w < kLeaders; w++) p = u128_xor(p, red[w]);
-        if (!one) {
-          st_u128(a.partials + g, p);
+        if (r0 == 0 && r1 == kRows) {
+          if (!one) st_u128(a.partials + g, p);
         } else {
+          // a piece of a split tile: its lane powers assumed rows up to the
+          // tile's end, so it still carries H^(kThreads * (kRows - r1));
+          // pieces meet in the tile's (zeroed) partial by XOR
+          if (r1 < kRows) p = gf_mul(p, ld_u128(a.kt.pow_hr + (size_t)user * kRows + (kRows - r1)));
+          uint32_t* dst = (uint32_t*)(a.partials + g);
+          for (int j = 0; j < 4; j++) atomicXor(dst + j, p.w[j]);
+        }
+        if (one) {
           // S = P_0 xor H*L, tag = E_K(J0) xor S (the finalize pass skips this segment)
           const u128 tag = u128_xor(p, red[kLeaders]);
           if (!OPEN) {
@@ -631,10 +642,13 @@ __global__ __launch_bounds__(256) void k_prologue(uint4* __restrict__ dst, const
                                                   const SegDesc* __restrict__ segs, uint32_t n,
                                                   const uint32_t* __restrict__ labels,
                                                   const uint32_t* __restrict__ bids, int32_t* __restrict__ verdicts,
-                                                  KeyTableDev kt, uint4* __restrict__ fin) {
+                                                  KeyTableDev kt, uint4* __restrict__ fin,
+                                                  uint4* __restrict__ zero, uint32_t n_zero) {
   __shared__ uint32_t te[256];
   const size_t gsz = (size_t)gridDim.x * blockDim.x;
   for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += gsz) dst[i] = src[i];
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n_zero; i += gsz)
+    zero[i] = make_uint4(0u, 0u, 0u, 0u);
   if (!verdicts) return;
   if (fin) {
     for (uint32_t i = threadIdx.x; i < 256u; i += blockDim.x) te[i] = c_aes.te0[i];
@@ -818,7 +832,7 @@ __global__ __launch_bounds__(64) void k_key_sched(const uint8_t* __restrict__ ke
   for (int i = 0; i < 4; i++) kt.h[4ull * u + i] = h[i];
 }
 
-constexpr uint32_t kPowersPerUser = kHPowers + kFinLanes + 1 + kHxLanes;
+constexpr uint32_t kPowersPerUser = kHPowers + kFinLanes + 1 + kHxLanes + kRows;
 
 __global__ __launch_bounds__(256) void k_key_powers(KeyTableDev kt) {
   const uint64_t idx = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -833,9 +847,12 @@ __global__ __launch_bounds__(256) void k_key_powers(KeyTableDev kt) {
     st_u128(kt.pow_ht + u * kFinLanes + l, gf_pow(h, (uint64_t)l * kTileBlocks));
   } else if (j == (uint32_t)(kHPowers + kFinLanes)) {
     st_u128(kt.pow_hlt + u, gf_pow(h, (uint64_t)kFinLanes * kTileBlocks));
-  } else {
+  } else if (j < (uint32_t)(kHPowers + kFinLanes + 1 + kHxLanes)) {
     const uint32_t k = j - (kHPowers + kFinLanes + 1);
     st_u128(kt.pow_hxl + u * kHxLanes + k, gf_mul(h, gf_xpow_elem(64 + (int)k)));
+  } else {
+    const uint32_t k = j - (kHPowers + kFinLanes + 1 + kHxLanes);
+    st_u128(kt.pow_hr + u * kRows + k, gf_pow(h, (uint64_t)k * kThreads));
   }
 }
 
@@ -880,8 +897,8 @@ hipError_t launch_key_setup(const uint8_t* keys_dev, KeyTableDev kt, hipStream_t
 
 
 hipError_t launch_gcm_tiles(const GcmArgs& a, int mode, uint32_t grid, hipStream_t s) {
-  if (a.n_tiles == 0) return hipSuccess;
-  const uint32_t g = a.n_tiles < grid ? a.n_tiles : grid;
+  if (a.n_ents == 0) return hipSuccess;
+  const uint32_t g = a.n_ents < grid ? a.n_ents : grid;
   switch (mode) {
     case 0: hipLaunchKernelGGL(k_gcm_tiles<0>, dim3(g), dim3(kThreads), 0, s, a); break;
     case kModeOpen: hipLaunchKernelGGL(k_gcm_tiles<kModeOpen>, dim3(g), dim3(kThreads), 0, s, a); break;
@@ -957,20 +974,20 @@ hipError_t launch_zero_chunks(const SegDesc* segs, uint32_t n_segs, const uint32
 
 hipError_t launch_prologue(void* dst, const void* src, size_t bytes, uint32_t n_segs, uint64_t bids_off,
                            const uint32_t* labels, int32_t* verdicts, const KeyTableDev* kt, uint4* fin,
-                           hipStream_t s) {
+                           uint4* zero, uint32_t n_zero, hipStream_t s) {
   if (bytes & 15u) return hipErrorInvalidValue;
   const size_t n16 = src ? bytes / 16 : 0;
-  if (n16 == 0 && !verdicts) return hipSuccess;
+  if (n16 == 0 && !verdicts && n_zero == 0) return hipSuccess;
   if (n16 && (((uintptr_t)dst | (uintptr_t)src) & 15u)) return hipErrorInvalidValue;
   const uint8_t* rd = src ? (const uint8_t*)src : (const uint8_t*)dst;  // where the tables are readable now
-  uint64_t grid = cdiv(n16, 256u);
+  uint64_t grid = cdiv(n16 > n_zero ? n16 : n_zero, 256u);
   if (verdicts && n_segs > grid) grid = n_segs;
   if (grid > 1024u) grid = 1024u;
   if (grid == 0) grid = 1;
   hipLaunchKernelGGL(k_prologue, dim3((uint32_t)grid), dim3(256), 0, s, (uint4*)dst, (const uint4*)src, n16,
                      (const SegDesc*)rd, n_segs, labels,
                      bids_off == kNoBids ? (const uint32_t*)nullptr : (const uint32_t*)(rd + bids_off), verdicts,
-                     kt ? *kt : KeyTableDev{}, kt ? fin : nullptr);
+                     kt ? *kt : KeyTableDev{}, kt ? fin : nullptr, zero, n_zero);
   return hipGetLastError();
 }
 
