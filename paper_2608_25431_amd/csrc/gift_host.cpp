@@ -8,6 +8,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <deque>
 #include <mutex>
 #include <string>
 #include <utility>
@@ -173,24 +174,19 @@ class Staging {
     }
     size_t need = (bytes + 255) & ~(size_t)255;
     if (head_ + need > kCap) head_ = 0;
-    // retire completed slots; wait for any slot overlapping [head_, head_+need)
-    for (size_t i = 0; i < live_.size();) {
-      Slot& sl = live_[i];
-      bool overlap = sl.off < head_ + need && head_ < sl.off + sl.len;
-      bool done = hipEventQuery(sl.ev) == hipSuccess;
-      if (overlap && !done) {
+    // retire finished slots oldest first, stopping at the first still in
+    // flight (one query per call in the usual single-stream case); a slot in
+    // flight that overlaps [head_, head_ + need) must finish first
+    while (!live_.empty() && (live_.front().done || hipEventQuery(live_.front().ev) == hipSuccess)) {
+      free_ev_.push_back(live_.front().ev);
+      live_.pop_front();
+    }
+    for (Slot& sl : live_)
+      if (!sl.done && sl.off < head_ + need && head_ < sl.off + sl.len) {
         hipError_t e = hipEventSynchronize(sl.ev);
         if (e != hipSuccess) return e;
-        done = true;
+        sl.done = true;
       }
-      if (done) {
-        free_ev_.push_back(sl.ev);
-        live_[i] = live_.back();
-        live_.pop_back();
-      } else {
-        i++;
-      }
-    }
     memcpy(base_ + head_, src, bytes);
     hipError_t e;
     if (dbase_ && !(bytes & 15u)) {
@@ -220,7 +216,7 @@ class Staging {
       free_ev_.push_back(ev);
       return e;
     }
-    live_.push_back(Slot{head_, need, ev});
+    live_.push_back(Slot{head_, need, ev, false});
     head_ += need;
     return hipSuccess;
   }
@@ -230,12 +226,13 @@ class Staging {
   struct Slot {
     size_t off, len;
     hipEvent_t ev;
+    bool done;  // its event has completed
   };
   std::mutex mu_;
   uint8_t* base_ = nullptr;
   uint8_t* dbase_ = nullptr;  // base_ as the device addresses it (mapped pinned memory)
   size_t head_ = 0;
-  std::vector<Slot> live_;
+  std::deque<Slot> live_;  // in allocation order
   std::vector<hipEvent_t> free_ev_;
 };
 

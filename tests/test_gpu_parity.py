@@ -444,6 +444,39 @@ def test_llama3_8b_kv_full_size():
     kt.destroy()
 
 
+def test_llama3_8b_kv_every_segment_verifies_in_openssl():
+    # Every ciphertext byte and every tag at full size, checked by an
+    # independent GCM implementation (OpenSSL, which also pins the oracle):
+    # it must accept each segment's tag and decrypt to the plaintext.  The
+    # work queue here splits 256 of the 4,321 tiles into pieces, inside
+    # segments whose other tiles stay whole.
+    import openssl_ref
+    if not openssl_ref.available():
+        pytest.skip("libcrypto not found")
+    from concurrent.futures import ThreadPoolExecutor
+    w = W.llama3_8b_kv()
+    t = w.tensors[0]
+    kt = gift.KeyTable(w.keys)
+    d = t.generate(DEV)
+    ct, tags, ver = seal(d, t.n_rows, t.row_bytes, t.segs, kt, w.nonce_base)
+    assert (host(ver) == 0).all()
+    ct_h, pt_h, tg = host(ct), host(d), host(tags).reshape(-1, 16)
+    del ct, d
+    kt.destroy()
+
+    def verifies(i):
+        s = t.segs[i]
+        off, ln = t.seg_bytes(i)
+        u = int(s["user"])
+        iv = oracle.segment_iv(w.nonce_base[u].tobytes(), int(s["iv_seq"]))
+        p = openssl_ref.gcm_decrypt(w.keys[u].tobytes(), iv, ct_h[off:off + ln], tg[i].tobytes())
+        return p is not None and p == pt_h[off:off + ln].tobytes()
+
+    with ThreadPoolExecutor(8) as ex:
+        ok = list(ex.map(verifies, range(len(t.segs))))
+    assert all(ok), [i for i, o in enumerate(ok) if not o]
+
+
 def test_tamper_config_full_size():
     w = W.tamper()
     t = w.tensors[0]
