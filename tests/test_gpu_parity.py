@@ -261,6 +261,54 @@ def test_random_tables_status_and_output_match_oracle(kt3):
     assert n_ok > 50
 
 
+def test_random_multi_tile_tables_with_labels_and_tamper(kt3):
+    # Segments of one to three 2 MiB tiles next to gaps and shorter ones:
+    # every whole tile of a longer segment is cut into pieces at the tail of
+    # the work queue (there are fewer than one per CU), one-tile segments get
+    # their tags in the tile kernel.  Fused owner check with one relabelled
+    # row, then open after one ciphertext bit and one tag bit are flipped:
+    # every byte, tag and verdict equals the oracle's.
+    keys, nb, kt = kt3
+    r = np.random.default_rng(2024)
+    for case in range(5):
+        rb = int(r.choice([65536, 65536 + 48, 40000]))
+        seg_rows = [int(x) for x in r.choice([1, 5, 32, 33, 47, 64, 65, 90], size=int(r.integers(3, 6)))]
+        table, row, seq = [], 0, 1000 * case
+        for k, n in enumerate(seg_rows):
+            row += int(r.integers(0, 3))  # gap rows
+            table.append((row, n, int(r.integers(0, 3)), seq + k))
+            row += n
+        n_rows = row + int(r.integers(0, 2))
+        data = r.integers(0, 256, n_rows * rb, dtype=np.uint8)
+        labels = np.full(n_rows, 0xFFFFFFFF, np.uint32)
+        for (b, n, u, _) in table:
+            labels[b:b + n] = u
+        mixed = int(r.integers(0, len(table)))
+        b, n, u, _ = table[mixed]
+        labels[b + int(r.integers(0, n))] = (u + 1) % 3
+        st, o_out, o_tags, o_ver = oracle.seal(data, n_rows, rb, table, keys, nb, labels=labels)
+        assert st == 0
+        d, lab = dev_u8(data), dev_u32(labels)
+        out, tags, ver = seal(d, n_rows, rb, table, kt, nb, labels_dev=lab)
+        n = len(table)
+        assert host(ver)[:n].tolist() == o_ver.tolist(), (case, table)
+        assert host(out).tobytes() == o_out.tobytes(), (case, table)
+        assert host(tags)[:16 * n].tobytes() == o_tags.tobytes(), (case, table)
+        # open without labels after flipping one ciphertext bit and one tag bit
+        ok = [i for i in range(n) if i != mixed]
+        ct_np, tg_np = o_out.copy().reshape(-1), o_tags.copy().reshape(-1)
+        i_ct = ok[int(r.integers(0, len(ok)))]
+        b, nr, _, _ = table[i_ct]
+        ct_np[b * rb + int(r.integers(0, nr * rb))] ^= np.uint8(1 << int(r.integers(0, 8)))
+        i_tg = ok[int(r.integers(0, len(ok)))]
+        tg_np[16 * i_tg + int(r.integers(0, 16))] ^= np.uint8(1 << int(r.integers(0, 8)))
+        st, o_back, o_ver2 = oracle.open_(ct_np, n_rows, rb, table, keys, nb, tg_np)
+        assert st == 0
+        back, ver2 = open_(dev_u8(ct_np), n_rows, rb, table, kt, nb, dev_u8(tg_np))
+        assert host(ver2)[:n].tolist() == o_ver2.tolist(), (case, table)
+        assert host(back).tobytes() == o_back.tobytes(), (case, table)
+
+
 def test_wrong_key_table_fails_every_segment(kt3):
     keys, nb, kt = kt3
     keys2, _ = keyset(3)
