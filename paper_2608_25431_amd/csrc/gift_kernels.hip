@@ -407,10 +407,23 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
       const int r_full = base < 0 ? (int)(((uint64_t)(-base) + kThreads - 1) / kThreads) : 0;
       const int r_end_full = (t == 0 && (len & 15u)) ? r1 - (r1 == kRows ? 1 : 0) : r1;
 
+      auto whole = [&](int r) { return aligned && r >= r_full && r < r_end_full; };
+      // paged: a lane's chunk offset for the next whole-block row is loaded
+      // one row ahead, so the gather or scatter address is ready when the row
+      // starts
+      constexpr bool PAGED = GATHER || SCATTER;
+      auto chunk_of = [&](int r) -> uint64_t {
+        const uint64_t i0 = (uint64_t)(base + (int64_t)r * kThreads + tid);
+        return a.chunk_off[chunk0 + (i0 >> a.chunk_shift)];
+      };
+      uint64_t c_next = (PAGED && whole(r_lo)) ? chunk_of(r_lo) : 0;
+
       for (int r = r_lo; r < r1; r++) {
         // the whole-block rows load their input before the AES rounds, so the
         // HBM latency overlaps the keystream
-        const bool fast = aligned && r >= r_full && r < r_end_full;
+        const bool fast = whole(r);
+        const uint64_t c_cur = c_next;
+        if (PAGED && whole(r + 1)) c_next = chunk_of(r + 1);
         const uint8_t* src = nullptr;
         uint8_t* dst = nullptr;
         uint4 v = make_uint4(0, 0, 0, 0);
@@ -418,8 +431,9 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
           // every lane's block index is >= 0 in these rows; pointer arithmetic
           // (not integers) keeps the global address space for the compiler
           const uint64_t i0 = (uint64_t)(base + (int64_t)r * kThreads + tid);
-          src = GATHER ? paged(i0) : a.in + off + 16ull * i0;
-          dst = SCATTER ? paged(i0) : a.out + off + 16ull * i0;
+          uint8_t* pg = a.pbase + c_cur + ((i0 & cmask) << 4);
+          src = GATHER ? pg : a.in + off + 16ull * i0;
+          dst = SCATTER ? pg : a.out + off + 16ull * i0;
           v = *(const uint4*)src;
         }
         uint32_t x0, x1, x2, x3;
