@@ -286,13 +286,16 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
   u128* red = (u128*)(smem + kLdsRed);
 
   // Replicated T-tables: word w = region*16384 + x*64 + slot holds
-  // T_{2*region + slot/32}[x] = rotl(Te0[x], 8*table).
-  for (uint32_t w = tid; w < 32768u; w += kThreads) {
-    uint32_t region = w >> 14, x = (w >> 6) & 255u, slot = w & 63u;
-    uint32_t tab = 2u * region + (slot >> 5);
-    uint32_t v = c_aes.te0[x];
-    uint32_t sh = 8u * tab;
-    ((uint32_t*)tt)[w] = (v << sh) | (v >> ((32u - sh) & 31u));
+  // T_{2*region + slot/32}[x] = rotl(Te0[x], 8*table).  Four consecutive
+  // slots hold the same word, so each thread writes 16 bytes at a time.
+  for (uint32_t q = tid; q < 8192u; q += kThreads) {
+    const uint32_t w = 4u * q;
+    const uint32_t region = w >> 14, x = (w >> 6) & 255u, slot = w & 63u;
+    const uint32_t tab = 2u * region + (slot >> 5);
+    const uint32_t v = c_aes.te0[x];
+    const uint32_t sh = 8u * tab;
+    const uint32_t r = (v << sh) | (v >> ((32u - sh) & 31u));
+    ((uint4*)tt)[q] = make_uint4(r, r, r, r);
   }
   const uint32_t L = ((tid & 31u) << 2) | 0x10000u;  // this lane's table copy
   uint32_t cur_user = 0xFFFFFFFFu;  // user whose GHASH tables are in LDS
