@@ -15,7 +15,14 @@
 // own blocks (d_t: distance from the tile's end), and lane l of a full tile
 // ends at distance (1023 - l) from the tile's end.  At tile end one leader
 // wave per SIMD folds the lane partials of four waves with LDS tables of
-// H^256 and applies the remaining per-lane power with one generic multiply.
+// H^256 and applies the remaining per-lane power with one generic multiply,
+// while the other waves prefetch the next tile.  The tail of the work queue
+// cuts some tiles into row pieces, whose partials meet by XOR.
+//
+// Around it: k_prologue (first kernel of a call: staged tables from pinned
+// host memory, owner check, E_K(J0) xor H*L of one-tile segments),
+// k_finalize (tags of longer segments), k_small (segments up to 1 KiB),
+// zero-fill, the paged-call helpers, per-token encryption and key setup.
 #include <hip/hip_runtime.h>
 
 #include "gift_device.hpp"
@@ -379,9 +386,9 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
       return a.pbase + a.chunk_off[chunk0 + (i >> a.chunk_shift)] + ((i & cmask) << 4);
     };
 
-    // Tile-uniform values live in SGPRs: the kernel also stores to global
-    // memory, so the compiler cannot prove these loads unclobbered and would
-    // otherwise keep all 60 round-key words in VGPRs.
+    // Tile-uniform values are read from the tile record into SGPRs
+    // (readfirstlane), so the per-block loop keeps no copy of the 60
+    // round-key words in VGPRs.
     uint32_t rk[60];
 #pragma unroll
     for (int i = 0; i < 60; i++) rk[i] = __builtin_amdgcn_readfirstlane(ti->rk[i]);
@@ -465,7 +472,6 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
         __builtin_amdgcn_s_setprio(1);
         y = ghash_step_lds(y, x, gt);
       }
-
     }  // verdict OK
 
     // Tile partial: lane tid contributes y * H^(kThreads + 1 - tid), its
