@@ -22,7 +22,10 @@
  *   scratch kept per (device, stream) for later calls (at most 16 buffers
  *   per device, each as large as the largest call on its stream needed; held
  *   until the process ends).  Calls on one stream reuse its buffer in stream
- *   order; a buffer moves to another stream only after its last use.
+ *   order; a buffer moves to another stream only after its last use.  A
+ *   call that reuses a buffer also makes its stream wait for the buffer's
+ *   last use, since one handle can name different streams (a handle reused
+ *   after hipStreamDestroy, hipStreamPerThread in each thread).
  * - Errors: a call returns GIFT_OK or a negative gift_status.  Argument
  *   errors are detected on the host before anything is enqueued; when a call
  *   returns an error no GPU work was enqueued and no output was touched.

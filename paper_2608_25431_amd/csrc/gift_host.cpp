@@ -248,6 +248,12 @@ inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 // Work on one stream runs in order, so the buffer of an earlier call on the
 // same stream can serve the next call at once: its first use there (the
 // descriptor upload) runs behind everything the earlier call enqueued.  A
+// handle does not always name one stream, though: the next stream created
+// after hipStreamDestroy can get the destroyed one's handle while its work is
+// still in flight, and hipStreamPerThread names a different stream in each
+// thread.  So a call that takes over a buffer also makes its stream wait for
+// the event recorded behind the buffer's last use (a no-op wait when that use
+// was on the same stream).  A
 // lease holds the entry's lock until its call has enqueued all its work, so
 // two host threads on one stream cannot interleave their uses of the buffer.
 // The event recorded when a lease ends guards the rare cases where a buffer
@@ -328,6 +334,13 @@ class ScratchLease {
         if (mine->bound && mine->stream == s) {  // still ours after the wait
           e_ = mine;
           lk_ = std::move(l);
+          // the handle may name another stream than the buffer's last use did
+          hipError_t w = hipSuccess;
+          if (e_->unsure)
+            w = settle(*e_);
+          else if (e_->recorded)
+            w = hipStreamWaitEvent(s, e_->done, 0);
+          if (w != hipSuccess) return w;
         }
       } else if (!e_) {
         break;  // every entry is busy on another stream

@@ -3,6 +3,7 @@ declares (no GPU: only calls that touch no device)."""
 import os
 import re
 import subprocess
+import sys
 
 import pytest
 
@@ -63,3 +64,12 @@ def test_null_key_table_is_rejected_on_the_host(lib):
     assert lib.gift_key_table_create(None, 1, None, ctypes.byref(ctypes.c_void_p())) == gift.E_INVALID
     assert lib.gift_key_table_destroy(None) == gift.OK
     assert lib.gift_key_table_users(None) == 0
+
+
+def test_loads_beside_torchs_hip_runtime(lib):
+    # torch ships its own libamdhip64, which a process that imports torch first
+    # has loaded: the library may only use entry points that runtime exports
+    code = ("import sys, ctypes, torch; sys.path.insert(0, %r); "
+            "from paper_2608_25431_amd import gift; ctypes.CDLL(gift.LIB_PATH)" % ROOT)
+    r = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, timeout=300)
+    assert r.returncode == 0, r.stderr[-2000:]

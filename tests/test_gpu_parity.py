@@ -492,6 +492,80 @@ def test_llama3_8b_kv_full_size():
     kt.destroy()
 
 
+def test_scratch_reuse_when_one_handle_names_several_streams(kt3):
+    # a stream destroyed while the library's work on it is in flight hands its
+    # handle to the next stream created, and hipStreamPerThread is one handle
+    # for a different stream in each thread: each must get scratch of its own
+    import ctypes
+    import threading
+    hip = ctypes.CDLL("libamdhip64.so")
+    keys, nb, kt = kt3
+
+    def case(n_segs, rows_per_seg, rb, user0, seq0):
+        n_rows = n_segs * rows_per_seg
+        data_np = rng.integers(0, 256, n_rows * rb, dtype=np.uint8)
+        table = [(k * rows_per_seg, rows_per_seg, (user0 + k) % 3, seq0 + k) for k in range(n_segs)]
+        return data_np, n_rows, rb, table
+
+    def buffers(c):
+        data_np, n_rows, rb, table = c
+        n = len(table)
+        return (dev_u8(data_np), torch.empty(n_rows * rb, dtype=torch.uint8, device=DEV),
+                torch.zeros(n * 16, dtype=torch.uint8, device=DEV))
+
+    def check(c, out, tags):
+        # segments tile the rows in order, so the output is their concatenation
+        data_np, n_rows, rb, table = c
+        segs = gift.as_segments(table)
+        per = int(segs[0]["row_count"]) * rb
+        ref = oracle_segments(keys, nb, segs, rb, lambda i: data_np[i * per:(i + 1) * per].tobytes())
+        assert host(out).tobytes() == b"".join(ct for ct, _ in ref)
+        assert host(tags).tobytes() == b"".join(tag for _, tag in ref)
+
+    big = case(32, 128, 65536, 0, 50000)     # 256 MiB, still running when the next call is enqueued
+    small = case(40, 2, 64, 1, 60000)
+    bufs_big, bufs_small = buffers(big), buffers(small)
+    torch.cuda.synchronize()
+    sa, sb = ctypes.c_void_p(), ctypes.c_void_p()
+    assert hip.hipStreamCreate(ctypes.byref(sa)) == 0
+    gift.seal(bufs_big[0], big[1], big[2], big[3], kt, nb, bufs_big[1], bufs_big[2], stream=sa.value)
+    assert hip.hipStreamDestroy(sa) == 0
+    assert hip.hipStreamCreate(ctypes.byref(sb)) == 0
+    gift.seal(bufs_small[0], small[1], small[2], small[3], kt, nb, bufs_small[1], bufs_small[2], stream=sb.value)
+    assert hip.hipStreamSynchronize(sb) == 0
+    torch.cuda.synchronize()
+    assert hip.hipStreamDestroy(sb) == 0
+    check(big, bufs_big[1], bufs_big[2])
+    check(small, bufs_small[1], bufs_small[2])
+
+    per_thread = 2  # hipStreamPerThread
+    cases = [[case(n, r, rb, t, 70000 + 1000 * t + 100 * i)
+              for i, (n, r, rb) in enumerate([(8, 64, 8192), (40, 2, 64), (3, 20, 4096), (700, 2, 64)])]
+             for t in range(2)]
+    bufs = [[buffers(c) for c in cs] for cs in cases]
+    torch.cuda.synchronize()
+    errors = []
+
+    def work(t):
+        try:
+            for c, (d, out, tags) in zip(cases[t], bufs[t]):
+                gift.seal(d, c[1], c[2], c[3], kt, nb, out, tags, stream=per_thread)
+            assert hip.hipStreamSynchronize(ctypes.c_void_p(per_thread)) == 0
+        except Exception as e:  # surfaced in the main thread
+            errors.append(e)
+
+    threads = [threading.Thread(target=work, args=(t,)) for t in range(2)]
+    for th in threads:
+        th.start()
+    for th in threads:
+        th.join()
+    assert not errors, errors
+    torch.cuda.synchronize()
+    for t in range(2):
+        for c, (d, out, tags) in zip(cases[t], bufs[t]):
+            check(c, out, tags)
+
+
 def test_llama3_8b_kv_every_segment_verifies_in_openssl():
     # Every ciphertext byte and every tag at full size, checked by an
     # independent GCM implementation (OpenSSL, which also pins the oracle):
