@@ -465,6 +465,17 @@ def main():
                      "traffic": profiled_traffic(w.name) if labels is not None else None,
                      "kernel_ms": round(k_ms, 4), "alg_bytes_per_launch": alg_bytes},
     }
+    # The same kernel against the limit that binds it: its LDS reads per
+    # 16-byte block (197 T-table words, 32 GHASH table entries of 16 B) at the
+    # rates standalone LDS probes reach on this chip: 29.1 random 4-byte
+    # lane-reads and 245 B of 16-byte reads per CU per clock.
+    lds_cycles = 197 / 29.1 + 32 * 16 / 245
+    lds_peak = 16 * 256 * 2.4e9 / lds_cycles / 1e9  # sealed GB/s, 256 CUs at the 2.4 GHz peak clock
+    kernel_sealed = tiled / (k_ms * 1e-3) / 1e9
+    res["lds_roofline"] = {"bound": "lds", "kernel": "k_gcm_tiles<seal>", "achieved": round(kernel_sealed, 2),
+                           "peak": round(lds_peak, 1), "unit": "GB/s sealed", "frac": round(kernel_sealed / lds_peak, 4),
+                           "lds_cycles_per_block": round(lds_cycles, 3),
+                           "note": "peak at the 2.4 GHz peak clock; the chip runs about 2.1-2.2 GHz under this load"}
     if w.name == "llama3_8b_kv" and not w.in_place:
         res["paged_seal"] = time_paged(gift, t, w, kt, data, out, max(5, args.steps // 4), args.warmup, torch)
         log(f"[bench] paged seal: {res['paged_seal']}")
