@@ -307,10 +307,19 @@ __device__ inline u128 gf_pow(const u128& h, uint64_t e) {
   return r;
 }
 
+// XOR over the 64 lanes of a wave, returned wave-uniform.  Within each row of
+// 16 lanes, DPP combines lanes 1 apart and 2 apart (quad permutations), then
+// mirrored half rows and mirrored rows, after which every lane holds its
+// row's XOR; the four rows are read out with readlane.  No LDS round trips (a
+// shuffle butterfly takes six dependent ones).  Every lane of the wave must
+// be active.
 __device__ __forceinline__ uint32_t wave_xor(uint32_t v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v ^= __shfl_xor(v, o, 64);
-  return v;
+  v ^= (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0xB1, 0xF, 0xF, true);   // quad_perm [1,0,3,2]
+  v ^= (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x4E, 0xF, 0xF, true);   // quad_perm [2,3,0,1]
+  v ^= (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x141, 0xF, 0xF, true);  // row_half_mirror
+  v ^= (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x140, 0xF, 0xF, true);  // row_mirror
+  return (uint32_t)__builtin_amdgcn_readlane((int)v, 0) ^ (uint32_t)__builtin_amdgcn_readlane((int)v, 16) ^
+         (uint32_t)__builtin_amdgcn_readlane((int)v, 32) ^ (uint32_t)__builtin_amdgcn_readlane((int)v, 48);
 }
 
 }  // namespace gift

@@ -22,61 +22,81 @@ using namespace gift;
 
 namespace gift {
 
-// Longest pieces first, so that a work queue over them ends with short work:
-// a counting sort by the number of rows each entry runs (the kernel's tiles
-// are aligned to the segment end, so only a segment's first tile is partial).
-// The tail also gets the pieces of up to `split` whole tiles of segments
-// longer than one tile, each cut into kRows / kPieceRows row ranges: the
-// workgroups run at slightly different speeds, and with whole tiles at the
-// end the fast ones would run out of work a tile's time before the slow ones.
-uint32_t tile_order(const SegDesc* descs, uint32_t n_segs, uint32_t n_tiles, uint32_t split, TileEnt* order) {
-  constexpr uint32_t kPieces = kRows / kPieceRows;
-  static_assert(kRows % kPieceRows == 0 && kPieceRows > 0, "pieces of a tile");
-  auto rows_of = [](uint64_t m, uint32_t t) -> uint32_t {
-    const int64_t base = (int64_t)m - (int64_t)(t + 1) * (int64_t)kTileBlocks;
-    return base >= 0 ? (uint32_t)kRows : (uint32_t)kRows - (uint32_t)((uint64_t)(-base) / kThreads);
-  };
+namespace {
+
+// Tile rows of tile t of a segment of m blocks.  Tiles are aligned to the
+// segment's end, so only a segment's first tile can be partial; its rows
+// below kRows - tile_rows hold no blocks.
+uint32_t tile_rows(uint64_t m, uint32_t t) {
+  const int64_t base = (int64_t)m - (int64_t)(t + 1) * (int64_t)kTileBlocks;
+  return base >= 0 ? (uint32_t)kRows : (uint32_t)kRows - (uint32_t)((uint64_t)(-base) / kThreads);
+}
+
+uint32_t tiles_of(const SegDesc& d) { return (uint32_t)(((uint64_t)d.nblocks + kTileBlocks - 1) / kTileBlocks); }
+
+}  // namespace
+
+uint32_t fine_cut(SegDesc* descs, uint32_t n_segs, uint32_t n_tiles, uint32_t cus, uint32_t* n_multi) {
+  if (n_tiles == 0 || cus == 0 || n_tiles >= cus) return 0;
+  uint64_t rows = 0;
+  for (uint32_t i = 0; i < n_segs; i++) {
+    if (descs[i].flags & kSegSmall) continue;
+    const uint32_t nt = tiles_of(descs[i]);
+    for (uint32_t t = 0; t < nt; t++) rows += tile_rows(descs[i].nblocks, t);
+  }
+  const uint32_t fine = (uint32_t)((rows + cus - 1) / cus);
+  if (fine >= (uint32_t)kRows) return 0;  // (not reached while n_tiles < cus)
+  for (uint32_t i = 0; i < n_segs; i++)
+    if ((descs[i].flags & kSegOneTile) && tile_rows(descs[i].nblocks, 0) > fine) {
+      descs[i].flags &= ~kSegOneTile;
+      (*n_multi)++;
+    }
+  return fine;
+}
+
+// Longest entries first, so that a work queue over them ends with short
+// work: a counting sort by the number of rows each entry runs.  Without a
+// fine cut, the tail also gets the pieces of up to `split` whole tiles of
+// segments longer than one tile: the workgroups run at slightly different
+// speeds, and with whole tiles at the end the fast ones would run out of work
+// a tile's time before the slow ones.
+uint32_t tile_order(const SegDesc* descs, uint32_t n_segs, uint32_t split, uint32_t fine, TileEnt* order) {
+  static_assert(kRows % kPieceRows == 0 && kPieceRows > 0 && kRows < 256, "pieces of a tile");
   auto pack = [](uint32_t t, uint32_t r0, uint32_t r1) { return t | (r0 << 16) | (r1 << 24); };
-  std::vector<uint32_t> count(kRows + 2, 0);
-  std::vector<uint8_t> cut(n_tiles, 0);
+  std::vector<std::pair<uint32_t, TileEnt>> ents;  // (rows run, entry) in tile order
   uint32_t n_cut = 0, g = 0;
   for (uint32_t i = 0; i < n_segs; i++) {
     if (descs[i].flags & kSegSmall) continue;
-    const uint64_t m = descs[i].nblocks;
-    const uint32_t nt = (uint32_t)((m + kTileBlocks - 1) / kTileBlocks);
+    const uint32_t nt = tiles_of(descs[i]), user = descs[i].user;
     for (uint32_t t = 0; t < nt; t++, g++) {
-      const uint32_t r = rows_of(m, t);
-      if (nt > 1 && r == (uint32_t)kRows && n_cut < split) {
-        cut[g] = 1;
+      const uint32_t r = tile_rows(descs[i].nblocks, t), lo = (uint32_t)kRows - r;
+      if (fine && r > fine) {
+        // pieces [r1 - fine, r1) from the tile's end down; the lowest may
+        // start below the tile's first row, which the kernel skips
+        for (uint32_t r1 = kRows; r1 > lo; r1 -= std::min(r1, fine)) {
+          const uint32_t r0 = r1 > fine ? r1 - fine : 0u;
+          ents.push_back({r1 - std::max(r0, lo), TileEnt{g, i, pack(t, r0, r1), user}});
+        }
+      } else if (!fine && nt > 1 && r == (uint32_t)kRows && n_cut < split) {
         n_cut++;
-        count[kPieceRows] += kPieces;
+        for (uint32_t q = 0; q < (uint32_t)(kRows / kPieceRows); q++)
+          ents.push_back({(uint32_t)kPieceRows, TileEnt{g, i, pack(t, q * kPieceRows, (q + 1) * kPieceRows), user}});
       } else {
-        count[r]++;
+        ents.push_back({r, TileEnt{g, i, pack(t, 0, kRows), user}});
       }
     }
   }
   // start of each row count's run, longest first
-  std::vector<uint32_t> pos(kRows + 2, 0);
+  std::vector<uint32_t> pos(kRows + 1, 0);
+  for (const auto& e : ents) pos[e.first]++;
   uint32_t acc = 0;
   for (int r = kRows; r >= 0; r--) {
+    const uint32_t c = pos[r];
     pos[r] = acc;
-    acc += count[r];
+    acc += c;
   }
-  g = 0;
-  for (uint32_t i = 0; i < n_segs; i++) {
-    if (descs[i].flags & kSegSmall) continue;
-    const uint64_t m = descs[i].nblocks;
-    const uint32_t nt = (uint32_t)((m + kTileBlocks - 1) / kTileBlocks);
-    for (uint32_t t = 0; t < nt; t++, g++) {
-      if (cut[g]) {
-        for (uint32_t q = 0; q < kPieces; q++)
-          order[pos[kPieceRows]++] = TileEnt{g, i, pack(t, q * kPieceRows, (q + 1) * kPieceRows), descs[i].user};
-      } else {
-        order[pos[rows_of(m, t)]++] = TileEnt{g, i, pack(t, 0, kRows), descs[i].user};
-      }
-    }
-  }
-  return n_tiles + n_cut * (kPieces - 1);
+  for (const auto& e : ents) order[pos[e.first]++] = e.second;
+  return (uint32_t)ents.size();
 }
 
 // tile_base (n + 1 entries: first tile of each segment; small segments have
@@ -578,15 +598,17 @@ gift_status run_gcm(const gift_tensor* t, const gift_segment_table* st, gift_key
 
   Plan P;
   build_plan(st->segs, n, t->n_rows, t->row_bytes, nonce_base, t->data, out, OPEN, P);
+  const uint32_t cus = (uint32_t)device_cus(dev);
+  const uint32_t fine = fine_cut(P.descs.data(), n, P.n_tiles, cus, &P.n_multi);
 
   // scratch: the staged tables (descs | zero ranges | tile queue | tile_base |
   // small list | queue head), then partials | verdicts | one-tile tag masks
   const size_t o_desc = 0;
   const size_t o_zr = o_desc + align256(sizeof(SegDesc) * n);
   const size_t o_to = o_zr + align256(sizeof(ZeroRange) * P.zr.size());
-  // the queue's tail splits about one whole tile per CU into pieces
-  const uint32_t split = P.n_multi ? (uint32_t)device_cus(dev) : 0u;
-  const size_t o_tb = o_to + align256(sizeof(TileEnt) * ((size_t)P.n_tiles + (uint64_t)(kRows / kPieceRows - 1) * split));
+  // without a fine cut, the queue's tail splits about one whole tile per CU into pieces
+  const uint32_t split = P.n_multi ? cus : 0u;
+  const size_t o_tb = o_to + align256(sizeof(TileEnt) * queue_capacity(P.n_tiles, split, fine, cus));
   const size_t o_sl = o_tb + align256(4ull * (n + 1));
   const size_t o_qh = o_sl + align256(4ull * (n ? n : 1));
   const size_t o_pt = o_qh + 256;  // end of the staged tables
@@ -601,7 +623,7 @@ gift_status run_gcm(const gift_tensor* t, const gift_segment_table* st, gift_key
   std::vector<uint8_t> host(o_pt);  // zero-filled: the queue head starts at 0
   if (n) memcpy(host.data() + o_desc, P.descs.data(), sizeof(SegDesc) * n);
   if (!P.zr.empty()) memcpy(host.data() + o_zr, P.zr.data(), sizeof(ZeroRange) * P.zr.size());
-  const uint32_t n_ents = P.n_tiles ? tile_order(P.descs.data(), n, P.n_tiles, split, (TileEnt*)(host.data() + o_to)) : 0u;
+  const uint32_t n_ents = P.n_tiles ? tile_order(P.descs.data(), n, split, fine, (TileEnt*)(host.data() + o_to)) : 0u;
   const bool pieces = n_ents > P.n_tiles;  // some tile is split: its partial is an XOR of pieces
   tile_tables(P.descs.data(), n, (uint32_t*)(host.data() + o_tb), (uint32_t*)(host.data() + o_sl));
   int32_t* verdicts = st->verdicts ? st->verdicts : (int32_t*)(scratch + o_vd);
@@ -803,6 +825,8 @@ gift_status run_paged(const gift_paged_kv* kv, const gift_request* reqs, uint32_
   }
   uint32_t shift = 0;
   while ((16ull << shift) < kv->chunk_bytes) shift++;
+  const uint32_t cus = (uint32_t)device_cus(dev);
+  const uint32_t fine = fine_cut(descs.data(), n, n_tiles, cus, &n_multi);
 
   // scratch: the staged tables (descs | block ids | tile queue | tile_base |
   // small list | queue head), then partials | verdicts | chunk offsets |
@@ -810,9 +834,9 @@ gift_status run_paged(const gift_paged_kv* kv, const gift_request* reqs, uint32_
   const size_t o_desc = 0;
   const size_t o_bid = o_desc + align256(sizeof(SegDesc) * n);
   const size_t o_to = o_bid + align256(4ull * total_bids);
-  // the queue's tail splits about one whole tile per CU into pieces
-  const uint32_t split = n_multi ? (uint32_t)device_cus(dev) : 0u;
-  const size_t o_tb = o_to + align256(sizeof(TileEnt) * ((size_t)n_tiles + (uint64_t)(kRows / kPieceRows - 1) * split));
+  // without a fine cut, the queue's tail splits about one whole tile per CU into pieces
+  const uint32_t split = n_multi ? cus : 0u;
+  const size_t o_tb = o_to + align256(sizeof(TileEnt) * queue_capacity(n_tiles, split, fine, cus));
   const size_t o_sl = o_tb + align256(4ull * (n + 1));
   const size_t o_qh = o_sl + align256(4ull * n);
   const size_t o_pt = o_qh + 256;  // end of the staged tables
@@ -833,7 +857,7 @@ gift_status run_paged(const gift_paged_kv* kv, const gift_request* reqs, uint32_
       bp += reqs[i].n_block_ids;
     }
   }
-  const uint32_t n_ents = n_tiles ? tile_order(descs.data(), n, n_tiles, split, (TileEnt*)(host.data() + o_to)) : 0u;
+  const uint32_t n_ents = n_tiles ? tile_order(descs.data(), n, split, fine, (TileEnt*)(host.data() + o_to)) : 0u;
   const bool pieces = n_ents > n_tiles;  // some tile is split: its partial is an XOR of pieces
   tile_tables(descs.data(), n, (uint32_t*)(host.data() + o_tb), (uint32_t*)(host.data() + o_sl));
   int32_t* verdicts = verdicts_user ? verdicts_user : (int32_t*)(scratch + o_vd);

@@ -132,13 +132,24 @@ constexpr uint64_t kNoBids = ~0ull;
 hipError_t launch_prologue(void* dst, const void* src, size_t bytes, uint32_t n_segs, uint64_t bids_off,
                            const uint32_t* labels, int32_t* verdicts, const KeyTableDev* kt, uint4* fin,
                            uint4* zero, uint32_t n_zero, hipStream_t s);
-// The work queue, longest pieces first: whole tiles, then by number of rows
-// the segments' partial first tiles and the pieces of split tiles.  Up to
-// `split` whole tiles of segments longer than one tile are split into
-// kRows / kPieceRows pieces.  Returns the number of entries written to order
-// (n_tiles + kRows / kPieceRows - 1 per split tile; order must have room for
-// n_tiles + (kRows / kPieceRows - 1) * split).
-uint32_t tile_order(const SegDesc* descs, uint32_t n_segs, uint32_t n_tiles, uint32_t split, TileEnt* order);
+// Piece size for a queue too short to occupy the device: when fewer tiles
+// than cus exist, every tile is cut into pieces of `fine` tile rows, fine =
+// ceil(tile rows of all tiles / cus), so that one tile no longer runs on one
+// CU while the others idle.  One-tile segments whose tile is cut lose
+// kSegOneTile (their tag comes from the finalize pass) and count into
+// *n_multi.  Returns 0 (no cut) when the tiles alone fill the device.
+uint32_t fine_cut(SegDesc* descs, uint32_t n_segs, uint32_t n_tiles, uint32_t cus, uint32_t* n_multi);
+// The work queue, longest entries first (by the rows each entry runs).  With
+// fine > 0 every tile of more than `fine` rows is cut into pieces of `fine`
+// rows, aligned to the tile's end; otherwise up to `split` whole tiles of
+// segments longer than one tile are cut into kRows / kPieceRows pieces (the
+// queue's tail).  Returns the number of entries written to order, at most
+// queue_capacity(n_tiles, split, fine, cus) for the cus given to fine_cut.
+uint32_t tile_order(const SegDesc* descs, uint32_t n_segs, uint32_t split, uint32_t fine, TileEnt* order);
+inline uint64_t queue_capacity(uint32_t n_tiles, uint32_t split, uint32_t fine, uint32_t cus) {
+  // fine >= rows / cus, so the pieces number at most rows / fine + n_tiles
+  return (uint64_t)n_tiles + (fine ? (uint64_t)cus : (uint64_t)(kRows / kPieceRows - 1) * split);
+}
 hipError_t launch_gcm_tiles(const GcmArgs& a, int mode, uint32_t grid, hipStream_t s);
 hipError_t launch_gcm_small(const GcmArgs& a, bool open, hipStream_t s);
 hipError_t launch_gcm_finalize(const GcmArgs& a, bool open, hipStream_t s);

@@ -1,0 +1,169 @@
+"""Host logic of the per-block kernel's work queue (no GPU): the fine cut of
+short queues and the order of tiles and pieces, called through the
+library's internal C++ entry points on random segment tables.
+
+What the kernel relies on: every tile's rows that hold blocks are covered
+exactly once by its entries; a tile that is cut has no whole-tile entry (a
+whole tile stores its GHASH partial, pieces XOR theirs into it); entries
+come longest first; a one-tile segment whose tile is cut loses its one-tile
+flag and counts as a multi-entry segment; the entries fit the capacity the
+host allocates."""
+import ctypes
+import subprocess
+
+import numpy as np
+import pytest
+
+from paper_2608_25431_amd import gift
+
+# compile-time constants of the library (gift_internal.hpp)
+THREADS, ROWS = 1024, 128
+TILE_BLOCKS = THREADS * ROWS
+PIECE_ROWS = ROWS // 4
+SMALL_MAX_BLOCKS = 64
+SEG_SMALL, SEG_ONE_TILE = 2, 4
+
+SEGDESC = np.dtype([("byte_off", "<u8"), ("len", "<u8"), ("row_begin", "<u8"), ("row_count", "<u8"),
+                    ("iv", "<u4", 3), ("user", "<u4"), ("nblocks", "<u4"), ("flags", "<u4"), ("chunk0", "<u8")])
+TILEENT = np.dtype([("g", "<u4"), ("s", "<u4"), ("trow", "<u4"), ("user", "<u4")])
+assert SEGDESC.itemsize == 64 and TILEENT.itemsize == 16
+
+
+@pytest.fixture(scope="module")
+def planner():
+    if not __import__("os").path.exists(gift.LIB_PATH):
+        from paper_2608_25431_amd import build
+        build.build()
+    lib = gift.lib()
+    out = subprocess.run(["nm", "-D", "--defined-only", gift.LIB_PATH], capture_output=True, text=True).stdout
+    names = [l.split()[-1] for l in out.splitlines() if l.strip()]
+    fine = getattr(lib, next(n for n in names if n.startswith("_ZN4gift8fine_cut")))
+    order = getattr(lib, next(n for n in names if n.startswith("_ZN4gift10tile_order")))
+    fine.argtypes = [ctypes.c_void_p, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint32,
+                     ctypes.POINTER(ctypes.c_uint32)]
+    fine.restype = ctypes.c_uint32
+    order.argtypes = [ctypes.c_void_p, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_void_p]
+    order.restype = ctypes.c_uint32
+    return fine, order
+
+
+def descs_of(nblocks, rng):
+    d = np.zeros(len(nblocks), SEGDESC)
+    d["nblocks"] = nblocks
+    d["user"] = rng.integers(0, 1000, len(nblocks))
+    small = d["nblocks"] <= SMALL_MAX_BLOCKS
+    one = ~small & (d["nblocks"] <= TILE_BLOCKS)
+    d["flags"] = 1 | np.where(small, SEG_SMALL, 0) | np.where(one, SEG_ONE_TILE, 0)
+    return d
+
+
+def tile_rows(m, t):
+    # rows of tile t that hold blocks: tiles end at the segment's end
+    missing = (t + 1) * TILE_BLOCKS - m
+    return ROWS if missing <= 0 else ROWS - missing // THREADS
+
+
+def plan(planner, d, cus):
+    fine_cut, tile_order = planner
+    n = len(d)
+    n_tiles = int(sum(-(-int(m) // TILE_BLOCKS) for m, f in zip(d["nblocks"], d["flags"]) if not f & SEG_SMALL))
+    flags0 = d["flags"].copy()
+    n_multi = ctypes.c_uint32(int(sum(1 for f in flags0 if not f & (SEG_SMALL | SEG_ONE_TILE))))
+    fine = fine_cut(d.ctypes.data, n, n_tiles, cus, ctypes.byref(n_multi))
+    split = cus if n_multi.value else 0
+    cap = n_tiles + (cus if fine else (ROWS // PIECE_ROWS - 1) * split)
+    order = np.zeros(max(cap, 1) + 8, TILEENT)
+    order[cap:]["g"] = 0xDEADBEEF  # guard entries past the capacity
+    n_ents = tile_order(d.ctypes.data, n, split, fine, order.ctypes.data) if n_tiles else 0
+    assert (order[cap:]["g"] == 0xDEADBEEF).all()
+    return n_tiles, flags0, n_multi.value, fine, split, order[:n_ents]
+
+
+def check(d, cus, n_tiles, flags0, n_multi, fine, split, ents):
+    segs = [i for i in range(len(d)) if not flags0[i] & SEG_SMALL]
+    tile_base, rows_total, g = {}, 0, 0
+    for i in segs:
+        tile_base[i] = g
+        nt = -(-int(d["nblocks"][i]) // TILE_BLOCKS)
+        rows_total += sum(tile_rows(int(d["nblocks"][i]), t) for t in range(nt))
+        g += nt
+    assert g == n_tiles
+    # the piece size: ceil(rows / cus) when the tiles alone cannot fill the device
+    if n_tiles == 0 or n_tiles >= cus:
+        assert fine == 0
+    else:
+        assert fine == -(-rows_total // cus) or (fine == 0 and -(-rows_total // cus) >= ROWS)
+    t_of = ents["trow"] & 0xFFFF
+    r0, r1 = (ents["trow"] >> 16) & 0xFF, ents["trow"] >> 24
+    assert (r0 < r1).all() and (r1 <= ROWS).all()
+    run = []
+    covered = {}
+    for k in range(len(ents)):
+        s, t = int(ents["s"][k]), int(t_of[k])
+        assert s in tile_base and ents["user"][k] == d["user"][s]
+        assert ents["g"][k] == tile_base[s] + t
+        lo = ROWS - tile_rows(int(d["nblocks"][s]), t)
+        a, b = max(int(r0[k]), lo), int(r1[k])
+        assert a < b, "an entry runs no row"
+        run.append(b - a)
+        covered.setdefault(int(ents["g"][k]), []).append((a, b, int(r0[k]), int(r1[k]), lo))
+    assert run == sorted(run, reverse=True), "longest entries first"
+    assert len(covered) == n_tiles
+    n_split = 0
+    for gg, parts in covered.items():
+        parts.sort()
+        lo = parts[0][4]
+        assert parts[0][0] == lo and parts[-1][1] == ROWS
+        for x, y in zip(parts, parts[1:]):
+            assert x[1] == y[0], "rows covered exactly once"
+        if len(parts) > 1:
+            n_split += 1
+            assert all(not (p[2] == 0 and p[3] == ROWS) for p in parts), "a cut tile has no whole-tile entry"
+            if fine:
+                assert all(p[1] - p[0] <= fine for p in parts)
+            else:
+                assert all(p[3] - p[2] == PIECE_ROWS for p in parts)
+    if not fine:
+        assert n_split <= split
+    # one-tile flags: kept unless the tile was cut; the multi-entry count follows
+    for i in segs:
+        cut = len(covered[tile_base[i]]) > 1
+        had = bool(flags0[i] & SEG_ONE_TILE)
+        assert bool(d["flags"][i] & SEG_ONE_TILE) == (had and not cut)
+    assert n_multi == sum(1 for i in segs if not d["flags"][i] & SEG_ONE_TILE)
+
+
+REGIMES = {
+    "tiny": lambda r, n: r.integers(1, 7000, n),
+    "one_tile": lambda r, n: r.integers(65, TILE_BLOCKS + 1, n),
+    "mixed": lambda r, n: np.concatenate([r.integers(1, 200, n // 3), r.integers(65, TILE_BLOCKS + 1, n // 3),
+                                          r.integers(TILE_BLOCKS, 9 * TILE_BLOCKS, n - 2 * (n // 3))]),
+    "multi": lambda r, n: r.integers(TILE_BLOCKS // 2, 40 * TILE_BLOCKS, n),
+    "whole_tiles": lambda r, n: TILE_BLOCKS * r.integers(1, 6, n),
+}
+
+
+@pytest.mark.parametrize("regime", sorted(REGIMES))
+@pytest.mark.parametrize("cus", [256, 64, 7, 1])
+def test_queue_covers_every_row_once_longest_first(planner, regime, cus):
+    rng = np.random.default_rng(1000 * sorted(REGIMES).index(regime) + cus)
+    for n in (1, 2, 5, 33, 200):
+        d = descs_of(REGIMES[regime](rng, n), rng)
+        res = plan(planner, d, cus)
+        check(d, cus, *res)
+
+
+def test_single_small_tile_is_cut_across_the_device(planner):
+    # a 1.5 MiB segment (96 tile rows) on 256 CUs: 96 one-row pieces
+    d = descs_of(np.array([96 * THREADS]), np.random.default_rng(1))
+    n_tiles, flags0, n_multi, fine, split, ents = plan(planner, d, 256)
+    assert (n_tiles, fine, len(ents), n_multi) == (1, 1, 96, 1)
+    assert not d["flags"][0] & SEG_ONE_TILE
+
+
+def test_full_device_queue_keeps_whole_tiles(planner):
+    # as many tiles as CUs: no fine cut, one-tile segments keep their path
+    d = descs_of(np.full(256, 3 * THREADS + 5), np.random.default_rng(2))
+    n_tiles, flags0, n_multi, fine, split, ents = plan(planner, d, 256)
+    assert fine == 0 and len(ents) == 256 and n_multi == 0
+    assert (d["flags"] & SEG_ONE_TILE).all()
