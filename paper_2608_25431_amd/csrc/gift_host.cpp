@@ -36,51 +36,84 @@ uint32_t tiles_of(const SegDesc& d) { return (uint32_t)(((uint64_t)d.nblocks + k
 
 }  // namespace
 
-uint32_t fine_cut(SegDesc* descs, uint32_t n_segs, uint32_t n_tiles, uint32_t cus, uint32_t* n_multi) {
-  if (n_tiles == 0 || cus == 0 || n_tiles >= cus) return 0;
-  uint64_t rows = 0;
-  for (uint32_t i = 0; i < n_segs; i++) {
+uint32_t plan_cuts(SegDesc* descs, uint32_t n_segs, uint32_t n_tiles, uint32_t cus, uint32_t* n_multi,
+                   uint8_t* cut) {
+  static_assert(kRows % kPieceRows == 0 && kPieceRows > 0 && kRows < 256, "pieces of a tile");
+  if (n_tiles == 0 || cus == 0) return 0;
+  std::vector<uint32_t> rows(n_tiles);
+  std::vector<uint32_t> seg(n_tiles);
+  uint64_t total = 0;
+  for (uint32_t i = 0, g = 0; i < n_segs; i++) {
     if (descs[i].flags & kSegSmall) continue;
     const uint32_t nt = tiles_of(descs[i]);
-    for (uint32_t t = 0; t < nt; t++) rows += tile_rows(descs[i].nblocks, t);
+    for (uint32_t t = 0; t < nt; t++, g++) {
+      rows[g] = tile_rows(descs[i].nblocks, t);
+      seg[g] = i;
+      total += rows[g];
+    }
   }
-  const uint32_t fine = (uint32_t)((rows + cus - 1) / cus);
-  if (fine >= (uint32_t)kRows) return 0;  // (not reached while n_tiles < cus)
-  for (uint32_t i = 0; i < n_segs; i++)
-    if ((descs[i].flags & kSegOneTile) && tile_rows(descs[i].nblocks, 0) > fine) {
-      descs[i].flags &= ~kSegOneTile;
+  uint32_t piece = 0;
+  memset(cut, 0, n_tiles);
+  if (n_tiles < cus) {
+    piece = (uint32_t)((total + cus - 1) / cus);
+    if (piece >= (uint32_t)kRows) return 0;  // (not reached while n_tiles < cus)
+    for (uint32_t g = 0; g < n_tiles; g++) cut[g] = rows[g] > piece;
+  } else {
+    // the queue's tail: up to cus of the largest tiles, in tile order
+    // within a row count
+    piece = kPieceRows;
+    std::vector<uint32_t> count(kRows + 1, 0);
+    for (uint32_t g = 0; g < n_tiles; g++) count[rows[g]]++;
+    uint32_t left = cus, from = kRows + 1, take_at = 0;  // cut every tile of more than `from` rows...
+    for (uint32_t r = kRows; r > (uint32_t)kPieceRows && left; r--) {
+      if (count[r] <= left) {
+        left -= count[r];
+        from = r;
+      } else {
+        take_at = r;  // ...and the first `left` tiles of `take_at` rows
+        break;
+      }
+    }
+    for (uint32_t g = 0; g < n_tiles; g++) {
+      if (rows[g] >= from) {
+        cut[g] = 1;
+      } else if (rows[g] == take_at && left) {
+        cut[g] = 1;
+        left--;
+      }
+    }
+  }
+  uint32_t n_cut = 0;
+  for (uint32_t g = 0; g < n_tiles; g++) {
+    if (!cut[g]) continue;
+    n_cut++;
+    SegDesc& d = descs[seg[g]];
+    if (d.flags & kSegOneTile) {
+      d.flags &= ~kSegOneTile;
       (*n_multi)++;
     }
-  return fine;
+  }
+  return n_cut ? piece : 0;
 }
 
 // Longest entries first, so that a work queue over them ends with short
-// work: a counting sort by the number of rows each entry runs.  Without a
-// fine cut, the tail also gets the pieces of up to `split` whole tiles of
-// segments longer than one tile: the workgroups run at slightly different
-// speeds, and with whole tiles at the end the fast ones would run out of work
-// a tile's time before the slow ones.
-uint32_t tile_order(const SegDesc* descs, uint32_t n_segs, uint32_t split, uint32_t fine, TileEnt* order) {
-  static_assert(kRows % kPieceRows == 0 && kPieceRows > 0 && kRows < 256, "pieces of a tile");
+// work: a counting sort by the number of rows each entry runs.
+uint32_t tile_order(const SegDesc* descs, uint32_t n_segs, uint32_t rows, const uint8_t* cut, TileEnt* order) {
   auto pack = [](uint32_t t, uint32_t r0, uint32_t r1) { return t | (r0 << 16) | (r1 << 24); };
   std::vector<std::pair<uint32_t, TileEnt>> ents;  // (rows run, entry) in tile order
-  uint32_t n_cut = 0, g = 0;
+  uint32_t g = 0;
   for (uint32_t i = 0; i < n_segs; i++) {
     if (descs[i].flags & kSegSmall) continue;
     const uint32_t nt = tiles_of(descs[i]), user = descs[i].user;
     for (uint32_t t = 0; t < nt; t++, g++) {
       const uint32_t r = tile_rows(descs[i].nblocks, t), lo = (uint32_t)kRows - r;
-      if (fine && r > fine) {
-        // pieces [r1 - fine, r1) from the tile's end down; the lowest may
+      if (cut[g] && rows) {
+        // pieces [r1 - rows, r1) from the tile's end down; the lowest may
         // start below the tile's first row, which the kernel skips
-        for (uint32_t r1 = kRows; r1 > lo; r1 -= std::min(r1, fine)) {
-          const uint32_t r0 = r1 > fine ? r1 - fine : 0u;
+        for (uint32_t r1 = kRows; r1 > lo; r1 -= std::min(r1, rows)) {
+          const uint32_t r0 = r1 > rows ? r1 - rows : 0u;
           ents.push_back({r1 - std::max(r0, lo), TileEnt{g, i, pack(t, r0, r1), user}});
         }
-      } else if (!fine && nt > 1 && r == (uint32_t)kRows && n_cut < split) {
-        n_cut++;
-        for (uint32_t q = 0; q < (uint32_t)(kRows / kPieceRows); q++)
-          ents.push_back({(uint32_t)kPieceRows, TileEnt{g, i, pack(t, q * kPieceRows, (q + 1) * kPieceRows), user}});
       } else {
         ents.push_back({r, TileEnt{g, i, pack(t, 0, kRows), user}});
       }
@@ -599,16 +632,15 @@ gift_status run_gcm(const gift_tensor* t, const gift_segment_table* st, gift_key
   Plan P;
   build_plan(st->segs, n, t->n_rows, t->row_bytes, nonce_base, t->data, out, OPEN, P);
   const uint32_t cus = (uint32_t)device_cus(dev);
-  const uint32_t fine = fine_cut(P.descs.data(), n, P.n_tiles, cus, &P.n_multi);
+  std::vector<uint8_t> cut(P.n_tiles);
+  const uint32_t piece = plan_cuts(P.descs.data(), n, P.n_tiles, cus, &P.n_multi, cut.data());
 
   // scratch: the staged tables (descs | zero ranges | tile queue | tile_base |
   // small list | queue head), then partials | verdicts | one-tile tag masks
   const size_t o_desc = 0;
   const size_t o_zr = o_desc + align256(sizeof(SegDesc) * n);
   const size_t o_to = o_zr + align256(sizeof(ZeroRange) * P.zr.size());
-  // without a fine cut, the queue's tail splits about one whole tile per CU into pieces
-  const uint32_t split = P.n_multi ? cus : 0u;
-  const size_t o_tb = o_to + align256(sizeof(TileEnt) * queue_capacity(P.n_tiles, split, fine, cus));
+  const size_t o_tb = o_to + align256(sizeof(TileEnt) * queue_capacity(P.n_tiles, cus));
   const size_t o_sl = o_tb + align256(4ull * (n + 1));
   const size_t o_qh = o_sl + align256(4ull * (n ? n : 1));
   const size_t o_pt = o_qh + 256;  // end of the staged tables
@@ -623,7 +655,7 @@ gift_status run_gcm(const gift_tensor* t, const gift_segment_table* st, gift_key
   std::vector<uint8_t> host(o_pt);  // zero-filled: the queue head starts at 0
   if (n) memcpy(host.data() + o_desc, P.descs.data(), sizeof(SegDesc) * n);
   if (!P.zr.empty()) memcpy(host.data() + o_zr, P.zr.data(), sizeof(ZeroRange) * P.zr.size());
-  const uint32_t n_ents = P.n_tiles ? tile_order(P.descs.data(), n, split, fine, (TileEnt*)(host.data() + o_to)) : 0u;
+  const uint32_t n_ents = P.n_tiles ? tile_order(P.descs.data(), n, piece, cut.data(), (TileEnt*)(host.data() + o_to)) : 0u;
   const bool pieces = n_ents > P.n_tiles;  // some tile is split: its partial is an XOR of pieces
   tile_tables(P.descs.data(), n, (uint32_t*)(host.data() + o_tb), (uint32_t*)(host.data() + o_sl));
   int32_t* verdicts = st->verdicts ? st->verdicts : (int32_t*)(scratch + o_vd);
@@ -826,7 +858,8 @@ gift_status run_paged(const gift_paged_kv* kv, const gift_request* reqs, uint32_
   uint32_t shift = 0;
   while ((16ull << shift) < kv->chunk_bytes) shift++;
   const uint32_t cus = (uint32_t)device_cus(dev);
-  const uint32_t fine = fine_cut(descs.data(), n, n_tiles, cus, &n_multi);
+  std::vector<uint8_t> cut(n_tiles);
+  const uint32_t piece = plan_cuts(descs.data(), n, n_tiles, cus, &n_multi, cut.data());
 
   // scratch: the staged tables (descs | block ids | tile queue | tile_base |
   // small list | queue head), then partials | verdicts | chunk offsets |
@@ -834,9 +867,7 @@ gift_status run_paged(const gift_paged_kv* kv, const gift_request* reqs, uint32_
   const size_t o_desc = 0;
   const size_t o_bid = o_desc + align256(sizeof(SegDesc) * n);
   const size_t o_to = o_bid + align256(4ull * total_bids);
-  // without a fine cut, the queue's tail splits about one whole tile per CU into pieces
-  const uint32_t split = n_multi ? cus : 0u;
-  const size_t o_tb = o_to + align256(sizeof(TileEnt) * queue_capacity(n_tiles, split, fine, cus));
+  const size_t o_tb = o_to + align256(sizeof(TileEnt) * queue_capacity(n_tiles, cus));
   const size_t o_sl = o_tb + align256(4ull * (n + 1));
   const size_t o_qh = o_sl + align256(4ull * n);
   const size_t o_pt = o_qh + 256;  // end of the staged tables
@@ -857,7 +888,7 @@ gift_status run_paged(const gift_paged_kv* kv, const gift_request* reqs, uint32_
       bp += reqs[i].n_block_ids;
     }
   }
-  const uint32_t n_ents = n_tiles ? tile_order(descs.data(), n, split, fine, (TileEnt*)(host.data() + o_to)) : 0u;
+  const uint32_t n_ents = n_tiles ? tile_order(descs.data(), n, piece, cut.data(), (TileEnt*)(host.data() + o_to)) : 0u;
   const bool pieces = n_ents > n_tiles;  // some tile is split: its partial is an XOR of pieces
   tile_tables(descs.data(), n, (uint32_t*)(host.data() + o_tb), (uint32_t*)(host.data() + o_sl));
   int32_t* verdicts = verdicts_user ? verdicts_user : (int32_t*)(scratch + o_vd);

@@ -76,15 +76,14 @@ struct KeyTableDev {
 // One entry of the tile kernel's work queue: rows [r0, r1) of tile g (in
 // tile_base numbering), which is tile t of segment s counted from the
 // segment's end; user is the segment's user.  trow packs t (bits 0-15), r0
-// (16-23) and r1 (24-31).  A whole tile has r0 = 0, r1 = kRows; the queue's
-// tail splits some tiles into pieces of rows, so that workgroups that run
-// faster take more of the last work.
+// (16-23) and r1 (24-31).  A whole tile has r0 = 0, r1 = kRows; a tile that
+// plan_cuts cuts has one entry per piece of rows instead.
 struct TileEnt {
   uint32_t g, s, trow, user;
 };
 static_assert(sizeof(TileEnt) == 16, "TileEnt layout");
 static_assert(kRows <= 255, "rows fit a byte of TileEnt::trow");
-constexpr int kPieceRows = kRows / 4;  // rows of one piece of a split tile
+constexpr int kPieceRows = kRows / 4;  // rows of the pieces cut at the queue's tail
 constexpr uint32_t kNoTile = 0xFFFFFFFFu;
 
 // Addressing of k_gcm_tiles: contiguous tensor, or a paged cache on the
@@ -132,23 +131,30 @@ constexpr uint64_t kNoBids = ~0ull;
 hipError_t launch_prologue(void* dst, const void* src, size_t bytes, uint32_t n_segs, uint64_t bids_off,
                            const uint32_t* labels, int32_t* verdicts, const KeyTableDev* kt, uint4* fin,
                            uint4* zero, uint32_t n_zero, hipStream_t s);
-// Piece size for a queue too short to occupy the device: when fewer tiles
-// than cus exist, every tile is cut into pieces of `fine` tile rows, fine =
-// ceil(tile rows of all tiles / cus), so that one tile no longer runs on one
-// CU while the others idle.  One-tile segments whose tile is cut lose
-// kSegOneTile (their tag comes from the finalize pass) and count into
-// *n_multi.  Returns 0 (no cut) when the tiles alone fill the device.
-uint32_t fine_cut(SegDesc* descs, uint32_t n_segs, uint32_t n_tiles, uint32_t cus, uint32_t* n_multi);
-// The work queue, longest entries first (by the rows each entry runs).  With
-// fine > 0 every tile of more than `fine` rows is cut into pieces of `fine`
-// rows, aligned to the tile's end; otherwise up to `split` whole tiles of
-// segments longer than one tile are cut into kRows / kPieceRows pieces (the
-// queue's tail).  Returns the number of entries written to order, at most
-// queue_capacity(n_tiles, split, fine, cus) for the cus given to fine_cut.
-uint32_t tile_order(const SegDesc* descs, uint32_t n_segs, uint32_t split, uint32_t fine, TileEnt* order);
-inline uint64_t queue_capacity(uint32_t n_tiles, uint32_t split, uint32_t fine, uint32_t cus) {
-  // fine >= rows / cus, so the pieces number at most rows / fine + n_tiles
-  return (uint64_t)n_tiles + (fine ? (uint64_t)cus : (uint64_t)(kRows / kPieceRows - 1) * split);
+// Which tiles the work queue cuts into pieces, and into pieces of how many
+// tile rows.  A tile runs on one CU, so:
+// - with fewer tiles than cus, every tile of more than `rows` rows is cut,
+//   rows = ceil(tile rows of all tiles / cus), so that one tile no longer
+//   runs on one CU while the others idle;
+// - otherwise up to cus tiles of more than kPieceRows rows, the largest
+//   first, are cut into pieces of kPieceRows rows that sort to the tail of
+//   the queue, so that the workgroups, which run at slightly different
+//   speeds, finish together.
+// cut[g] = 1 for each cut tile g (n_tiles entries).  One-tile segments whose
+// tile is cut lose kSegOneTile (their tag comes from the finalize pass) and
+// count into *n_multi.  Returns the piece rows (0: nothing is cut).
+uint32_t plan_cuts(SegDesc* descs, uint32_t n_segs, uint32_t n_tiles, uint32_t cus, uint32_t* n_multi,
+                   uint8_t* cut);
+// The work queue, longest entries first (by the rows each entry runs): each
+// tile whole, or for cut tiles pieces of `rows` rows aligned to the tile's
+// end.  Returns the number of entries written to order, at most
+// queue_capacity(n_tiles, cus) for the cus given to plan_cuts.
+uint32_t tile_order(const SegDesc* descs, uint32_t n_segs, uint32_t rows, const uint8_t* cut, TileEnt* order);
+inline uint64_t queue_capacity(uint32_t n_tiles, uint32_t cus) {
+  // a tail cut adds at most kRows / kPieceRows - 1 entries for each of at
+  // most cus tiles; a fine cut (rows >= all rows / cus) at most all rows /
+  // rows <= cus entries beyond one per tile
+  return (uint64_t)n_tiles + (uint64_t)(kRows / kPieceRows - 1) * cus;
 }
 hipError_t launch_gcm_tiles(const GcmArgs& a, int mode, uint32_t grid, hipStream_t s);
 hipError_t launch_gcm_small(const GcmArgs& a, bool open, hipStream_t s);

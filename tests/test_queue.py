@@ -37,14 +37,14 @@ def planner():
     lib = gift.lib()
     out = subprocess.run(["nm", "-D", "--defined-only", gift.LIB_PATH], capture_output=True, text=True).stdout
     names = [l.split()[-1] for l in out.splitlines() if l.strip()]
-    fine = getattr(lib, next(n for n in names if n.startswith("_ZN4gift8fine_cut")))
+    cuts = getattr(lib, next(n for n in names if n.startswith("_ZN4gift9plan_cuts")))
     order = getattr(lib, next(n for n in names if n.startswith("_ZN4gift10tile_order")))
-    fine.argtypes = [ctypes.c_void_p, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint32,
-                     ctypes.POINTER(ctypes.c_uint32)]
-    fine.restype = ctypes.c_uint32
-    order.argtypes = [ctypes.c_void_p, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_void_p]
+    cuts.argtypes = [ctypes.c_void_p, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint32,
+                     ctypes.POINTER(ctypes.c_uint32), ctypes.c_void_p]
+    cuts.restype = ctypes.c_uint32
+    order.argtypes = [ctypes.c_void_p, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_void_p, ctypes.c_void_p]
     order.restype = ctypes.c_uint32
-    return fine, order
+    return cuts, order
 
 
 def descs_of(nblocks, rng):
@@ -64,35 +64,48 @@ def tile_rows(m, t):
 
 
 def plan(planner, d, cus):
-    fine_cut, tile_order = planner
+    plan_cuts, tile_order = planner
     n = len(d)
     n_tiles = int(sum(-(-int(m) // TILE_BLOCKS) for m, f in zip(d["nblocks"], d["flags"]) if not f & SEG_SMALL))
     flags0 = d["flags"].copy()
     n_multi = ctypes.c_uint32(int(sum(1 for f in flags0 if not f & (SEG_SMALL | SEG_ONE_TILE))))
-    fine = fine_cut(d.ctypes.data, n, n_tiles, cus, ctypes.byref(n_multi))
-    split = cus if n_multi.value else 0
-    cap = n_tiles + (cus if fine else (ROWS // PIECE_ROWS - 1) * split)
+    cut = np.full(max(n_tiles, 1), 7, np.uint8)
+    piece = plan_cuts(d.ctypes.data, n, n_tiles, cus, ctypes.byref(n_multi), cut.ctypes.data)
+    cap = n_tiles + (ROWS // PIECE_ROWS - 1) * cus
     order = np.zeros(max(cap, 1) + 8, TILEENT)
     order[cap:]["g"] = 0xDEADBEEF  # guard entries past the capacity
-    n_ents = tile_order(d.ctypes.data, n, split, fine, order.ctypes.data) if n_tiles else 0
+    n_ents = tile_order(d.ctypes.data, n, piece, cut.ctypes.data, order.ctypes.data) if n_tiles else 0
     assert (order[cap:]["g"] == 0xDEADBEEF).all()
-    return n_tiles, flags0, n_multi.value, fine, split, order[:n_ents]
+    return n_tiles, flags0, n_multi.value, piece, cut[:n_tiles], order[:n_ents]
 
 
-def check(d, cus, n_tiles, flags0, n_multi, fine, split, ents):
+def check(d, cus, n_tiles, flags0, n_multi, piece, cut, ents):
     segs = [i for i in range(len(d)) if not flags0[i] & SEG_SMALL]
-    tile_base, rows_total, g = {}, 0, 0
+    tile_base, rows, g = {}, [], 0
     for i in segs:
         tile_base[i] = g
         nt = -(-int(d["nblocks"][i]) // TILE_BLOCKS)
-        rows_total += sum(tile_rows(int(d["nblocks"][i]), t) for t in range(nt))
+        rows += [tile_rows(int(d["nblocks"][i]), t) for t in range(nt)]
         g += nt
     assert g == n_tiles
-    # the piece size: ceil(rows / cus) when the tiles alone cannot fill the device
-    if n_tiles == 0 or n_tiles >= cus:
-        assert fine == 0
+    rows = np.array(rows, np.int64)
+    assert set(np.unique(cut)) <= {0, 1}
+    cut = cut.astype(bool)
+    # which tiles are cut, into pieces of how many rows
+    if n_tiles == 0:
+        assert piece == 0
+    elif n_tiles < cus:
+        fine = -(-int(rows.sum()) // cus)
+        assert (cut == (rows > fine)).all()
+        assert piece == (fine if cut.any() else 0)
     else:
-        assert fine == -(-rows_total // cus) or (fine == 0 and -(-rows_total // cus) >= ROWS)
+        assert piece == (PIECE_ROWS if cut.any() else 0)
+        assert cut.sum() <= cus and (rows[cut] > PIECE_ROWS).all()
+        longer = rows > PIECE_ROWS
+        if cut.sum() < cus:
+            assert (cut == longer).all(), "every tile longer than a piece is cut"
+        if cut.any() and (longer & ~cut).any():
+            assert rows[cut].min() >= rows[longer & ~cut].max(), "the largest tiles are cut"
     t_of = ents["trow"] & 0xFFFF
     r0, r1 = (ents["trow"] >> 16) & 0xFF, ents["trow"] >> 24
     assert (r0 < r1).all() and (r1 <= ROWS).all()
@@ -109,27 +122,22 @@ def check(d, cus, n_tiles, flags0, n_multi, fine, split, ents):
         covered.setdefault(int(ents["g"][k]), []).append((a, b, int(r0[k]), int(r1[k]), lo))
     assert run == sorted(run, reverse=True), "longest entries first"
     assert len(covered) == n_tiles
-    n_split = 0
     for gg, parts in covered.items():
         parts.sort()
         lo = parts[0][4]
         assert parts[0][0] == lo and parts[-1][1] == ROWS
         for x, y in zip(parts, parts[1:]):
             assert x[1] == y[0], "rows covered exactly once"
-        if len(parts) > 1:
-            n_split += 1
+        if cut[gg]:
+            assert len(parts) > 1
             assert all(not (p[2] == 0 and p[3] == ROWS) for p in parts), "a cut tile has no whole-tile entry"
-            if fine:
-                assert all(p[1] - p[0] <= fine for p in parts)
-            else:
-                assert all(p[3] - p[2] == PIECE_ROWS for p in parts)
-    if not fine:
-        assert n_split <= split
+            assert all((ROWS - p[3]) % piece == 0 and p[3] - p[2] <= piece for p in parts), "pieces end-aligned"
+        else:
+            assert len(parts) == 1 and parts[0][2:4] == (0, ROWS)
     # one-tile flags: kept unless the tile was cut; the multi-entry count follows
     for i in segs:
-        cut = len(covered[tile_base[i]]) > 1
         had = bool(flags0[i] & SEG_ONE_TILE)
-        assert bool(d["flags"][i] & SEG_ONE_TILE) == (had and not cut)
+        assert bool(d["flags"][i] & SEG_ONE_TILE) == (had and not cut[tile_base[i]])
     assert n_multi == sum(1 for i in segs if not d["flags"][i] & SEG_ONE_TILE)
 
 
@@ -156,14 +164,22 @@ def test_queue_covers_every_row_once_longest_first(planner, regime, cus):
 def test_single_small_tile_is_cut_across_the_device(planner):
     # a 1.5 MiB segment (96 tile rows) on 256 CUs: 96 one-row pieces
     d = descs_of(np.array([96 * THREADS]), np.random.default_rng(1))
-    n_tiles, flags0, n_multi, fine, split, ents = plan(planner, d, 256)
-    assert (n_tiles, fine, len(ents), n_multi) == (1, 1, 96, 1)
+    n_tiles, flags0, n_multi, piece, cut, ents = plan(planner, d, 256)
+    assert (n_tiles, piece, len(ents), n_multi) == (1, 1, 96, 1)
     assert not d["flags"][0] & SEG_ONE_TILE
 
 
-def test_full_device_queue_keeps_whole_tiles(planner):
-    # as many tiles as CUs: no fine cut, one-tile segments keep their path
+def test_full_device_queue_of_short_tiles_is_not_cut(planner):
+    # as many short tiles as CUs: nothing to cut, one-tile segments keep their path
     d = descs_of(np.full(256, 3 * THREADS + 5), np.random.default_rng(2))
-    n_tiles, flags0, n_multi, fine, split, ents = plan(planner, d, 256)
-    assert fine == 0 and len(ents) == 256 and n_multi == 0
+    n_tiles, flags0, n_multi, piece, cut, ents = plan(planner, d, 256)
+    assert piece == 0 and len(ents) == 256 and n_multi == 0
     assert (d["flags"] & SEG_ONE_TILE).all()
+
+
+def test_one_tile_segments_past_the_cu_count_share_the_tail(planner):
+    # 300 one-tile segments of 96 rows on 256 CUs: 256 of them are cut into
+    # three pieces, so no CU runs two whole tiles while others idle
+    d = descs_of(np.full(300, 96 * THREADS), np.random.default_rng(3))
+    n_tiles, flags0, n_multi, piece, cut, ents = plan(planner, d, 256)
+    assert (piece, int(cut.sum()), len(ents), n_multi) == (PIECE_ROWS, 256, 44 + 3 * 256, 256)
