@@ -3,7 +3,10 @@
 Every entry point has the C name without the ``gift_`` prefix.  Device
 buffers may be passed as torch tensors (their ``data_ptr()`` is used) or as
 raw integer device addresses; host arrays are numpy arrays or bytes.  A
-non-OK status raises :class:`GiftError`.  There is no fallback: if the HIP
+tensor passed as a device buffer must be a contiguous CUDA tensor of at
+least the bytes the call touches, else ValueError is raised before the call
+(the C ABI cannot see buffer sizes).  A non-OK status raises
+:class:`GiftError`.  There is no fallback: if the HIP
 library is not built, importing the binding's functions raises.
 """
 import ctypes
@@ -158,6 +161,27 @@ def _ptr(x):
     raise TypeError(f"cannot take the address of {type(x)}")
 
 
+def _dev(x, nbytes, name):
+    """Address of a device buffer of at least nbytes.  A torch tensor must be a
+    contiguous CUDA tensor that large (a host buffer, or one too short, would
+    make the kernels fault instead of failing here); an int is taken as a
+    device address as is; None is NULL."""
+    if x is None or isinstance(x, int):
+        return x
+    if isinstance(x, np.ndarray):
+        raise ValueError(f"{name}: a numpy array is host memory; pass a CUDA tensor or a device address")
+    if hasattr(x, "data_ptr"):
+        if not getattr(x, "is_cuda", False):
+            raise ValueError(f"{name}: tensor must be on the GPU")
+        if not x.is_contiguous():
+            raise ValueError(f"{name}: tensor must be contiguous")
+        have = x.numel() * x.element_size()
+        if have < nbytes:
+            raise ValueError(f"{name}: {have} bytes, the call needs {nbytes}")
+        return x.data_ptr()
+    raise TypeError(f"{name}: cannot take the address of {type(x)}")
+
+
 def _stream(stream):
     if stream is None:
         try:
@@ -227,9 +251,10 @@ def key_table_create(keys, n_users=None, stream=None):
     return KeyTable(keys, n_users, stream)
 
 
-def _table(segs, row_labels, verdicts):
+def _table(segs, row_labels, verdicts, n_rows=0):
     sg = as_segments(segs)
-    t = _SegTable(sg.ctypes.data if len(sg) else None, len(sg), _ptr(row_labels), _ptr(verdicts))
+    t = _SegTable(sg.ctypes.data if len(sg) else None, len(sg), _dev(row_labels, 4 * n_rows, "row_labels"),
+                  _dev(verdicts, 4 * len(sg), "verdicts"))
     return t, sg
 
 
@@ -242,35 +267,37 @@ def _nonce(nonce_base, kt):
 
 def seal(data, n_rows, row_bytes, segs, kt, nonce_base, out, tags, row_labels=None, verdicts=None, stream=None):
     """gift_seal.  data/out/tags/row_labels/verdicts are device buffers."""
-    t = _Tensor(_ptr(data), n_rows, row_bytes)
-    tab, keep = _table(segs, row_labels, verdicts)
+    total = n_rows * row_bytes
+    t = _Tensor(_dev(data, total, "data"), n_rows, row_bytes)
+    tab, keep = _table(segs, row_labels, verdicts, n_rows)
+    o, tg = _dev(out, total, "out"), _dev(tags, 16 * len(keep), "tags")
     nb = _nonce(nonce_base, kt)
-    _check(lib().gift_seal(ctypes.byref(t), ctypes.byref(tab), kt.handle, nb.ctypes.data, _ptr(out), _ptr(tags),
-                           _stream(stream)))
+    _check(lib().gift_seal(ctypes.byref(t), ctypes.byref(tab), kt.handle, nb.ctypes.data, o, tg, _stream(stream)))
     del keep
 
 
 def open(data, n_rows, row_bytes, segs, kt, nonce_base, out, tags, verdicts, row_labels=None, stream=None):
     """gift_open.  verdicts (device int32[n_segs]) is required."""
-    t = _Tensor(_ptr(data), n_rows, row_bytes)
-    tab, keep = _table(segs, row_labels, verdicts)
+    total = n_rows * row_bytes
+    t = _Tensor(_dev(data, total, "data"), n_rows, row_bytes)
+    tab, keep = _table(segs, row_labels, verdicts, n_rows)
+    o, tg = _dev(out, total, "out"), _dev(tags, 16 * len(keep), "tags")
     nb = _nonce(nonce_base, kt)
-    _check(lib().gift_open(ctypes.byref(t), ctypes.byref(tab), kt.handle, nb.ctypes.data, _ptr(out), _ptr(tags),
-                           _stream(stream)))
+    _check(lib().gift_open(ctypes.byref(t), ctypes.byref(tab), kt.handle, nb.ctypes.data, o, tg, _stream(stream)))
     del keep
 
 
 def check_owner(segs, labels, n_rows, verdicts, stream=None):
     """gift_check_owner."""
     tab, keep = _table(segs, None, verdicts)
-    _check(lib().gift_check_owner(ctypes.byref(tab), _ptr(labels), n_rows, _stream(stream)))
+    _check(lib().gift_check_owner(ctypes.byref(tab), _dev(labels, 4 * n_rows, "labels"), n_rows, _stream(stream)))
     del keep
 
 
 def paged_kv(cache, cache_bytes, layer_stride, block_stride, part_stride, chunk_bytes, n_layers, n_parts, n_blocks):
     """gift_paged_kv for a device allocation (torch tensor or address)."""
-    return _PagedKV(_ptr(cache), cache_bytes, layer_stride, block_stride, part_stride, chunk_bytes, n_layers, n_parts,
-                    n_blocks)
+    return _PagedKV(_dev(cache, cache_bytes, "cache"), cache_bytes, layer_stride, block_stride, part_stride, chunk_bytes,
+                    n_layers, n_parts, n_blocks)
 
 
 def _requests(reqs):
@@ -281,39 +308,47 @@ def _requests(reqs):
     return arr, keep
 
 
+def _paged_bufs(kv, keep, n, export, tags, verdicts, block_labels):
+    total = kv.n_layers * kv.n_parts * kv.chunk_bytes * sum(int(b.size) for b in keep)
+    return (_dev(export, total, "export buffer"), _dev(tags, 16 * n, "tags"), _dev(verdicts, 4 * n, "verdicts"),
+            _dev(block_labels, 4 * kv.n_blocks, "block_labels"))
+
+
 def seal_paged(kv, reqs, kt, nonce_base, out, tags, block_labels=None, verdicts=None, stream=None):
     """gift_seal_paged.  kv from paged_kv(); reqs: list of (block_ids, user, iv_seq)."""
     arr, keep = _requests(reqs)
+    o, tg, vd, lb = _paged_bufs(kv, keep, len(reqs), out, tags, verdicts, block_labels)
     nb = _nonce(nonce_base, kt)
-    _check(lib().gift_seal_paged(ctypes.byref(kv), ctypes.addressof(arr) if reqs else None, len(reqs),
-                                 _ptr(block_labels), kt.handle, nb.ctypes.data, _ptr(out), _ptr(tags), _ptr(verdicts),
-                                 _stream(stream)))
+    _check(lib().gift_seal_paged(ctypes.byref(kv), ctypes.addressof(arr) if reqs else None, len(reqs), lb, kt.handle,
+                                 nb.ctypes.data, o, tg, vd, _stream(stream)))
     del keep
 
 
 def open_paged(kv, reqs, kt, nonce_base, sealed, tags, verdicts, block_labels=None, stream=None):
     """gift_open_paged."""
     arr, keep = _requests(reqs)
+    sd, tg, vd, lb = _paged_bufs(kv, keep, len(reqs), sealed, tags, verdicts, block_labels)
     nb = _nonce(nonce_base, kt)
-    _check(lib().gift_open_paged(ctypes.byref(kv), ctypes.addressof(arr) if reqs else None, len(reqs),
-                                 _ptr(block_labels), kt.handle, nb.ctypes.data, _ptr(sealed), _ptr(tags),
-                                 _ptr(verdicts), _stream(stream)))
+    _check(lib().gift_open_paged(ctypes.byref(kv), ctypes.addressof(arr) if reqs else None, len(reqs), lb, kt.handle,
+                                 nb.ctypes.data, sd, tg, vd, _stream(stream)))
     del keep
 
 
 def token_encrypt(segs, tokens, nonces, n_tokens, kt, eos_token, out, stream=None):
     """gift_token_encrypt: tokens/nonces device u64[n_tokens], out device u8[n_tokens*16]."""
     tab, keep = _table(segs, None, None)
-    _check(lib().gift_token_encrypt(ctypes.byref(tab), _ptr(tokens), _ptr(nonces), n_tokens, kt.handle, eos_token,
-                                    _ptr(out), _stream(stream)))
+    _check(lib().gift_token_encrypt(ctypes.byref(tab), _dev(tokens, 8 * n_tokens, "tokens"),
+                                    _dev(nonces, 8 * n_tokens, "nonces"), n_tokens, kt.handle, eos_token,
+                                    _dev(out, 16 * n_tokens, "out"), _stream(stream)))
     del keep
 
 
 def token_decrypt(segs, blocks, n_tokens, kt, eos_token, tokens_out, nonces_out=None, stream=None):
     """gift_token_decrypt."""
     tab, keep = _table(segs, None, None)
-    _check(lib().gift_token_decrypt(ctypes.byref(tab), _ptr(blocks), n_tokens, kt.handle, eos_token, _ptr(tokens_out),
-                                    _ptr(nonces_out), _stream(stream)))
+    _check(lib().gift_token_decrypt(ctypes.byref(tab), _dev(blocks, 16 * n_tokens, "blocks"), n_tokens, kt.handle,
+                                    eos_token, _dev(tokens_out, 8 * n_tokens, "tokens_out"),
+                                    _dev(nonces_out, 8 * n_tokens, "nonces_out"), _stream(stream)))
     del keep
 
 

@@ -5,6 +5,7 @@ import re
 import subprocess
 import sys
 
+import numpy as np
 import pytest
 
 from paper_2608_25431_amd import gift
@@ -73,3 +74,58 @@ def test_loads_beside_torchs_hip_runtime(lib):
             "from paper_2608_25431_amd import gift; ctypes.CDLL(gift.LIB_PATH)" % ROOT)
     r = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, timeout=300)
     assert r.returncode == 0, r.stderr[-2000:]
+
+
+def test_binding_rejects_host_and_short_device_buffers():
+    # checked before the library is called, so no GPU is needed: a host buffer
+    # or a short one would otherwise reach the kernels as a device address
+    torch = pytest.importorskip("torch")
+    import types
+    kt = types.SimpleNamespace(handle=None, n_users=1)
+    nb = np.zeros(12, np.uint8)
+    cpu = torch.zeros(64, dtype=torch.uint8)
+    with pytest.raises(ValueError, match="on the GPU"):
+        gift.seal(cpu, 1, 64, [(0, 1, 0, 0)], kt, nb, cpu, cpu)
+    with pytest.raises(ValueError, match="host memory"):
+        gift.seal(np.zeros(64, np.uint8), 1, 64, [(0, 1, 0, 0)], kt, nb, 0, 0)
+
+
+class _FakeCuda:
+    """Stands in for a CUDA tensor of n bytes at a fake address."""
+
+    is_cuda = True
+
+    def __init__(self, n, contiguous=True):
+        self.n, self.contiguous = n, contiguous
+
+    def data_ptr(self):
+        return 1 << 40
+
+    def is_contiguous(self):
+        return self.contiguous
+
+    def numel(self):
+        return self.n
+
+    def element_size(self):
+        return 1
+
+
+def test_binding_checks_device_buffer_sizes():
+    import types
+    kt = types.SimpleNamespace(handle=None, n_users=1)
+    nb = np.zeros(12, np.uint8)
+    segs = [(0, 1, 0, 0), (1, 1, 0, 1)]
+    ok = _FakeCuda(128)
+    with pytest.raises(ValueError, match="tags: 16 bytes, the call needs 32"):
+        gift.seal(ok, 2, 64, segs, kt, nb, ok, _FakeCuda(16))
+    with pytest.raises(ValueError, match="out: 100 bytes"):
+        gift.seal(ok, 2, 64, segs, kt, nb, _FakeCuda(100), ok)
+    with pytest.raises(ValueError, match="verdicts: 4 bytes"):
+        gift.open(ok, 2, 64, segs, kt, nb, ok, ok, _FakeCuda(4))
+    with pytest.raises(ValueError, match="row_labels: 4 bytes"):
+        gift.seal(ok, 2, 64, segs, kt, nb, ok, ok, row_labels=_FakeCuda(4))
+    with pytest.raises(ValueError, match="contiguous"):
+        gift.seal(ok, 2, 64, segs, kt, nb, _FakeCuda(128, contiguous=False), ok)
+    with pytest.raises(ValueError, match="nonces: 8 bytes"):
+        gift.token_encrypt(segs, _FakeCuda(16), _FakeCuda(8), 2, kt, 0, _FakeCuda(32))

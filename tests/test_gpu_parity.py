@@ -733,13 +733,17 @@ def test_one_block_over_the_limit_is_rejected(kt3):
     keys, nb, kt = kt3
     small = dev_u8(np.zeros(64, np.uint8))
     tags = torch.zeros(16, dtype=torch.uint8, device=DEV)
-    # 2^32 - 1 blocks: never touched, rejected on the host
-    # (the library trusts the declared tensor size, so only calls that the
-    # host rejects may describe more bytes than the buffer holds)
-    s = status_of(gift.seal, small, 1, 16 * ((1 << 32) - 1), [(0, 1, 0, 0)], kt, nb, small, tags)
+    # 2^32 - 1 blocks: never touched, rejected on the host.  The library
+    # trusts the declared tensor size, so only calls that the host rejects may
+    # describe more bytes than the buffer holds; raw addresses keep the
+    # binding's own size check out of the way of the C ABI's.
+    p, tp = small.data_ptr(), tags.data_ptr()
+    s = status_of(gift.seal, p, 1, 16 * ((1 << 32) - 1), [(0, 1, 0, 0)], kt, nb, p, tp)
     assert s == gift.E_TOO_LARGE
-    s = status_of(gift.seal, small, 3, 16 * ((1 << 31) - 1), [(0, 3, 0, 0)], kt, nb, small, tags)
+    s = status_of(gift.seal, p, 3, 16 * ((1 << 31) - 1), [(0, 3, 0, 0)], kt, nb, p, tp)
     assert s == gift.E_TOO_LARGE
+    with pytest.raises(ValueError, match="data: 64 bytes"):
+        gift.seal(small, 1, 16 * ((1 << 32) - 1), [(0, 1, 0, 0)], kt, nb, small, tags)
 
 
 def test_many_segments_and_users():
