@@ -112,10 +112,22 @@ def cpu_baseline(w, t, plain_dev, seconds_target=15.0, threads=None):
         "value": round(total / dt / 1e9, 6),
         "unit": "GB/s",
         "cores": threads,
+        "cpu": cpu_model(),
         "kind": "oracle",
         "sample": f"{n_jobs} segment prefixes of {chunk >> 20} MiB ({total / 2**20:.0f} MiB) of the same workload, "
                   f"one GCM message each, {threads} threads, {dt:.1f} s",
     }
+
+
+def cpu_model():
+    """The host CPU's model name (as lscpu reports it), for the CPU figures."""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def cpu_openssl(w, t, plain_dev, threads=None, max_bytes=4 << 30):
@@ -177,7 +189,7 @@ def cpu_openssl(w, t, plain_dev, threads=None, max_bytes=4 << 30):
             list(ex.map(run, jobs))
             times.append(time.perf_counter() - t0)
     dt = sorted(times)[len(times) // 2]
-    return {"value": round(total / dt / 1e9, 3), "unit": "GB/s", "cores": threads, "kind": "openssl-evp",
+    return {"value": round(total / dt / 1e9, 3), "unit": "GB/s", "cores": threads, "cpu": cpu_model(), "kind": "openssl-evp",
             "label": "optimized CPU reference (AES-NI / carry-less multiply), not the oracle",
             "sample": f"{len(jobs)} whole segments ({total / 2**30:.2f} GiB) of the same workload, median of 5 passes "
                       f"of {dt:.3f} s"}
