@@ -309,6 +309,64 @@ def test_random_multi_tile_tables_with_labels_and_tamper(kt3):
         assert host(back).tobytes() == o_back.tobytes(), (case, table)
 
 
+def test_one_tile_segments_cut_at_the_queue_tail(kt3):
+    # More one-tile segments than CUs, most longer than a 32-row piece: the
+    # largest tiles (up to one per CU) are cut into pieces at the tail of the
+    # work queue, their segments lose the one-tile path and get their tags and
+    # open verdicts from the finalize pass, next to uncut ones (short
+    # segments, and long ones beyond the CU count).  Fused owner check with
+    # two relabelled rows, then open with one ciphertext bit and one tag bit
+    # flipped; the references are per-segment oracle GCM messages.
+    keys, nb, kt = kt3
+    r = np.random.default_rng(77)
+    rb = 16384  # one tile row per tensor row
+    seg_rows = [int(x) for x in r.integers(33, 41, 260)] + [int(x) for x in r.integers(1, 5, 40)]
+    r.shuffle(seg_rows)
+    table, row = [], 0
+    for k, n in enumerate(seg_rows):
+        table.append((row, n, k % 3, 5000 + k))
+        row += n
+    n_rows = row + 2  # two uncovered rows at the end
+    n = len(table)
+    data = r.integers(0, 256, n_rows * rb, dtype=np.uint8)
+    labels = np.full(n_rows, 0xFFFFFFFF, np.uint32)
+    for (b, nr, u, _) in table:
+        labels[b:b + nr] = u
+    mixed = [int(x) for x in r.choice(n, 2, replace=False)]
+    for i in mixed:
+        b, nr, u, _ = table[i]
+        labels[b + int(r.integers(0, nr))] = (u + 1) % 3
+    segs = gift.as_segments(table)
+    ref = oracle_segments(keys, nb, segs, rb, lambda i: data[table[i][0] * rb:(table[i][0] + table[i][1]) * rb].tobytes())
+    exp_out = np.zeros(n_rows * rb, np.uint8)
+    exp_tags = np.zeros(16 * n, np.uint8)
+    for i, (b, nr, _, _) in enumerate(table):
+        if i not in mixed:
+            exp_out[b * rb:(b + nr) * rb] = np.frombuffer(ref[i][0], np.uint8)
+            exp_tags[16 * i:16 * i + 16] = np.frombuffer(ref[i][1], np.uint8)
+    out, tags, ver = seal(dev_u8(data), n_rows, rb, table, kt, nb, labels_dev=dev_u32(labels))
+    exp_ver = [gift.SEG_OWNER_MIXED if i in mixed else gift.SEG_OK for i in range(n)]
+    assert host(ver)[:n].tolist() == exp_ver
+    assert host(tags)[:16 * n].tobytes() == exp_tags.tobytes()
+    assert host(out).tobytes() == exp_out.tobytes()
+    # open, without labels, the sealed tensor with one ciphertext and one tag bit flipped
+    ok = [i for i in range(n) if i not in mixed and seg_rows[i] > 32]
+    i_ct, i_tg = [int(x) for x in r.choice(ok, 2, replace=False)]
+    ct = exp_out.copy()
+    b, nr, _, _ = table[i_ct]
+    ct[b * rb + int(r.integers(0, nr * rb))] ^= np.uint8(1 << int(r.integers(0, 8)))
+    tg = exp_tags.copy()
+    tg[16 * i_tg + int(r.integers(0, 16))] ^= np.uint8(1 << int(r.integers(0, 8)))
+    back, ver2 = open_(dev_u8(ct), n_rows, rb, table, kt, nb, dev_u8(tg))
+    bad = set(mixed) | {i_ct, i_tg}  # the mixed segments' zero tags do not verify either
+    assert host(ver2)[:n].tolist() == [gift.SEG_AUTH_FAIL if i in bad else gift.SEG_OK for i in range(n)]
+    exp_back = np.zeros(n_rows * rb, np.uint8)
+    for i, (b, nr, _, _) in enumerate(table):
+        if i not in bad:
+            exp_back[b * rb:(b + nr) * rb] = data[b * rb:(b + nr) * rb]
+    assert host(back).tobytes() == exp_back.tobytes()
+
+
 def test_wrong_key_table_fails_every_segment(kt3):
     keys, nb, kt = kt3
     keys2, _ = keyset(3)
