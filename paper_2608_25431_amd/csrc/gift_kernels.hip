@@ -499,21 +499,25 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
                 lane);
     }
     __syncthreads();
-    if (tid == 0) {
+    // wave 0 finishes the tile (fold, one and the row range are wave-uniform);
+    // lane 0 writes
+    if (wave == 0) {
       if (fold) {
         u128 p = red[0];
         for (int w = 1; w < kLeaders; w++) p = u128_xor(p, red[w]);
         if (r0 == 0 && r1 == kRows) {
-          if (!one) st_u128(a.partials + g, p);
+          if (!one && lane == 0) st_u128(a.partials + g, p);
         } else {
-          // a piece of a split tile: its lane powers assumed rows up to the
+          // a piece of a cut tile: its lane powers assumed rows up to the
           // tile's end, so it still carries H^(kThreads * (kRows - r1));
           // pieces meet in the tile's (zeroed) partial by XOR
-          if (r1 < kRows) p = gf_mul(p, ld_u128(a.kt.pow_hr + (size_t)user * kRows + (kRows - r1)));
-          uint32_t* dst = (uint32_t*)(a.partials + g);
-          for (int j = 0; j < 4; j++) atomicXor(dst + j, p.w[j]);
+          if (r1 < kRows) p = gf_mul_wave(p, ld_u128(a.kt.pow_hr + (size_t)user * kRows + (kRows - r1)), lane);
+          if (lane == 0) {
+            uint32_t* dst = (uint32_t*)(a.partials + g);
+            for (int j = 0; j < 4; j++) atomicXor(dst + j, p.w[j]);
+          }
         }
-        if (one) {
+        if (one && lane == 0) {
           // S = P_0 xor H*L, tag = E_K(J0) xor S (the finalize pass skips this segment)
           const u128 tag = u128_xor(p, red[kLeaders]);
           if (!OPEN) {
@@ -526,7 +530,7 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
             a.verdicts[s] = diff ? kVerdictAuthFail : kVerdictOk;
           }
         }
-      } else if (one && !OPEN) {
+      } else if (one && !OPEN && lane == 0) {
         uint32_t* to = (uint32_t*)(a.tags_out + 16ull * s);  // rejected: zero tag
         for (int j = 0; j < 4; j++) to[j] = 0u;
       }
