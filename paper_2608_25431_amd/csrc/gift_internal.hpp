@@ -103,7 +103,7 @@ struct GcmArgs {
   const uint32_t* tile_base;   // [n_segs + 1] first tile of each segment (small ones: 0 tiles)
   const uint32_t* small_list;  // [n_small] indices of small segments
   uint32_t n_tiles;
-  uint32_t n_ents;             // entries of the work queue (tiles, some split into pieces)
+  uint32_t n_ents;             // entries of the work queue (tiles, some cut into pieces)
   uint32_t n_small;
   uint32_t n_multi;            // segments of more than one tile (the finalize pass)
   uint4* partials;             // [n_tiles] GHASH partial of each tile

@@ -16,8 +16,9 @@
 // ends at distance (1023 - l) from the tile's end.  At tile end one leader
 // wave per SIMD folds the lane partials of four waves with LDS tables of
 // H^256 and applies the remaining per-lane power with one generic multiply,
-// while the other waves prefetch the next tile.  The tail of the work queue
-// cuts some tiles into row pieces, whose partials meet by XOR.
+// while the other waves prefetch the next tile.  The host cuts some tiles
+// into row pieces (every tile when a call has fewer tiles than CUs, else up
+// to one per CU at the queue's tail), whose partials meet by XOR.
 //
 // Around it: k_prologue (first kernel of a call: staged tables from pinned
 // host memory, owner check, E_K(J0) xor H*L of one-tile segments),
