@@ -64,7 +64,7 @@ uint32_t plan_cuts(SegDesc* descs, uint32_t n_segs, uint32_t n_tiles, uint32_t c
     piece = kPieceRows;
     std::vector<uint32_t> count(kRows + 1, 0);
     for (uint32_t g = 0; g < n_tiles; g++) count[rows[g]]++;
-    uint32_t left = cus, from = kRows + 1, take_at = 0;  // cut every tile of more than `from` rows...
+    uint32_t left = cus, from = kRows + 1, take_at = 0;  // cut every tile of at least `from` rows...
     for (uint32_t r = kRows; r > (uint32_t)kPieceRows && left; r--) {
       if (count[r] <= left) {
         left -= count[r];
