@@ -237,8 +237,12 @@ gift_status gift_seal_paged(const gift_paged_kv* kv, const gift_request* reqs, u
  * Open a contiguous sealed buffer (laid out as gift_seal_paged writes it)
  * into the paged cache: request i's plaintext is scattered into the chunks
  * of its block table (which may differ from the blocks it was sealed from,
- * e.g. on swap-in).  A request that fails authentication (AUTH_FAIL) or the
- * label check (OWNER_MIXED) has every chunk of its table zeroed.
+ * e.g. on swap-in).  A request that fails authentication (AUTH_FAIL) has
+ * every chunk of its table zeroed (its blocks passed the label check, so they
+ * are its own).  A request rejected by the label check (OWNER_MIXED) writes
+ * nothing into the cache: its table names a block of another owner, whose
+ * contents stay as they were, so a manipulated table shows only as this
+ * request's failure (Sec. 3, workflow step 3; Sec. 4.1, launch rejection).
  *   in        device, the sealed buffer; must not overlap the cache.
  *   tags      device, n_reqs*16 bytes.  verdicts: device, required.
  */

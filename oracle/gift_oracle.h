@@ -111,9 +111,10 @@ int oracle_check_owner(const oracle_segment* segs, uint32_t n_segs, const uint32
  * each part, in that order; it is one GCM message.  Seal writes request i's
  * ciphertext at out + (sum of earlier requests' lengths).  With
  * block_labels, a request holding a block labelled with anyone else is
- * rejected (zero ciphertext and tag on seal; on open its chunks are zeroed).
- * Open scatters verified plaintext into the table's chunks and zeroes the
- * chunks of failed requests.
+ * rejected: zero ciphertext and tag on seal; on open nothing is written
+ * into the cache (its table names another owner's block, which must keep
+ * its contents).  Open scatters verified plaintext into the table's chunks
+ * and zeroes the chunks of requests that fail authentication.
  * Validation: geometry (INVALID: chunk a power of two >= 16, strides multiples
  * of 16, counts >= 1, strided dimensions that do not overlap), then per
  * request in order: INVALID (empty table, sentinel user), RANGE (block id,

@@ -167,7 +167,11 @@ int oracle_open_paged(uint8_t* cache, const oracle_paged_kv* kv, const oracle_re
     const oracle_request* r = &reqs[i];
     uint64_t len = per_block * r->n_block_ids;
     if (request_mixed(r, block_labels)) {
-      scatter(cache, kv, r, NULL);
+      /* Rejected at launch (Sec. 4.1, malicious behaviour detection): the
+       * request's table names a block of another owner, so the open runs
+       * for none of its chunks and writes nothing -- that owner's block
+       * keeps its contents, and the manipulation shows only as this
+       * request's failure (Sec. 3, workflow step 3). */
       verdicts[i] = ORACLE_SEG_OWNER_MIXED;
     } else {
       uint8_t* msg = (uint8_t*)malloc(len);

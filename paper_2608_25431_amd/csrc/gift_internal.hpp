@@ -163,7 +163,7 @@ hipError_t launch_zero_ranges(uint8_t* out, const ZeroRange* r, uint32_t n, cons
                               hipStream_t s);
 hipError_t launch_wipe(void* p, size_t bytes, hipStream_t s);
 // Paged calls: chunk offsets from the block tables (segment rows index bids),
-// and zeroing of every chunk of segments whose verdict is not OK.
+// and zeroing of every chunk of segments whose verdict is AUTH_FAIL.
 hipError_t launch_chunk_table(const SegDesc* segs, uint32_t n_segs, const uint32_t* bids, uint32_t n_layers,
                               uint32_t n_parts, uint64_t layer_stride, uint64_t block_stride, uint64_t part_stride,
                               uint64_t* chunk_off, hipStream_t s);

@@ -399,13 +399,16 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
 
     u128 y = u128_zero();
     if (verdict != kVerdictOk) {
-      // rejected before this call's data is touched: release zeros only
-      for (int r = r_lo; r < r1; r++) {
-        const int64_t i0 = base + (int64_t)r * kThreads + tid;
-        if (i0 >= 0) {
-          const uint64_t rem = len - 16ull * (uint64_t)i0;
-          uint8_t* dst = SCATTER ? paged((uint64_t)i0) : a.out + off + 16ull * (uint64_t)i0;
-          store_block(dst, u128_zero(), rem >= 16 ? 16u : (uint32_t)rem, aligned);
+      // rejected before this call's data is touched: release zeros only.  A
+      // scatter into the cache writes nothing at all: the request's table
+      // names a block of another owner, which keeps its contents.
+      if (!SCATTER) {
+        for (int r = r_lo; r < r1; r++) {
+          const int64_t i0 = base + (int64_t)r * kThreads + tid;
+          if (i0 >= 0) {
+            const uint64_t rem = len - 16ull * (uint64_t)i0;
+            store_block(a.out + off + 16ull * (uint64_t)i0, u128_zero(), rem >= 16 ? 16u : (uint32_t)rem, aligned);
+          }
         }
       }
     } else {
@@ -811,9 +814,11 @@ __global__ __launch_bounds__(256) void k_chunk_table(const SegDesc* __restrict__
   }
 }
 
-// Open through block tables: zero the chunks of requests whose verdict is not
-// OK.  A workgroup takes whole tiles of kTileBlocks blocks (the GCM kernel's
-// tiles, found through tile_base), so the work per workgroup is bounded.
+// Open through block tables: zero the chunks of requests that failed
+// authentication (their blocks passed the label check, so they are the
+// request's own; a request rejected by the label check writes nothing).  A
+// workgroup takes whole tiles of kTileBlocks blocks (the GCM kernel's tiles,
+// found through tile_base), so the work per workgroup is bounded.
 __global__ __launch_bounds__(256) void k_zero_chunks(const SegDesc* __restrict__ segs, uint32_t n,
                                                      const uint32_t* __restrict__ tile_base, uint32_t n_tiles,
                                                      const int32_t* __restrict__ verdicts,
@@ -829,7 +834,7 @@ __global__ __launch_bounds__(256) void k_zero_chunks(const SegDesc* __restrict__
       else
         hi = mid;
     }
-    if (verdicts[lo] == kVerdictOk) continue;
+    if (verdicts[lo] != kVerdictAuthFail) continue;
     const uint64_t m = segs[lo].nblocks, c0 = segs[lo].chunk0;
     const uint64_t t = g - tile_base[lo];
     // tiles are aligned to the end of the segment, as in k_gcm_tiles

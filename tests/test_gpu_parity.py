@@ -904,7 +904,18 @@ def dev_kv(g, cache_dev):
                          g.n_layers, g.n_parts, g.n_blocks)
 
 
-def paged_case(keys, nb, kt, g, reqs, moved=None, labels=None, tamper=None):
+def gather_blocks(cache, g, bids):
+    """The bytes of the given blocks, every layer and part, from a host copy."""
+    out = []
+    for b in bids:
+        for l in range(g.n_layers):
+            for p in range(g.n_parts):
+                o = l * g.layer_stride + int(b) * g.block_stride + p * g.part_stride
+                out.append(cache[o:o + g.chunk_bytes].tobytes())
+    return b"".join(out)
+
+
+def paged_case(keys, nb, kt, g, reqs, moved=None, labels=None, tamper=None, want_cache=False):
     cache = rng.integers(0, 256, g.cache_bytes, dtype=np.uint8)
     st, o_sealed, o_tags, o_ver = oracle.seal_paged(cache, g, reqs, keys, nb, labels=labels)
     assert st == 0
@@ -930,7 +941,10 @@ def paged_case(keys, nb, kt, g, reqs, moved=None, labels=None, tamper=None):
     ver2 = torch.full((n,), -1, dtype=torch.int32, device=DEV)
     gift.open_paged(kv, dst, kt, nb, sealed, tags, ver2, block_labels=lab)
     assert host(ver2).tolist() == o_ver2.tolist()
-    assert host(c_dev).tobytes() == o_after.tobytes()
+    after = host(c_dev)
+    assert after.tobytes() == o_after.tobytes()
+    if want_cache:
+        return o_ver, o_ver2, cache, after
     return o_ver, o_ver2
 
 
@@ -982,8 +996,12 @@ def test_paged_manipulated_table_and_tamper(kt3):
         labels[reqs[0][0][0]] = (reqs[1][1] + 1) % 3
     evil[1] = (np.concatenate([reqs[1][0], reqs[0][0][:1]]), reqs[1][1], reqs[1][2])
     evil[0] = (reqs[0][0][1:], reqs[0][1], reqs[0][2])
-    ver, ver2 = paged_case(keys, nb, kt, g, evil, labels=labels)
+    ver, ver2, before, after = paged_case(keys, nb, kt, g, evil, labels=labels, want_cache=True)
     assert ver[1] == gift.SEG_OWNER_MIXED and ver2[1] == gift.SEG_OWNER_MIXED
+    # the rejected open wrote nothing: the foreign block named by the
+    # manipulated table, and the request's own blocks, keep their contents
+    for b in evil[1][0]:
+        assert gather_blocks(after, g, [b]) == gather_blocks(before, g, [b]), f"block {b}" 
     # a flipped ciphertext bit in request 2 fails it and zeroes its blocks
     per = g.n_layers * g.n_parts * g.chunk_bytes
     off = per * (len(reqs[0][0]) + len(reqs[1][0])) + 77

@@ -98,6 +98,24 @@ def test_manipulated_block_table_is_rejected_by_labels():
     assert oracle.seal_paged(cache, g, honest, keys, nb, labels=l2)[3].tolist() == [oracle.SEG_OWNER_MIXED, 0]
 
 
+def test_open_with_a_manipulated_table_writes_nothing():
+    # user 1's table on open names user 0's resident block 9: the request is
+    # rejected before anything runs, so block 9 (and user 1's own blocks)
+    # keep their contents; only the honest request is opened
+    g = geom()
+    keys, nb, cache = setup(g)
+    labels = np.array([0, 0, 1, 1, 2, 2, 0, 1, 2, 0], np.uint32)
+    honest = [([0, 1, 6], 0, 1), ([2, 3], 1, 1)]
+    _, sealed, tags, _ = oracle.seal_paged(cache, g, honest, keys, nb, labels=labels)
+    resident = np.random.default_rng(3).integers(0, 256, cache.size, dtype=np.uint8)
+    evil = [([0, 1, 6], 0, 1), ([2, 9], 1, 1)]
+    st, after, ver = oracle.open_paged(resident, g, evil, keys, nb, sealed, tags, labels=labels)
+    assert st == 0 and ver.tolist() == [0, oracle.SEG_OWNER_MIXED]
+    for b in (2, 3, 9):
+        assert gather_np(after, g, [b]).tobytes() == gather_np(resident, g, [b]).tobytes()
+    assert gather_np(after, g, [0, 1, 6]).tobytes() == gather_np(cache, g, [0, 1, 6]).tobytes()
+
+
 def test_tampered_request_fails_and_its_blocks_are_zeroed():
     g = geom()
     keys, nb, cache = setup(g)
