@@ -11,7 +11,7 @@ LIB = os.path.join(HERE, "liboracle.so")
 
 
 def build(verbose: bool = False) -> str:
-    cmd = ["gcc", "-std=c99", "-O2", "-Wall", "-Wextra", "-fPIC", "-shared", "-pthread",
+    cmd = ["gcc", "-std=c99", "-O3", "-Wall", "-Wextra", "-fPIC", "-shared", "-pthread",
            "-o", LIB + ".tmp"] + [os.path.join(HERE, s) for s in SOURCES]
     if verbose:
         print(" ".join(cmd))

@@ -10,7 +10,10 @@ import oracle
 from paper_2608_25431_amd import gift
 
 DEV = "cuda"
-THREADS = min(16, os.cpu_count() or 4)
+# worker threads for the oracle: the cores this process may run on, at most
+# the 16-core share of one GPU on the test hosts
+CORES = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else (os.cpu_count() or 4)
+THREADS = max(1, min(16, CORES))
 
 
 def dev_u8(a):
