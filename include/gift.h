@@ -156,6 +156,30 @@ gift_status gift_seal(const gift_tensor* t, const gift_segment_table* st, gift_k
                       const uint8_t* nonce_base, void* out, uint8_t* tags, hipStream_t stream);
 
 /*
+ * gift_seal for callers that cannot allocate device memory: code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc.  Same
+ * arguments, semantics, validation and outputs as gift_seal, but it calls no
+ * hipMalloc, hipFree, hipHostMalloc or hipEventCreate: its device workspace
+ * is a fixed array of GIFT_NOALLOC_WORKSPACE_BYTES in the library's code
+ * object, one per device (held until the process ends), and its tables go
+ * through a staging ring allocated up front.  Both are set up by
+ * gift_key_table_create on the key table's device, so a key table must have
+ * been created on the current device first.
+ *   Limit: the call's workspace (64 B per segment, 16 B per 2 MiB tile and per
+ *   queue entry, 32 B per zero range and 4 MiB of uncovered rows, ...) must
+ *   fit GIFT_NOALLOC_WORKSPACE_BYTES, and its staged tables half of that;
+ *   otherwise it returns GIFT_E_NOMEM before enqueuing anything.  The
+ *   benchmark workloads need at most about 1 MiB.
+ *   Every call on a device shares that device's workspace and leaves its
+ *   contents there; each call sets what must start at zero itself.  Calls
+ *   ordered on one stream are safe; calls that overlap on one device (other
+ *   streams, or host threads on different streams) race on the workspace.
+ */
+#define GIFT_NOALLOC_WORKSPACE_BYTES (8u << 20)
+gift_status gift_seal_noalloc(const gift_tensor* t, const gift_segment_table* st, gift_key_table kt,
+                              const uint8_t* nonce_base, void* out, uint8_t* tags, hipStream_t stream);
+
+/*
  * Open (verify + decrypt) each segment of the sealed tensor `t`.  A segment
  * whose tag does not verify -- wrong key, wrong user, wrong iv_seq, moved or
  * modified ciphertext or tag -- gets verdict AUTH_FAIL and zero bytes in

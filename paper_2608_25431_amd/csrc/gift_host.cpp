@@ -198,15 +198,39 @@ int device_cus(int dev) {
 // completed.
 class Staging {
  public:
+  static constexpr size_t kCap = 8u << 20;
+  static constexpr size_t kMaxStaged = kCap / 2;  // larger tables take a private synchronous path
+
+  // Allocates the ring and a pool of kEvents events, once; the key-table
+  // constructor calls it, so a call that may not allocate finds them ready.
+  hipError_t prepare() {
+    std::lock_guard<std::mutex> g(mu_);
+    hipError_t e = ring();
+    while (e == hipSuccess && n_events_ < kEvents) {
+      hipEvent_t ev;
+      e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
+      if (e == hipSuccess) {
+        free_ev_.push_back(ev);
+        n_events_++;
+      }
+    }
+    return e;
+  }
+
   // Copies bytes into the ring, then consume(src) enqueues on s the kernel
   // that reads them: src is the copy's device address, or nullptr when the
   // bytes were DMA-copied to dst instead (no device address for the ring, or
-  // a table too large for it).
+  // a table too large for it).  With no_alloc the call creates nothing: it
+  // needs a prepared ring with a device address and at most kMaxStaged
+  // bytes, and when every pooled event is in flight it waits for the oldest
+  // slot and takes its event.
   template <class F>
-  hipError_t upload(void* dst, const void* src, size_t bytes, hipStream_t s, F&& consume) {
+  hipError_t upload(void* dst, const void* src, size_t bytes, hipStream_t s, F&& consume, bool no_alloc = false) {
     std::lock_guard<std::mutex> g(mu_);
     if (bytes == 0) return consume((const void*)nullptr);
-    if (bytes > kCap / 2) {  // rare: very large tables take a private synchronous path
+    if (no_alloc && (base_ == nullptr || dbase_ == nullptr || bytes > kMaxStaged || (bytes & 15u)))
+      return hipErrorNotInitialized;
+    if (bytes > kMaxStaged) {  // rare: very large tables take a private synchronous path
       void* tmp = nullptr;
       hipError_t e = hipHostMalloc(&tmp, bytes, hipHostMallocDefault);
       if (e != hipSuccess) return e;
@@ -218,12 +242,8 @@ class Staging {
       return e != hipSuccess ? e : consume((const void*)nullptr);
     }
     if (base_ == nullptr) {
-      hipError_t e = hipHostMalloc((void**)&base_, kCap, hipHostMallocMapped);
-      if (e != hipSuccess) {
-        base_ = nullptr;
-        return e;
-      }
-      if (hipHostGetDevicePointer((void**)&dbase_, base_, 0) != hipSuccess) dbase_ = nullptr;
+      hipError_t e = ring();
+      if (e != hipSuccess) return e;
     }
     size_t need = (bytes + 255) & ~(size_t)255;
     if (head_ + need > kCap) head_ = 0;
@@ -253,10 +273,24 @@ class Staging {
       return e;
     }
     hipEvent_t ev;
+    if (free_ev_.empty() && no_alloc && !live_.empty()) {
+      // every pooled event is in flight: the oldest slot's event is the next free
+      e = hipEventSynchronize(live_.front().ev);
+      if (e != hipSuccess) {
+        (void)hipStreamSynchronize(s);
+        return e;
+      }
+      free_ev_.push_back(live_.front().ev);
+      live_.pop_front();
+    }
     if (!free_ev_.empty()) {
       ev = free_ev_.back();
       free_ev_.pop_back();
+    } else if (no_alloc) {
+      (void)hipStreamSynchronize(s);
+      return hipErrorNotInitialized;
     } else {
+      n_events_++;
       e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
       if (e != hipSuccess) {
         (void)hipStreamSynchronize(s);
@@ -275,7 +309,18 @@ class Staging {
   }
 
  private:
-  static constexpr size_t kCap = 8u << 20;
+  static constexpr int kEvents = 64;
+  // the pinned, mapped ring and its device address (mu_ held)
+  hipError_t ring() {
+    if (base_ != nullptr) return hipSuccess;
+    hipError_t e = hipHostMalloc((void**)&base_, kCap, hipHostMallocMapped);
+    if (e != hipSuccess) {
+      base_ = nullptr;
+      return e;
+    }
+    if (hipHostGetDevicePointer((void**)&dbase_, base_, 0) != hipSuccess) dbase_ = nullptr;
+    return hipSuccess;
+  }
   struct Slot {
     size_t off, len;
     hipEvent_t ev;
@@ -287,6 +332,7 @@ class Staging {
   size_t head_ = 0;
   std::deque<Slot> live_;  // in allocation order
   std::vector<hipEvent_t> free_ev_;
+  int n_events_ = 0;  // events created so far
 };
 
 Staging* staging_for(int dev) {
@@ -601,9 +647,12 @@ gift_status current_device(int* dev) {
   return GIFT_OK;
 }
 
+// no_alloc: the call's scratch is the device's fixed workspace
+// (static_scratch) instead of a leased buffer, and its tables go through the
+// prepared staging ring; nothing is allocated or created.
 template <bool OPEN>
 gift_status run_gcm(const gift_tensor* t, const gift_segment_table* st, gift_key_table kt, const uint8_t* nonce_base,
-                    void* out, uint8_t* tags_out, const uint8_t* tags_in, hipStream_t stream) {
+                    void* out, uint8_t* tags_out, const uint8_t* tags_in, hipStream_t stream, bool no_alloc = false) {
   g_last_error.clear();
   if (!t || !st || !kt) return fail(GIFT_E_INVALID, "null tensor, segment table or key table");
   const uint32_t n = st->n_segs;
@@ -648,9 +697,21 @@ gift_status run_gcm(const gift_tensor* t, const gift_segment_table* st, gift_key
   const size_t o_fn = o_vd + align256(4ull * (n ? n : 1));
   const size_t bytes = o_fn + align256(16ull * (n ? n : 1));
   ScratchLease lease;
-  hipError_t e = lease.acquire(dev, stream, bytes);
-  if (e != hipSuccess) return hip_fail(e, "device scratch");
-  uint8_t* scratch = lease.ptr;
+  uint8_t* scratch = nullptr;
+  hipError_t e = hipSuccess;
+  if (no_alloc) {
+    if (bytes > kStaticScratchBytes || o_pt > Staging::kMaxStaged)
+      return fail(GIFT_E_NOMEM,
+                  "gift_seal_noalloc: the call needs %zu bytes of workspace (%zu of them staged tables); the fixed "
+                  "workspace holds %zu (%zu staged)",
+                  bytes, o_pt, kStaticScratchBytes, Staging::kMaxStaged);
+    scratch = static_scratch(dev);
+    if (!scratch) return fail(GIFT_E_INVALID, "gift_seal_noalloc: no workspace on device %d (create a key table there first)", dev);
+  } else {
+    e = lease.acquire(dev, stream, bytes);
+    if (e != hipSuccess) return hip_fail(e, "device scratch");
+    scratch = lease.ptr;
+  }
 
   std::vector<uint8_t> host(o_pt);  // zero-filled: the queue head starts at 0
   if (n) memcpy(host.data() + o_desc, P.descs.data(), sizeof(SegDesc) * n);
@@ -662,10 +723,13 @@ gift_status run_gcm(const gift_tensor* t, const gift_segment_table* st, gift_key
   Staging* sg = staging_for(dev);
   if (!sg) return fail(GIFT_E_INVALID, "device index %d unsupported", dev);
   // the prologue copies the tables and settles the verdicts (owner check)
-  e = sg->upload(scratch, host.data(), o_pt, stream, [&](const void* src) {
-    return launch_prologue(scratch, src, o_pt, n, kNoBids, st->row_labels, n ? verdicts : nullptr, &kt->dev,
-                           (uint4*)(scratch + o_fn), (uint4*)(scratch + o_pt), pieces ? P.n_tiles : 0u, stream);
-  });
+  e = sg->upload(
+      scratch, host.data(), o_pt, stream,
+      [&](const void* src) {
+        return launch_prologue(scratch, src, o_pt, n, kNoBids, st->row_labels, n ? verdicts : nullptr, &kt->dev,
+                               (uint4*)(scratch + o_fn), (uint4*)(scratch + o_pt), pieces ? P.n_tiles : 0u, stream);
+      },
+      no_alloc);
   if (e != hipSuccess) return hip_fail(e, "staging upload");
 
   const SegDesc* d_desc = (const SegDesc*)(scratch + o_desc);
@@ -1057,6 +1121,13 @@ gift_status gift_key_table_create(const uint8_t* keys, uint32_t n_users, hipStre
   hipError_t e2 = hipStreamSynchronize(stream);
   (void)hipFree(kdev);
   if (e == hipSuccess) e = e2;
+  // set-up of this device for gift_seal_noalloc: the fixed workspace's
+  // address and the staging ring with its event pool
+  if (e == hipSuccess) e = static_scratch_setup(dev);
+  if (e == hipSuccess) {
+    Staging* sg = staging_for(dev);
+    e = sg ? sg->prepare() : hipErrorInvalidDevice;
+  }
   if (e != hipSuccess) {
     (void)hipFree(mem);
     delete kt;
@@ -1086,6 +1157,11 @@ gift_status gift_key_table_destroy(gift_key_table kt) {
 gift_status gift_seal(const gift_tensor* t, const gift_segment_table* st, gift_key_table kt, const uint8_t* nonce_base,
                       void* out, uint8_t* tags, hipStream_t stream) {
   return run_gcm<false>(t, st, kt, nonce_base, out, tags, nullptr, stream);
+}
+
+gift_status gift_seal_noalloc(const gift_tensor* t, const gift_segment_table* st, gift_key_table kt,
+                              const uint8_t* nonce_base, void* out, uint8_t* tags, hipStream_t stream) {
+  return run_gcm<false>(t, st, kt, nonce_base, out, tags, nullptr, stream, true);
 }
 
 gift_status gift_open(const gift_tensor* t, const gift_segment_table* st, gift_key_table kt, const uint8_t* nonce_base,

@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "gift.h"
+
 namespace gift {
 
 // Work decomposition of the per-block kernel: one workgroup per CU (its LDS
@@ -115,6 +117,16 @@ struct GcmArgs {
   const uint8_t* tags_in;      // open: [n_segs][16]
   KeyTableDev kt;
 };
+
+// Fixed per-device workspace of gift_seal_noalloc (gift_kernels.hip): a
+// __device__ array of kStaticScratchBytes in the library's code object.
+// static_scratch_setup(dev) looks up its address on device dev, which must be
+// current, once (the key-table constructor calls it); static_scratch(dev)
+// returns that address, or nullptr before set-up.
+constexpr size_t kStaticScratchBytes = GIFT_NOALLOC_WORKSPACE_BYTES;
+constexpr int kStaticScratchDevices = 64;
+hipError_t static_scratch_setup(int dev);
+uint8_t* static_scratch(int dev);
 
 // Launch wrappers (gift_kernels.hip).  All enqueue on `s` and return the
 // launch status.

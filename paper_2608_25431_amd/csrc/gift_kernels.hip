@@ -26,6 +26,8 @@
 // zero-fill, the paged-call helpers, per-token encryption and key setup.
 #include <hip/hip_runtime.h>
 
+#include <mutex>
+
 #include "gift_device.hpp"
 #include "gift_internal.hpp"
 
@@ -1022,6 +1024,35 @@ hipError_t launch_prologue(void* dst, const void* src, size_t bytes, uint32_t n_
                      bids_off == kNoBids ? (const uint32_t*)nullptr : (const uint32_t*)(rd + bids_off), verdicts,
                      kt ? *kt : KeyTableDev{}, kt ? fin : nullptr, zero, n_zero);
   return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Fixed workspace of gift_seal_noalloc.  Each device holds its own copy of
+// the array at its own address; host code never uses the array's name (a
+// host-side stand-in), only the address hipGetSymbolAddress gives for the
+// current device, looked up once per device at set-up.
+// ---------------------------------------------------------------------------
+static __device__ __align__(256) uint8_t scratch[kStaticScratchBytes];
+
+static std::mutex g_scratch_mu;
+static uint8_t* g_scratch_addr[kStaticScratchDevices] = {nullptr};
+
+hipError_t static_scratch_setup(int dev) {
+  if (dev < 0 || dev >= kStaticScratchDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> g(g_scratch_mu);
+  if (g_scratch_addr[dev]) return hipSuccess;
+  void* ptr = nullptr;
+  const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+  if (e != hipSuccess) return e;
+  if (ptr == nullptr || ((uintptr_t)ptr & 255u)) return hipErrorInvalidSymbol;
+  g_scratch_addr[dev] = (uint8_t*)ptr;
+  return hipSuccess;
+}
+
+uint8_t* static_scratch(int dev) {
+  if (dev < 0 || dev >= kStaticScratchDevices) return nullptr;
+  std::lock_guard<std::mutex> g(g_scratch_mu);
+  return g_scratch_addr[dev];
 }
 
 hipError_t launch_wipe(void* p, size_t bytes, hipStream_t s) {

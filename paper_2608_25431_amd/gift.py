@@ -64,7 +64,8 @@ class _Request(ctypes.Structure):
 
 assert ctypes.sizeof(_Segment) == SEGMENT_DTYPE.itemsize == 32
 
-EXPORTS = ("gift_key_table_create", "gift_key_table_users", "gift_key_table_destroy", "gift_seal", "gift_open",
+EXPORTS = ("gift_key_table_create", "gift_key_table_users", "gift_key_table_destroy", "gift_seal", "gift_seal_noalloc",
+           "gift_open",
            "gift_check_owner", "gift_seal_paged", "gift_open_paged", "gift_token_encrypt", "gift_token_decrypt", "gift_profile_next_call",
            "gift_status_string", "gift_last_error",
            # include/gift_ift.h
@@ -94,6 +95,8 @@ def lib():
         L.gift_key_table_destroy.restype = st
         L.gift_seal.argtypes = [ctypes.POINTER(_Tensor), ctypes.POINTER(_SegTable), P, P, P, P, P]
         L.gift_seal.restype = st
+        L.gift_seal_noalloc.argtypes = [ctypes.POINTER(_Tensor), ctypes.POINTER(_SegTable), P, P, P, P, P]
+        L.gift_seal_noalloc.restype = st
         L.gift_open.argtypes = [ctypes.POINTER(_Tensor), ctypes.POINTER(_SegTable), P, P, P, P, P]
         L.gift_open.restype = st
         L.gift_check_owner.argtypes = [ctypes.POINTER(_SegTable), P, ctypes.c_uint64, P]
@@ -273,6 +276,20 @@ def seal(data, n_rows, row_bytes, segs, kt, nonce_base, out, tags, row_labels=No
     o, tg = _dev(out, total, "out"), _dev(tags, 16 * len(keep), "tags")
     nb = _nonce(nonce_base, kt)
     _check(lib().gift_seal(ctypes.byref(t), ctypes.byref(tab), kt.handle, nb.ctypes.data, o, tg, _stream(stream)))
+    del keep
+
+
+def seal_noalloc(data, n_rows, row_bytes, segs, kt, nonce_base, out, tags, row_labels=None, verdicts=None,
+                 stream=None):
+    """gift_seal_noalloc: gift_seal on the device's fixed workspace (no
+    device allocation; calls that overlap on one device race)."""
+    total = n_rows * row_bytes
+    t = _Tensor(_dev(data, total, "data"), n_rows, row_bytes)
+    tab, keep = _table(segs, row_labels, verdicts, n_rows)
+    o, tg = _dev(out, total, "out"), _dev(tags, 16 * len(keep), "tags")
+    nb = _nonce(nonce_base, kt)
+    _check(lib().gift_seal_noalloc(ctypes.byref(t), ctypes.byref(tab), kt.handle, nb.ctypes.data, o, tg,
+                                   _stream(stream)))
     del keep
 
 
