@@ -34,116 +34,67 @@ uint32_t tile_rows(uint64_t m, uint32_t t) {
 
 uint32_t tiles_of(const SegDesc& d) { return (uint32_t)(((uint64_t)d.nblocks + kTileBlocks - 1) / kTileBlocks); }
 
+size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
+
 }  // namespace
 
-uint32_t plan_cuts(SegDesc* descs, uint32_t n_segs, uint32_t n_tiles, uint32_t cus, uint32_t* n_multi,
-                   uint8_t* cut) {
-  static_assert(kRows % kPieceRows == 0 && kPieceRows > 0 && kRows < 256, "pieces of a tile");
-  if (n_tiles == 0 || cus == 0) return 0;
-  std::vector<uint32_t> rows(n_tiles);
-  std::vector<uint32_t> seg(n_tiles);
-  uint64_t total = 0;
-  for (uint32_t i = 0, g = 0; i < n_segs; i++) {
-    if (descs[i].flags & kSegSmall) continue;
-    const uint32_t nt = tiles_of(descs[i]);
-    for (uint32_t t = 0; t < nt; t++, g++) {
-      rows[g] = tile_rows(descs[i].nblocks, t);
-      seg[g] = i;
-      total += rows[g];
-    }
-  }
-  uint32_t piece = 0;
-  memset(cut, 0, n_tiles);
-  if (n_tiles < cus) {
-    piece = (uint32_t)((total + cus - 1) / cus);
-    if (piece >= (uint32_t)kRows) return 0;  // (not reached while n_tiles < cus)
-    for (uint32_t g = 0; g < n_tiles; g++) cut[g] = rows[g] > piece;
-  } else {
-    // the queue's tail: up to cus of the largest tiles, in tile order
-    // within a row count
-    piece = kPieceRows;
-    std::vector<uint32_t> count(kRows + 1, 0);
-    for (uint32_t g = 0; g < n_tiles; g++) count[rows[g]]++;
-    uint32_t left = cus, from = kRows + 1, take_at = 0;  // cut every tile of at least `from` rows...
-    for (uint32_t r = kRows; r > (uint32_t)kPieceRows && left; r--) {
-      if (count[r] <= left) {
-        left -= count[r];
-        from = r;
-      } else {
-        take_at = r;  // ...and the first `left` tiles of `take_at` rows
-        break;
-      }
-    }
-    for (uint32_t g = 0; g < n_tiles; g++) {
-      if (rows[g] >= from) {
-        cut[g] = 1;
-      } else if (rows[g] == take_at && left) {
-        cut[g] = 1;
-        left--;
-      }
-    }
-  }
-  uint32_t n_cut = 0;
-  for (uint32_t g = 0; g < n_tiles; g++) {
-    if (!cut[g]) continue;
-    n_cut++;
-    SegDesc& d = descs[seg[g]];
-    if (d.flags & kSegOneTile) {
-      d.flags &= ~kSegOneTile;
-      (*n_multi)++;
-    }
-  }
-  return n_cut ? piece : 0;
+// What the host decides for a call's launches, from per-segment counts only
+// (the tile tables and the work queue are built on the device by
+// launch_expand): the queue's capacity, the tile kernel's grid and whether
+// the finalize pass may have work.
+struct QueuePlan {
+  uint64_t cap = 0;
+  uint32_t grid = 0;
+  bool finalize = false;
+};
+
+QueuePlan plan_queue(uint32_t n_tiles, uint64_t tile_rows_all, uint32_t n_multi, uint32_t one_rows_max, uint32_t cus) {
+  QueuePlan q;
+  if (n_tiles == 0 || cus == 0) return q;
+  q.cap = queue_capacity(n_tiles, cus);
+  // the expansion kernel's cut: with fewer tiles than CUs, tiles of more than
+  // ceil(rows / cus) rows; otherwise tiles of more than kPieceRows rows at most
+  const bool fine = n_tiles < cus;
+  const uint64_t p = fine ? (tile_rows_all + cus - 1) / cus : (uint64_t)kPieceRows;
+  const uint64_t cut_above = (fine && p >= (uint64_t)kRows) ? (uint64_t)kRows : p;
+  // every entry runs at least one row, so entries <= rows; extra workgroups
+  // find no entry and leave
+  q.grid = fine ? (uint32_t)std::min<uint64_t>(cus, tile_rows_all) : cus;
+  q.finalize = n_multi > 0 || (uint64_t)one_rows_max > cut_above;
+  return q;
 }
 
-// Longest entries first, so that a work queue over them ends with short
-// work: a counting sort by the number of rows each entry runs.
-uint32_t tile_order(const SegDesc* descs, uint32_t n_segs, uint32_t rows, const uint8_t* cut, TileEnt* order) {
-  auto pack = [](uint32_t t, uint32_t r0, uint32_t r1) { return t | (r0 << 16) | (r1 << 24); };
-  std::vector<std::pair<uint32_t, TileEnt>> ents;  // (rows run, entry) in tile order
-  uint32_t g = 0;
-  for (uint32_t i = 0; i < n_segs; i++) {
-    if (descs[i].flags & kSegSmall) continue;
-    const uint32_t nt = tiles_of(descs[i]), user = descs[i].user;
-    for (uint32_t t = 0; t < nt; t++, g++) {
-      const uint32_t r = tile_rows(descs[i].nblocks, t), lo = (uint32_t)kRows - r;
-      if (cut[g] && rows) {
-        // pieces [r1 - rows, r1) from the tile's end down; the lowest may
-        // start below the tile's first row, which the kernel skips
-        for (uint32_t r1 = kRows; r1 > lo; r1 -= std::min(r1, rows)) {
-          const uint32_t r0 = r1 > rows ? r1 - rows : 0u;
-          ents.push_back({r1 - std::max(r0, lo), TileEnt{g, i, pack(t, r0, r1), user}});
-        }
-      } else {
-        ents.push_back({r, TileEnt{g, i, pack(t, 0, kRows), user}});
-      }
-    }
-  }
-  // start of each row count's run, longest first
-  std::vector<uint32_t> pos(kRows + 1, 0);
-  for (const auto& e : ents) pos[e.first]++;
-  uint32_t acc = 0;
-  for (int r = kRows; r >= 0; r--) {
-    const uint32_t c = pos[r];
-    pos[r] = acc;
-    acc += c;
-  }
-  for (const auto& e : ents) order[pos[e.first]++] = e.second;
-  return (uint32_t)ents.size();
-}
-
-// tile_base (n + 1 entries: first tile of each segment; small segments have
-// none) and the list of small segments, as the kernels read them.
-void tile_tables(const SegDesc* descs, uint32_t n, uint32_t* tile_base, uint32_t* small_list) {
-  uint32_t t = 0, k = 0;
-  for (uint32_t i = 0; i < n; i++) {
-    tile_base[i] = t;
-    if (descs[i].flags & kSegSmall)
-      small_list[k++] = i;
-    else
-      t += (uint32_t)(((uint64_t)descs[i].nblocks + kTileBlocks - 1) / kTileBlocks);
-  }
-  tile_base[n] = t;
+// Test hook, not part of the C ABI: runs the expansion kernel on host
+// descriptors and copies its tables back (seg_cut[n], tile_base[n + 1],
+// small list[n], cap queue entries and their count).  Synchronous; it
+// allocates device buffers of its own.
+int expand_for_test(const SegDesc* descs, uint32_t n, uint32_t cus, uint32_t* seg_cut, uint32_t* tile_base,
+                    uint32_t* small_list, TileEnt* order, uint32_t cap, uint32_t* n_ents) {
+  if (n == 0) return (int)hipErrorInvalidValue;
+  std::vector<SegBrief> brief(n + 1);  // an even count: the kernel reads them two at a time
+  for (uint32_t i = 0; i < n; i++) brief[i] = SegBrief{descs[i].nblocks, descs[i].user};
+  const size_t o_tb = align_up(sizeof(SegBrief) * (n + 1)), o_sl = o_tb + align_up(4ull * (n + 1)),
+               o_si = o_sl + align_up(4ull * n), o_sc = o_si + align_up(sizeof(SegInfo) * n),
+               o_to = o_sc + align_up(4ull * n), o_ne = o_to + align_up(sizeof(TileEnt) * (cap ? cap : 1)),
+               bytes = o_ne + 256;
+  uint8_t* m = nullptr;
+  hipError_t e = hipMalloc((void**)&m, bytes);
+  if (e != hipSuccess) return (int)e;
+  e = hipMemset(m, 0, bytes);
+  if (e == hipSuccess) e = hipMemcpy(m, brief.data(), sizeof(SegBrief) * (n + 1), hipMemcpyHostToDevice);
+  if (e == hipSuccess)
+    e = launch_expand((const SegBrief*)m, n,
+                      ExpandArgs{(uint32_t*)(m + o_tb), (uint32_t*)(m + o_sl), (TileEnt*)(m + o_to), cap, cus,
+                                 (uint32_t*)(m + o_ne), (SegInfo*)(m + o_si), (uint32_t*)(m + o_sc), kSmallMaxBlocks},
+                      nullptr);
+  if (e == hipSuccess) e = hipDeviceSynchronize();
+  if (e == hipSuccess) e = hipMemcpy(seg_cut, m + o_sc, 4ull * n, hipMemcpyDeviceToHost);
+  if (e == hipSuccess) e = hipMemcpy(tile_base, m + o_tb, 4ull * (n + 1), hipMemcpyDeviceToHost);
+  if (e == hipSuccess) e = hipMemcpy(small_list, m + o_sl, 4ull * n, hipMemcpyDeviceToHost);
+  if (e == hipSuccess && cap) e = hipMemcpy(order, m + o_to, sizeof(TileEnt) * cap, hipMemcpyDeviceToHost);
+  if (e == hipSuccess) e = hipMemcpy(n_ents, m + o_ne, 4, hipMemcpyDeviceToHost);
+  hipError_t e2 = hipFree(m);
+  return (int)(e != hipSuccess ? e : e2);
 }
 
 }  // namespace gift
@@ -526,10 +477,12 @@ class ScratchLease {
 
 struct Plan {
   std::vector<SegDesc> descs;
-  std::vector<ZeroRange> zr;
+  std::vector<ZeroRange> zr;  // rows no segment covers
   uint32_t n_tiles = 0;
   uint32_t n_small = 0;
-  uint32_t n_multi = 0;
+  uint32_t n_multi = 0;        // segments of more than one tile
+  uint64_t tile_rows = 0;      // tile rows of all tiles
+  uint32_t one_rows_max = 0;   // most tile rows of a one-tile segment
 };
 
 enum class Check { kOwner, kGcm, kBlock };
@@ -585,10 +538,9 @@ gift_status check_segments(const gift_segment* segs, uint32_t n, uint64_t n_rows
   return GIFT_OK;
 }
 
-// Descriptors, zero ranges (uncovered rows; for open also every tiled
-// segment, zeroed only when its verdict is not OK) and work counts.
+// Descriptors, zero ranges of uncovered rows, and per-segment work counts.
 void build_plan(const gift_segment* segs, uint32_t n, uint64_t n_rows, uint64_t row_bytes, const uint8_t* nonce_base,
-                const void* in, const void* out, bool open, Plan& P) {
+                const void* in, const void* out, Plan& P) {
   P.descs.resize(n);
   std::vector<std::pair<uint64_t, uint64_t>> cover(n);
   for (uint32_t i = 0; i < n; i++) {
@@ -614,10 +566,14 @@ void build_plan(const gift_segment* segs, uint32_t n, uint64_t n_rows, uint64_t 
     const bool small = nb <= kSmallMaxBlocks;
     const bool one = !small && nb <= kTileBlocks;
     d.flags = (aligned ? kSegAligned : 0u) | (small ? kSegSmall : 0u) | (one ? kSegOneTile : 0u);
-    if (small)
+    if (small) {
       P.n_small++;
-    else
-      P.n_tiles += (uint32_t)((nb + kTileBlocks - 1) / kTileBlocks);
+    } else {
+      const uint32_t nt = tiles_of(d), r = tile_rows(nb, nt - 1);
+      P.n_tiles += nt;
+      P.tile_rows += (uint64_t)(nt - 1) * kRows + r;
+      if (one) P.one_rows_max = std::max(P.one_rows_max, r);
+    }
     if (!small && !one) P.n_multi++;
     cover[i] = {s.row_begin, s.row_count};
   }
@@ -628,10 +584,6 @@ void build_plan(const gift_segment* segs, uint32_t n, uint64_t n_rows, uint64_t 
     cur = c.first + c.second;
   }
   if (cur < n_rows) P.zr.push_back(ZeroRange{cur * row_bytes, (n_rows - cur) * row_bytes, -1, {0, 0, 0}});
-  if (open)
-    for (uint32_t i = 0; i < n; i++)
-      if (!(P.descs[i].flags & kSegSmall))
-        P.zr.push_back(ZeroRange{P.descs[i].byte_off, P.descs[i].len, (int32_t)i, {0, 0, 0}});
   // pieces of at most kZeroPieceBytes, so that one workgroup takes one piece
   std::vector<ZeroRange> pieces;
   pieces.reserve(P.zr.size());
@@ -679,20 +631,24 @@ gift_status run_gcm(const gift_tensor* t, const gift_segment_table* st, gift_key
   if (dev != kt->device) return fail(GIFT_E_INVALID, "key table belongs to device %d, current is %d", kt->device, dev);
 
   Plan P;
-  build_plan(st->segs, n, t->n_rows, t->row_bytes, nonce_base, t->data, out, OPEN, P);
+  build_plan(st->segs, n, t->n_rows, t->row_bytes, nonce_base, t->data, out, P);
   const uint32_t cus = (uint32_t)device_cus(dev);
-  std::vector<uint8_t> cut(P.n_tiles);
-  const uint32_t piece = plan_cuts(P.descs.data(), n, P.n_tiles, cus, &P.n_multi, cut.data());
+  const QueuePlan Q = plan_queue(P.n_tiles, P.tile_rows, P.n_multi, P.one_rows_max, cus);
 
-  // scratch: the staged tables (descs | zero ranges | tile queue | tile_base |
-  // small list | queue head), then partials | verdicts | one-tile tag masks
+  // scratch: the staged tables (descs | brief records | zero ranges | queue
+  // head), then what the device builds and fills (tile_base | small list |
+  // segment values | cut marks | work queue | partials | verdicts | one-tile tag masks)
   const size_t o_desc = 0;
-  const size_t o_zr = o_desc + align256(sizeof(SegDesc) * n);
-  const size_t o_to = o_zr + align256(sizeof(ZeroRange) * P.zr.size());
-  const size_t o_tb = o_to + align256(sizeof(TileEnt) * queue_capacity(P.n_tiles, cus));
+  const size_t o_br = o_desc + align256(sizeof(SegDesc) * n);
+  const size_t o_zr = o_br + align256(sizeof(SegBrief) * (n + 1));
+  const size_t o_qh = o_zr + align256(sizeof(ZeroRange) * P.zr.size());
+  const size_t o_st = o_qh + 256;  // end of the staged tables
+  const size_t o_tb = o_st;
   const size_t o_sl = o_tb + align256(4ull * (n + 1));
-  const size_t o_qh = o_sl + align256(4ull * (n ? n : 1));
-  const size_t o_pt = o_qh + 256;  // end of the staged tables
+  const size_t o_si = o_sl + align256(4ull * (n ? n : 1));
+  const size_t o_sc = o_si + align256(sizeof(SegInfo) * (n ? n : 1));
+  const size_t o_to = o_sc + align256(4ull * (n ? n : 1));
+  const size_t o_pt = o_to + align256(sizeof(TileEnt) * (Q.cap ? Q.cap : 1));
   const size_t o_vd = o_pt + align256(16ull * (P.n_tiles ? P.n_tiles : 1));
   const size_t o_fn = o_vd + align256(4ull * (n ? n : 1));
   const size_t bytes = o_fn + align256(16ull * (n ? n : 1));
@@ -700,11 +656,11 @@ gift_status run_gcm(const gift_tensor* t, const gift_segment_table* st, gift_key
   uint8_t* scratch = nullptr;
   hipError_t e = hipSuccess;
   if (no_alloc) {
-    if (bytes > kStaticScratchBytes || o_pt > Staging::kMaxStaged)
+    if (bytes > kStaticScratchBytes || o_st > Staging::kMaxStaged)
       return fail(GIFT_E_NOMEM,
                   "gift_seal_noalloc: the call needs %zu bytes of workspace (%zu of them staged tables); the fixed "
                   "workspace holds %zu (%zu staged)",
-                  bytes, o_pt, kStaticScratchBytes, Staging::kMaxStaged);
+                  bytes, o_st, kStaticScratchBytes, Staging::kMaxStaged);
     scratch = static_scratch(dev);
     if (!scratch) return fail(GIFT_E_INVALID, "gift_seal_noalloc: no workspace on device %d (create a key table there first)", dev);
   } else {
@@ -713,21 +669,28 @@ gift_status run_gcm(const gift_tensor* t, const gift_segment_table* st, gift_key
     scratch = lease.ptr;
   }
 
-  std::vector<uint8_t> host(o_pt);  // zero-filled: the queue head starts at 0
+  std::vector<uint8_t> host(o_st);  // zero-filled: the queue head starts at 0
   if (n) memcpy(host.data() + o_desc, P.descs.data(), sizeof(SegDesc) * n);
+  {
+    SegBrief* br = (SegBrief*)(host.data() + o_br);
+    for (uint32_t i = 0; i < n; i++) br[i] = SegBrief{P.descs[i].nblocks, P.descs[i].user};
+  }
   if (!P.zr.empty()) memcpy(host.data() + o_zr, P.zr.data(), sizeof(ZeroRange) * P.zr.size());
-  const uint32_t n_ents = P.n_tiles ? tile_order(P.descs.data(), n, piece, cut.data(), (TileEnt*)(host.data() + o_to)) : 0u;
-  const bool pieces = n_ents > P.n_tiles;  // some tile is split: its partial is an XOR of pieces
-  tile_tables(P.descs.data(), n, (uint32_t*)(host.data() + o_tb), (uint32_t*)(host.data() + o_sl));
   int32_t* verdicts = st->verdicts ? st->verdicts : (int32_t*)(scratch + o_vd);
   Staging* sg = staging_for(dev);
   if (!sg) return fail(GIFT_E_INVALID, "device index %d unsupported", dev);
-  // the prologue copies the tables and settles the verdicts (owner check)
+  // the prologue copies the tables, settles the verdicts (owner check),
+  // zeroes the tile partials (pieces of a cut tile XOR theirs into them) and
+  // expands the segment table on the device
+  const ExpandArgs ex{(uint32_t*)(scratch + o_tb), (uint32_t*)(scratch + o_sl), (TileEnt*)(scratch + o_to),
+                      (uint32_t)Q.cap, cus, nullptr, (SegInfo*)(scratch + o_si), (uint32_t*)(scratch + o_sc),
+                      kSmallMaxBlocks};
   e = sg->upload(
-      scratch, host.data(), o_pt, stream,
+      scratch, host.data(), o_st, stream,
       [&](const void* src) {
-        return launch_prologue(scratch, src, o_pt, n, kNoBids, st->row_labels, n ? verdicts : nullptr, &kt->dev,
-                               (uint4*)(scratch + o_fn), (uint4*)(scratch + o_pt), pieces ? P.n_tiles : 0u, stream);
+        return launch_prologue(scratch, src, o_st, n, kNoBids, st->row_labels, n ? verdicts : nullptr, &kt->dev,
+                               (uint4*)(scratch + o_fn), (uint4*)(scratch + o_pt), P.n_tiles, o_br,
+                               n ? &ex : nullptr, stream);
       },
       no_alloc);
   if (e != hipSuccess) return hip_fail(e, "staging upload");
@@ -747,12 +710,13 @@ gift_status run_gcm(const gift_tensor* t, const gift_segment_table* st, gift_key
       a.tile_base = (const uint32_t*)(scratch + o_tb);
       a.small_list = (const uint32_t*)(scratch + o_sl);
       a.n_tiles = P.n_tiles;
-      a.n_ents = n_ents;
+      a.n_ents = (uint32_t)Q.cap;
       a.n_small = P.n_small;
-      a.n_multi = P.n_multi;
+      a.n_multi = Q.finalize ? 1u : 0u;
       a.partials = (uint4*)(scratch + o_pt);
       a.fin = (const uint4*)(scratch + o_fn);
       a.tile_order = (const TileEnt*)(scratch + o_to);
+      a.seg_cut = (const uint32_t*)(scratch + o_sc);
       a.tile_counter = (uint32_t*)(scratch + o_qh);
       a.verdicts = verdicts;
       a.tags_out = tags_out;
@@ -765,7 +729,7 @@ gift_status run_gcm(const gift_tensor* t, const gift_segment_table* st, gift_key
           break;
         }
       }
-      e = launch_gcm_tiles(a, OPEN ? kModeOpen : 0, (uint32_t)device_cus(dev), stream);
+      e = launch_gcm_tiles(a, OPEN ? kModeOpen : 0, Q.grid, stream);
       if (e != hipSuccess) {
         rs = hip_fail(e, "gcm launch");
         break;
@@ -779,6 +743,10 @@ gift_status run_gcm(const gift_tensor* t, const gift_segment_table* st, gift_key
       }
       e = launch_gcm_small(a, OPEN, stream);
       if (e == hipSuccess) e = launch_gcm_finalize(a, OPEN, stream);
+      // open: segments that failed are zeroed after their verdicts are known
+      if (e == hipSuccess && OPEN)
+        e = launch_zero_failed(d_desc, n, a.tile_base, P.n_tiles, verdicts, nullptr, (uint8_t*)out, 0u, cus * 4u,
+                               stream);
       if (e != hipSuccess) {
         rs = hip_fail(e, "gcm launch");
         break;
@@ -894,7 +862,8 @@ gift_status run_paged(const gift_paged_kv* kv, const gift_request* reqs, uint32_
   // descriptors: rows = positions in the uploaded block-id array
   std::vector<SegDesc> descs(n);
   uint64_t boff = 0, bpos = 0, cpos = 0;
-  uint32_t n_tiles = 0, n_multi = 0;
+  uint32_t n_tiles = 0, n_multi = 0, one_rows_max = 0;
+  uint64_t tile_rows_all = 0;
   for (uint32_t i = 0; i < n; i++) {
     const gift_request& r = reqs[i];
     SegDesc& d = descs[i];
@@ -914,7 +883,10 @@ gift_status run_paged(const gift_paged_kv* kv, const gift_request* reqs, uint32_
     for (int w = 0; w < 3; w++)
       d.iv[w] = (uint32_t)iv[4 * w] | ((uint32_t)iv[4 * w + 1] << 8) | ((uint32_t)iv[4 * w + 2] << 16) |
                 ((uint32_t)iv[4 * w + 3] << 24);
-    n_tiles += (uint32_t)(((uint64_t)d.nblocks + kTileBlocks - 1) / kTileBlocks);
+    const uint32_t nt = tiles_of(d), rows = tile_rows(d.nblocks, nt - 1);
+    n_tiles += nt;
+    tile_rows_all += (uint64_t)(nt - 1) * kRows + rows;
+    if (nt == 1) one_rows_max = std::max(one_rows_max, rows);
     boff += d.len;
     bpos += r.n_block_ids;
     cpos += per_block_chunks * r.n_block_ids;
@@ -922,19 +894,22 @@ gift_status run_paged(const gift_paged_kv* kv, const gift_request* reqs, uint32_
   uint32_t shift = 0;
   while ((16ull << shift) < kv->chunk_bytes) shift++;
   const uint32_t cus = (uint32_t)device_cus(dev);
-  std::vector<uint8_t> cut(n_tiles);
-  const uint32_t piece = plan_cuts(descs.data(), n, n_tiles, cus, &n_multi, cut.data());
+  const QueuePlan Q = plan_queue(n_tiles, tile_rows_all, n_multi, one_rows_max, cus);
 
-  // scratch: the staged tables (descs | block ids | tile queue | tile_base |
-  // small list | queue head), then partials | verdicts | chunk offsets |
-  // one-tile tag masks
+  // scratch: the staged tables (descs | brief records | block ids | queue
+  // head), then what the device builds and fills (tile_base | small list |
+  // segment values | cut marks | work queue | partials | verdicts | chunk offsets | one-tile tag masks)
   const size_t o_desc = 0;
-  const size_t o_bid = o_desc + align256(sizeof(SegDesc) * n);
-  const size_t o_to = o_bid + align256(4ull * total_bids);
-  const size_t o_tb = o_to + align256(sizeof(TileEnt) * queue_capacity(n_tiles, cus));
+  const size_t o_br = o_desc + align256(sizeof(SegDesc) * n);
+  const size_t o_bid = o_br + align256(sizeof(SegBrief) * (n + 1));
+  const size_t o_qh = o_bid + align256(4ull * total_bids);
+  const size_t o_st = o_qh + 256;  // end of the staged tables
+  const size_t o_tb = o_st;
   const size_t o_sl = o_tb + align256(4ull * (n + 1));
-  const size_t o_qh = o_sl + align256(4ull * n);
-  const size_t o_pt = o_qh + 256;  // end of the staged tables
+  const size_t o_si = o_sl + align256(4ull * n);
+  const size_t o_sc = o_si + align256(sizeof(SegInfo) * n);
+  const size_t o_to = o_sc + align256(4ull * n);
+  const size_t o_pt = o_to + align256(sizeof(TileEnt) * (Q.cap ? Q.cap : 1));
   const size_t o_vd = o_pt + align256(16ull * (n_tiles ? n_tiles : 1));
   const size_t o_ck = o_vd + align256(4ull * n);
   const size_t o_fn = o_ck + align256(8ull * cpos);
@@ -943,8 +918,12 @@ gift_status run_paged(const gift_paged_kv* kv, const gift_request* reqs, uint32_
   hipError_t e = lease.acquire(dev, stream, bytes);
   if (e != hipSuccess) return hip_fail(e, "device scratch");
   uint8_t* scratch = lease.ptr;
-  std::vector<uint8_t> host(o_pt);  // zero-filled: the queue head starts at 0
+  std::vector<uint8_t> host(o_st);  // zero-filled: the queue head starts at 0
   memcpy(host.data() + o_desc, descs.data(), sizeof(SegDesc) * n);
+  {
+    SegBrief* br = (SegBrief*)(host.data() + o_br);
+    for (uint32_t i = 0; i < n; i++) br[i] = SegBrief{descs[i].nblocks, descs[i].user};
+  }
   {
     uint32_t* bp = (uint32_t*)(host.data() + o_bid);
     for (uint32_t i = 0; i < n; i++) {
@@ -952,17 +931,17 @@ gift_status run_paged(const gift_paged_kv* kv, const gift_request* reqs, uint32_
       bp += reqs[i].n_block_ids;
     }
   }
-  const uint32_t n_ents = n_tiles ? tile_order(descs.data(), n, piece, cut.data(), (TileEnt*)(host.data() + o_to)) : 0u;
-  const bool pieces = n_ents > n_tiles;  // some tile is split: its partial is an XOR of pieces
-  tile_tables(descs.data(), n, (uint32_t*)(host.data() + o_tb), (uint32_t*)(host.data() + o_sl));
   int32_t* verdicts = verdicts_user ? verdicts_user : (int32_t*)(scratch + o_vd);
   Staging* sg = staging_for(dev);
-  // the prologue copies the tables and settles the verdicts (owner check by block id)
-  e = sg ? sg->upload(scratch, host.data(), o_pt, stream,
+  // the prologue copies the tables, settles the verdicts (owner check by
+  // block id), zeroes the tile partials and expands the segment table
+  const ExpandArgs ex{(uint32_t*)(scratch + o_tb), (uint32_t*)(scratch + o_sl), (TileEnt*)(scratch + o_to),
+                      (uint32_t)Q.cap, cus, nullptr, (SegInfo*)(scratch + o_si), (uint32_t*)(scratch + o_sc), 0u};
+  e = sg ? sg->upload(scratch, host.data(), o_st, stream,
                       [&](const void* src) {
-                        return launch_prologue(scratch, src, o_pt, n, o_bid, labels, verdicts, &kt->dev,
-                                               (uint4*)(scratch + o_fn), (uint4*)(scratch + o_pt),
-                                               pieces ? n_tiles : 0u, stream);
+                        return launch_prologue(scratch, src, o_st, n, o_bid, labels, verdicts, &kt->dev,
+                                               (uint4*)(scratch + o_fn), (uint4*)(scratch + o_pt), n_tiles, o_br,
+                                               &ex, stream);
                       })
          : hipErrorInvalidDevice;
   if (e != hipSuccess) return hip_fail(e, "staging upload");
@@ -988,12 +967,13 @@ gift_status run_paged(const gift_paged_kv* kv, const gift_request* reqs, uint32_
     a.tile_base = (const uint32_t*)(scratch + o_tb);
     a.small_list = (const uint32_t*)(scratch + o_sl);
     a.n_tiles = n_tiles;
-    a.n_ents = n_ents;
-    a.n_multi = n_multi;
+    a.n_ents = (uint32_t)Q.cap;
+    a.n_multi = Q.finalize ? 1u : 0u;
     a.n_small = 0;
     a.partials = (uint4*)(scratch + o_pt);
     a.fin = (const uint4*)(scratch + o_fn);
     a.tile_order = (const TileEnt*)(scratch + o_to);
+    a.seg_cut = (const uint32_t*)(scratch + o_sc);
     a.tile_counter = (uint32_t*)(scratch + o_qh);
     a.verdicts = verdicts;
     a.tags_out = tags_out;
@@ -1006,12 +986,12 @@ gift_status run_paged(const gift_paged_kv* kv, const gift_request* reqs, uint32_
         break;
       }
     }
-    e = launch_gcm_tiles(a, OPEN ? (kModeOpen | kModeScatter) : kModeGather, (uint32_t)device_cus(dev), stream);
+    e = launch_gcm_tiles(a, OPEN ? (kModeOpen | kModeScatter) : kModeGather, Q.grid, stream);
     if (e == hipSuccess && g_prof_after) e = hipEventRecord(g_prof_after, stream);
     if (e == hipSuccess) e = launch_gcm_finalize(a, OPEN, stream);
     if (e == hipSuccess && OPEN)
-      e = launch_zero_chunks(d_desc, n, (const uint32_t*)(scratch + o_tb), n_tiles, verdicts, d_ck,
-                             (uint8_t*)kv->base, shift, (uint32_t)device_cus(dev) * 4u, stream);
+      e = launch_zero_failed(d_desc, n, (const uint32_t*)(scratch + o_tb), n_tiles, verdicts, d_ck,
+                             (uint8_t*)kv->base, shift, cus * 4u, stream);
     if (e != hipSuccess) {
       rs = hip_fail(e, "paged gcm launch");
       break;
@@ -1181,7 +1161,7 @@ gift_status gift_check_owner(const gift_segment_table* st, const uint32_t* label
   int dev;
   if ((sv = current_device(&dev)) != GIFT_OK) return sv;
   Plan P;
-  build_plan(st->segs, n, n_rows, 1, nullptr, nullptr, nullptr, false, P);
+  build_plan(st->segs, n, n_rows, 1, nullptr, nullptr, nullptr, P);
   const size_t bytes = sizeof(SegDesc) * n;
   ScratchLease lease;
   hipError_t e = lease.acquire(dev, stream, bytes);
@@ -1191,7 +1171,7 @@ gift_status gift_check_owner(const gift_segment_table* st, const uint32_t* label
   e = sg ? sg->upload(d, P.descs.data(), bytes, stream,
                       [&](const void* src) {
                         return launch_prologue(d, src, bytes, n, kNoBids, labels, st->verdicts, nullptr, nullptr,
-                                               nullptr, 0u, stream);
+                                               nullptr, 0u, 0u, nullptr, stream);
                       })
          : hipErrorInvalidDevice;
   hipError_t e2 = lease.release();
@@ -1219,7 +1199,7 @@ static gift_status run_tokens(bool decrypt, const gift_segment_table* st, uint64
   if ((sv = current_device(&dev)) != GIFT_OK) return sv;
   if (dev != kt->device) return fail(GIFT_E_INVALID, "key table belongs to device %d, current is %d", kt->device, dev);
   Plan P;
-  build_plan(st->segs, n, n_tokens, 1, nullptr, nullptr, nullptr, false, P);
+  build_plan(st->segs, n, n_tokens, 1, nullptr, nullptr, nullptr, P);
   SegDesc* d = nullptr;
   hipError_t e = hipSuccess;
   ScratchLease lease;
@@ -1232,7 +1212,7 @@ static gift_status run_tokens(bool decrypt, const gift_segment_table* st, uint64
     e = sg ? sg->upload(d, P.descs.data(), bytes, stream,
                         [&](const void* src) {
                           return launch_prologue(d, src, bytes, n, kNoBids, nullptr, nullptr, nullptr, nullptr,
-                                                 nullptr, 0u, stream);
+                                                 nullptr, 0u, 0u, nullptr, stream);
                         })
            : hipErrorInvalidDevice;
   }

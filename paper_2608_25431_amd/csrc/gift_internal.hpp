@@ -31,8 +31,9 @@ constexpr int kFinLanes = 64;                              // lanes of the per-s
 constexpr int kLeaders = 4;
 static_assert(kThreads % (64 * kLeaders) == 0, "waves per leader");
 
-// kSegOneTile: a tiled segment of at most kTileBlocks blocks; the tile kernel
-// writes its tag (open: its verdict) itself and the finalize pass skips it.
+// kSegOneTile: a tiled segment of at most kTileBlocks blocks; unless its tile
+// is cut into pieces, the tile kernel writes its tag (open: its verdict)
+// itself and the finalize pass skips it.
 enum : uint32_t { kSegAligned = 1u, kSegSmall = 2u, kSegOneTile = 4u };
 
 // Device descriptor of one segment (64 B), built on the host.
@@ -79,7 +80,7 @@ struct KeyTableDev {
 // tile_base numbering), which is tile t of segment s counted from the
 // segment's end; user is the segment's user.  trow packs t (bits 0-15), r0
 // (16-23) and r1 (24-31).  A whole tile has r0 = 0, r1 = kRows; a tile that
-// plan_cuts cuts has one entry per piece of rows instead.
+// the expansion kernel cuts has one entry per piece of rows instead.
 struct TileEnt {
   uint32_t g, s, trow, user;
 };
@@ -105,13 +106,14 @@ struct GcmArgs {
   const uint32_t* tile_base;   // [n_segs + 1] first tile of each segment (small ones: 0 tiles)
   const uint32_t* small_list;  // [n_small] indices of small segments
   uint32_t n_tiles;
-  uint32_t n_ents;             // entries of the work queue (tiles, some cut into pieces)
+  uint32_t n_ents;             // capacity of the work queue (tiles, some cut into pieces; kNoTile after the last)
   uint32_t n_small;
-  uint32_t n_multi;            // segments of more than one tile (the finalize pass)
+  uint32_t n_multi;            // nonzero: launch the finalize pass (some segment may have more than one entry)
   uint4* partials;             // [n_tiles] GHASH partial of each tile
   const uint4* fin;            // [n_segs] E_K(J0) xor H*L of one-tile segments (from the prologue)
-  const TileEnt* tile_order;   // [n_tiles] tiles in the order the workgroups claim them
-  uint32_t* tile_counter;      // work-queue head, zeroed by the expansion kernel
+  const TileEnt* tile_order;   // [n_ents] tiles and pieces in the order the workgroups claim them
+  const uint32_t* seg_cut;     // [n_segs] 1: a one-tile segment cut into pieces (the finalize pass forms its tag)
+  uint32_t* tile_counter;      // work-queue head, zeroed with the staged tables
   int32_t* verdicts;           // [n_segs]
   uint8_t* tags_out;           // seal: [n_segs][16]
   const uint8_t* tags_in;      // open: [n_segs][16]
@@ -131,41 +133,66 @@ uint8_t* static_scratch(int dev);
 // Launch wrappers (gift_kernels.hip).  All enqueue on `s` and return the
 // launch status.
 hipError_t launch_key_setup(const uint8_t* keys_dev, KeyTableDev kt, hipStream_t s);
+// Outputs of the segment-table expansion (see launch_prologue): tile_base
+// [n + 1] (exclusive scan of each segment's tiles), the small-segment list,
+// and the work queue of cap entries; *n_ents (device, may be NULL) gets the
+// number of entries; seg_cut marks the one-tile segments whose tile it cuts.
+// A tile runs on one CU, so:
+// - with fewer tiles than cus, every tile of more than p = ceil(tile rows of
+//   all tiles / cus) rows is cut into pieces of p rows;
+// - otherwise up to cus tiles of more than kPieceRows rows, the largest
+//   first (in tile order within a row count), are cut into pieces of
+//   kPieceRows rows, which sort to the tail of the queue, so that the
+//   workgroups, which run at slightly different speeds, finish together.
+// The queue holds every whole tile and every piece, longest first, padded
+// with kNoTile entries up to cap.
+// The host stages one brief record per segment beside the descriptors: what
+// the expansion reads of a segment (8 B instead of its 64-B descriptor).  A
+// segment is small when it has at most the call's small_max blocks (0 in
+// calls without a small-segment path) and one-tile when it is not small and
+// has at most kTileBlocks blocks, as its descriptor's flags say.
+struct SegBrief {
+  uint32_t nblocks, user;
+};
+static_assert(sizeof(SegBrief) == 8, "SegBrief layout");
+// Per-segment values of the expansion: blocks, flags, user, first tile,
+// first run (runs of up to 16 tiles), cut rank of its first candidate tile.
+struct SegInfo {
+  uint32_t m, flags, user, tb, rb, tk;
+};
+struct ExpandArgs {
+  uint32_t* tile_base;
+  uint32_t* small_list;
+  TileEnt* order;
+  uint32_t cap;
+  uint32_t cus;
+  uint32_t* n_ents;
+  SegInfo* info;      // [n] scratch, used when the call has more segments than the expansion keeps in LDS
+  uint32_t* seg_cut;  // [n] out: 1 for a one-tile segment whose tile is cut (its tag comes from the finalize pass)
+  uint32_t small_max;  // blocks of the largest small segment (0: the call has no small-segment path)
+};
 // First kernel of a call.  Copies bytes of staged tables from src (the
-// mapped host ring; nullptr: they are in dst already) to dst, and, when
-// verdicts is not NULL, writes each segment's first verdict: the owner check
-// against labels (indexed by row, or by the block ids at byte bids_off of the
-// tables for paged calls) or OK without labels.  With a key table it also
-// writes fin[s] = E_K(J0) xor H*L of every one-tile segment s and zeroes the
-// n_zero tile partials at zero (the tile kernel XORs pieces into them).  The
-// descriptors sit at byte 0 of the tables.
+// mapped host ring; nullptr: they are in dst already) to dst, zeroes the
+// n_zero tile partials at zero (pieces of a cut tile XOR theirs into them),
+// and, when verdicts is not NULL, writes each segment's first verdict: the
+// owner check against labels (indexed by row, or by the block ids at byte
+// bids_off of the tables for paged calls) or OK without labels.  With a key
+// table it also writes fin[s] = E_K(J0) xor H*L of every one-tile segment s.
+// The descriptors sit at byte 0 of the tables.  With ex, one workgroup runs
+// the segment-table expansion into *ex meanwhile, from the brief records at
+// byte brief_off of the tables.
 constexpr uint64_t kNoBids = ~0ull;
 hipError_t launch_prologue(void* dst, const void* src, size_t bytes, uint32_t n_segs, uint64_t bids_off,
                            const uint32_t* labels, int32_t* verdicts, const KeyTableDev* kt, uint4* fin,
-                           uint4* zero, uint32_t n_zero, hipStream_t s);
-// Which tiles the work queue cuts into pieces, and into pieces of how many
-// tile rows.  A tile runs on one CU, so:
-// - with fewer tiles than cus, every tile of more than `rows` rows is cut,
-//   rows = ceil(tile rows of all tiles / cus), so that one tile no longer
-//   runs on one CU while the others idle;
-// - otherwise up to cus tiles of more than kPieceRows rows, the largest
-//   first, are cut into pieces of kPieceRows rows that sort to the tail of
-//   the queue, so that the workgroups, which run at slightly different
-//   speeds, finish together.
-// cut[g] = 1 for each cut tile g (n_tiles entries).  One-tile segments whose
-// tile is cut lose kSegOneTile (their tag comes from the finalize pass) and
-// count into *n_multi.  Returns the piece rows (0: nothing is cut).
-uint32_t plan_cuts(SegDesc* descs, uint32_t n_segs, uint32_t n_tiles, uint32_t cus, uint32_t* n_multi,
-                   uint8_t* cut);
-// The work queue, longest entries first (by the rows each entry runs): each
-// tile whole, or for cut tiles pieces of `rows` rows aligned to the tile's
-// end.  Returns the number of entries written to order, at most
-// queue_capacity(n_tiles, cus) for the cus given to plan_cuts.
-uint32_t tile_order(const SegDesc* descs, uint32_t n_segs, uint32_t rows, const uint8_t* cut, TileEnt* order);
+                           uint4* zero, uint32_t n_zero, uint64_t brief_off, const ExpandArgs* ex, hipStream_t s);
+// The expansion alone, on brief records in device memory: the library's test
+// hook.
+hipError_t launch_expand(const SegBrief* brief, uint32_t n_segs, const ExpandArgs& x, hipStream_t s);
+// Entries the work queue can hold: a tail cut adds at most
+// kRows / kPieceRows - 1 entries for each of at most cus tiles; a fine cut
+// (pieces of p >= all rows / cus rows) at most all rows / p <= cus entries
+// beyond one per tile.
 inline uint64_t queue_capacity(uint32_t n_tiles, uint32_t cus) {
-  // a tail cut adds at most kRows / kPieceRows - 1 entries for each of at
-  // most cus tiles; a fine cut (rows >= all rows / cus) at most all rows /
-  // rows <= cus entries beyond one per tile
   return (uint64_t)n_tiles + (uint64_t)(kRows / kPieceRows - 1) * cus;
 }
 hipError_t launch_gcm_tiles(const GcmArgs& a, int mode, uint32_t grid, hipStream_t s);
@@ -174,14 +201,17 @@ hipError_t launch_gcm_finalize(const GcmArgs& a, bool open, hipStream_t s);
 hipError_t launch_zero_ranges(uint8_t* out, const ZeroRange* r, uint32_t n, const int32_t* verdicts, uint32_t grid,
                               hipStream_t s);
 hipError_t launch_wipe(void* p, size_t bytes, hipStream_t s);
-// Paged calls: chunk offsets from the block tables (segment rows index bids),
-// and zeroing of every chunk of segments whose verdict is AUTH_FAIL.
+// Paged calls: chunk offsets from the block tables (segment rows index bids).
 hipError_t launch_chunk_table(const SegDesc* segs, uint32_t n_segs, const uint32_t* bids, uint32_t n_layers,
                               uint32_t n_parts, uint64_t layer_stride, uint64_t block_stride, uint64_t part_stride,
                               uint64_t* chunk_off, hipStream_t s);
-hipError_t launch_zero_chunks(const SegDesc* segs, uint32_t n_segs, const uint32_t* tile_base, uint32_t n_tiles,
-                              const int32_t* verdicts, const uint64_t* chunk_off, uint8_t* pbase,
-                              uint32_t chunk_shift, uint32_t grid, hipStream_t s);
+// Open: zeroes the output of failed segments tile by tile -- contiguous
+// (chunk_off NULL, base = out): every segment whose verdict is not OK;
+// through block tables (base = the cache): requests whose verdict is
+// AUTH_FAIL only (a request rejected by the label check writes nothing).
+hipError_t launch_zero_failed(const SegDesc* segs, uint32_t n_segs, const uint32_t* tile_base, uint32_t n_tiles,
+                              const int32_t* verdicts, const uint64_t* chunk_off, uint8_t* base, uint32_t chunk_shift,
+                              uint32_t grid, hipStream_t s);
 // Per-token block encryption (decrypt == true: the inverse).  Rows of the
 // descriptors are token indices.
 hipError_t launch_tokens(const SegDesc* segs, uint32_t n_segs, bool decrypt, const uint64_t* tokens,

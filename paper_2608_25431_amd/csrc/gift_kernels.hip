@@ -26,6 +26,8 @@
 // zero-fill, the paged-call helpers, per-token encryption and key setup.
 #include <hip/hip_runtime.h>
 
+#include <stddef.h>
+
 #include <mutex>
 
 #include "gift_device.hpp"
@@ -376,7 +378,8 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
     const uint64_t off = ti->desc.byte_off, len = ti->desc.len;
     const uint32_t flags = __builtin_amdgcn_readfirstlane(ti->desc.flags);
     const bool aligned = (flags & kSegAligned) != 0;
-    const bool one = (flags & kSegOneTile) != 0;
+    // a one-tile segment whose tile is cut into pieces gets its tag from the finalize pass
+    const bool one = (flags & kSegOneTile) != 0 && r0 == 0 && r1 == kRows;
     if (one && tid == 0) red[kLeaders] = u128{{ti->fin.x, ti->fin.y, ti->fin.z, ti->fin.w}};  // for the tile end
     const int64_t base = (int64_t)m - (int64_t)(t + 1) * (int64_t)kTileBlocks;  // block index of virtual slot 0
     const int r_start = base < 0 ? (int)((uint64_t)(-base) / kThreads) : 0;
@@ -557,7 +560,7 @@ __global__ __launch_bounds__(kFinLanes) void k_finalize(GcmArgs a) {
   for (uint32_t i = lane; i < 256u; i += kFinLanes) te[i] = c_aes.te0[i];
   __syncthreads();
   const SegDesc sd = a.segs[s];
-  if (sd.flags & (kSegSmall | kSegOneTile)) return;
+  if ((sd.flags & kSegSmall) || ((sd.flags & kSegOneTile) && !a.seg_cut[s])) return;
   const int32_t verdict = a.verdicts[s];
   if (verdict != kVerdictOk) {
     if (!OPEN && lane < 4) ((uint32_t*)(a.tags_out + 16ull * s))[lane] = 0u;
@@ -663,55 +666,482 @@ __global__ __launch_bounds__(64) void k_small(GcmArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// First kernel of a call.  It copies the call's staged tables (descriptors,
-// tile queue, tile_base, small list, zeroed queue head, ...) from the mapped
-// host ring into device scratch, and settles every segment's first verdict:
-// with labels, the owner check (OWNER_MIXED iff some row label differs from
-// the segment's user; the sentinels never equal a user), else OK.  The check
-// reads descriptors and block ids where the copy reads them, so the two parts
-// never wait on each other.
+// Segment-table expansion, by one workgroup of a call's first kernel: from
+// the descriptors to the tables the GCM kernels read.
+//   - tile_base: exclusive scan of the tiles of each segment (small segments
+//     have none), tile_base[n] = all tiles;
+//   - small_list: the small segments in table order;
+//   - the cut: a tile runs on one CU, so with fewer tiles than CUs every
+//     tile of more than p = ceil(all tile rows / CUs) rows is cut into
+//     pieces of p rows; otherwise up to one tile per CU, the largest of more
+//     than kPieceRows rows (in tile order within a row count), is cut into
+//     pieces of kPieceRows rows.  Pieces are aligned to the tile's end; the
+//     lowest may start below the tile's first row.  A one-tile segment
+//     whose tile is cut is marked in seg_cut (its tag comes from the
+//     finalize pass);
+//   - the work queue: every whole tile and every piece, longest first (a
+//     counting sort by the rows an entry runs), padded with kNoTile up to
+//     cap entries.
+// Each segment's tiles are split into runs of at most kRunTiles; threads
+// take contiguous ranges of runs, so thread order is tile order.  Whole
+// tiles and whole pieces take their slots by a scan over the threads, in
+// tile order; the other entries (partial first tiles, remainder pieces) by
+// LDS atomics, in no fixed order: which CU runs which entry changes no
+// result.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void k_prologue(uint4* __restrict__ dst, const uint4* __restrict__ src, size_t n16,
-                                                  const SegDesc* __restrict__ segs, uint32_t n,
-                                                  const uint32_t* __restrict__ labels,
-                                                  const uint32_t* __restrict__ bids, int32_t* __restrict__ verdicts,
-                                                  KeyTableDev kt, uint4* __restrict__ fin,
-                                                  uint4* __restrict__ zero, uint32_t n_zero) {
+constexpr int kExpandThreads = 1024;  // the most threads an expanding workgroup may have
+constexpr int kPrologueThreads = 256;
+constexpr uint32_t kRunTiles = 16;
+
+__device__ __forceinline__ uint32_t tiles_in(uint32_t nblocks) {
+  return (uint32_t)(((uint64_t)nblocks + kTileBlocks - 1) / kTileBlocks);
+}
+
+// Rows of tile t of a segment of m blocks (tiles aligned to its end: only the
+// first tile, t = tiles - 1, can be partial).
+__device__ __forceinline__ uint32_t tile_rows_of(uint32_t m, uint32_t t) {
+  const int64_t base = (int64_t)m - (int64_t)(t + 1) * (int64_t)kTileBlocks;
+  return base >= 0 ? (uint32_t)kRows : (uint32_t)kRows - (uint32_t)((uint64_t)(-base) / kThreads);
+}
+
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x, uint32_t lane) {
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const uint32_t y = __shfl_up(x, d, 64);
+    if (lane >= (uint32_t)d) x += y;
+  }
+  return x;
+}
+
+// Exclusive prefix sum of v over the workgroup in thread order; *total gets
+// the sum of all.  wsum: one LDS word per wave.
+__device__ uint32_t block_scan(uint32_t v, uint32_t* wsum, uint32_t* total) {
+  const uint32_t lane = threadIdx.x & 63u, wave = threadIdx.x >> 6;
+  const uint32_t x = wave_incl_scan(v, lane);
+  __syncthreads();  // wsum is free
+  if (lane == 63u) wsum[wave] = x;
+  __syncthreads();
+  uint32_t before = 0, all = 0;
+  for (uint32_t w = 0; w < blockDim.x / 64u; w++) {
+    const uint32_t c = wsum[w];
+    before += w < wave ? c : 0u;
+    all += c;
+  }
+  *total = all;
+  return before + x - v;
+}
+
+// Exclusive prefix sums of three values at once (one pass of barriers).
+__device__ uint3 block_scan3(uint3 v, uint3* wsum, uint3* total) {
+  const uint32_t lane = threadIdx.x & 63u, wave = threadIdx.x >> 6;
+  const uint3 x = make_uint3(wave_incl_scan(v.x, lane), wave_incl_scan(v.y, lane), wave_incl_scan(v.z, lane));
+  __syncthreads();  // wsum is free
+  if (lane == 63u) wsum[wave] = x;
+  __syncthreads();
+  uint3 before = make_uint3(0u, 0u, 0u), all = make_uint3(0u, 0u, 0u);
+  for (uint32_t w = 0; w < blockDim.x / 64u; w++) {
+    const uint3 c = wsum[w];
+    if (w < wave) {
+      before.x += c.x;
+      before.y += c.y;
+      before.z += c.z;
+    }
+    all.x += c.x;
+    all.y += c.y;
+    all.z += c.z;
+  }
+  *total = all;
+  return make_uint3(before.x + x.x - v.x, before.y + x.y - v.y, before.z + x.z - v.z);
+}
+
+// Expansion by the calling workgroup (all its threads call it), from the
+// per-segment brief records (the source may be host memory).  A one-tile
+// segment whose tile is cut gets seg_cut = 1 (every segment gets its 0 or 1).
+// The per-segment values the walks need sit in LDS for up to kInfoLds
+// segments, else in x.info.
+constexpr uint32_t kInfoLds = 1024;
+
+__device__ void expand_tables(const SegBrief* brief, uint32_t n, const ExpandArgs& x) {
+  __shared__ uint32_t hist[kRows + 1];    // tiles by rows
+  __shared__ uint32_t cursor[kRows + 1];  // entries by rows run, then the next free slot of each
+  __shared__ uint32_t wsum[kExpandThreads / 64];
+  __shared__ uint3 wsum3[kExpandThreads / 64];
+  __shared__ uint32_t first_seg[kExpandThreads];  // segment of each thread's first run
+  __shared__ SegInfo info_lds[kInfoLds];
+  __shared__ unsigned long long rows_all;
+  __shared__ uint32_t c_piece, c_from, c_take, c_left, c_fine, c_ents, c_full_at, c_piece_at;
+  const uint32_t tid = threadIdx.x, nt_ = blockDim.x, lane = tid & 63u;
+  SegInfo* info = n <= kInfoLds ? info_lds : x.info;
+  for (uint32_t i = tid; i <= (uint32_t)kRows; i += nt_) hist[i] = cursor[i] = 0u;
+  first_seg[tid] = 0xFFFFFFFFu;
+  if (tid == 0) rows_all = 0ull;
+
+  // the brief records, two per 16-byte load, several loads in flight per
+  // thread (the source may be host memory); flags as the descriptors have them
+  {
+    const uint4* src = (const uint4*)brief;
+    const uint32_t n16 = (n + 1) / 2;
+    constexpr int kInFlight = 8;
+    auto note = [&](uint32_t i, uint32_t m, uint32_t user) {
+      const bool small = m <= x.small_max;
+      info[i].m = m;
+      info[i].flags = small ? kSegSmall : (m <= kTileBlocks ? kSegOneTile : 0u);
+      info[i].user = user;
+      x.seg_cut[i] = 0u;
+    };
+    for (uint32_t i0 = tid; i0 < n16; i0 += kInFlight * nt_) {
+      uint4 q[kInFlight];
+#pragma unroll
+      for (int k = 0; k < kInFlight; k++)
+        if (i0 + k * nt_ < n16) q[k] = src[i0 + k * nt_];
+#pragma unroll
+      for (int k = 0; k < kInFlight; k++) {
+        const uint32_t i = i0 + k * nt_;
+        if (i >= n16) break;
+        note(2 * i, q[k].x, q[k].y);
+        if (2 * i + 1 < n) note(2 * i + 1, q[k].z, q[k].w);
+      }
+    }
+  }
+  __syncthreads();
+
+  // segments [s0, s1) of this thread: count tiles, rows, small segments and runs
+  const uint32_t per = (n + nt_ - 1) / nt_;
+  const uint32_t s0 = min(n, tid * per), s1 = min(n, s0 + per);
+  uint32_t my_tiles = 0, my_small = 0, my_runs = 0, my_whole = 0;
+  unsigned long long my_rows = 0;
+  for (uint32_t s = s0; s < s1; s++) {
+    const uint32_t m = info[s].m;
+    if (info[s].flags & kSegSmall) {
+      my_small++;
+      continue;
+    }
+    const uint32_t nt = tiles_in(m), r = tile_rows_of(m, nt - 1);
+    my_tiles += nt;
+    my_runs += (nt + kRunTiles - 1) / kRunTiles;
+    my_rows += (unsigned long long)(nt - 1) * kRows + r;
+    my_whole += nt - 1;
+    atomicAdd(&hist[r], 1u);
+  }
+  // the whole tiles below each segment's first tile, and the rows, once per wave
+  for (int d = 32; d >= 1; d >>= 1) {
+    my_whole += __shfl_xor(my_whole, d, 64);
+    my_rows += __shfl_xor(my_rows, d, 64);
+  }
+  if (lane == 0u) {
+    if (my_whole) atomicAdd(&hist[kRows], my_whole);
+    if (my_rows) atomicAdd(&rows_all, my_rows);
+  }
+  uint3 tot;
+  const uint3 base0 = block_scan3(make_uint3(my_tiles, my_small, my_runs), wsum3, &tot);
+  const uint32_t tb0 = base0.x, sm0 = base0.y, rn0 = base0.z;
+  const uint32_t n_tiles = tot.x, n_runs = tot.z;
+  const uint32_t per_r = (n_runs + nt_ - 1) / nt_;  // runs per thread
+  {
+    uint32_t tb = tb0, sm = sm0, rn = rn0;
+    for (uint32_t s = s0; s < s1; s++) {
+      x.tile_base[s] = tb;
+      info[s].tb = tb;
+      info[s].rb = rn;
+      const SegInfo v = info[s];
+      if (v.flags & kSegSmall) {
+        x.small_list[sm++] = s;
+        continue;
+      }
+      const uint32_t nt = tiles_in(v.m), nr = (nt + kRunTiles - 1) / kRunTiles;
+      // this segment's runs fall in the run ranges of threads rn / per_r ..
+      // (rn + nr - 1) / per_r; the lowest such segment starts a thread's range
+      for (uint32_t c = rn / per_r; c <= (rn + nr - 1) / per_r; c++) atomicMin(&first_seg[c], s);
+      tb += nt;
+      rn += nr;
+    }
+  }
+  if (tid == 0) x.tile_base[n] = n_tiles;
+  __syncthreads();  // hist, rows_all, first_seg and the segment values complete
+
+  // the cut (wave 0): with enough tiles, every tile of at least `from` rows
+  // and the first `left` tiles of `take` rows, counted from the longest down
+  // to at most cus tiles
+  if (tid < 64u) {
+    uint32_t piece = 0, from = kRows + 1, take = 0, left = 0, fine = 0;
+    if (n_tiles > 0 && n_tiles < x.cus) {
+      const unsigned long long p = (rows_all + x.cus - 1) / x.cus;
+      if (p < (unsigned long long)kRows) {
+        piece = (uint32_t)p;
+        fine = 1;
+      }
+    } else if (n_tiles > 0) {
+      piece = kPieceRows;
+      // lane k holds rows kRows - k and kRows - 64 - k (those above kPieceRows)
+      constexpr uint32_t kSpan = (uint32_t)(kRows - kPieceRows);
+      static_assert(kSpan <= 128, "two row counts per lane");
+      const uint32_t ra = kRows - lane, rb = kRows - 64u - lane;
+      const uint32_t ha = lane < kSpan ? hist[ra] : 0u, hb = lane + 64u < kSpan ? hist[rb] : 0u;
+      const uint32_t ia = wave_incl_scan(ha, lane);  // tiles of at least ra rows
+      const uint32_t tot_a = __shfl(ia, 63, 64);
+      const uint32_t ib = tot_a + wave_incl_scan(hb, lane);
+      // from = the least row count whose tiles and all longer ones fit in cus
+      const unsigned long long fa = __ballot(lane < kSpan && ia <= x.cus);
+      const unsigned long long fb = __ballot(lane + 64u < kSpan && ib <= x.cus);
+      uint32_t fit = 0;  // tiles of at least `from` rows
+      if (fb) {
+        const uint32_t k = 63u - (uint32_t)__clzll(fb);  // the highest lane: the fewest rows
+        from = kRows - 64u - k;
+        fit = __shfl(ib, k, 64);
+      } else if (fa) {
+        const uint32_t k = 63u - (uint32_t)__clzll(fa);
+        from = kRows - k;
+        fit = __shfl(ia, k, 64);
+      }
+      left = x.cus - fit;
+      if (left) {
+        // the longest row count below from that has tiles (above kPieceRows)
+        const unsigned long long ta = __ballot(lane < kSpan && ra < from && ha > 0u);
+        const unsigned long long tb = __ballot(lane + 64u < kSpan && rb < from && hb > 0u);
+        if (ta)
+          take = kRows + 1u - (uint32_t)__ffsll((unsigned long long)ta);
+        else if (tb)
+          take = kRows - 63u - (uint32_t)__ffsll((unsigned long long)tb);
+      }
+    }
+    if (tid == 0) {
+      c_piece = piece;
+      c_from = from;
+      c_take = take;
+      c_left = take ? left : 0u;
+      c_fine = fine;
+    }
+  }
+  __syncthreads();
+  const uint32_t piece = c_piece, from = c_from, take = c_take, left = c_left;
+  const bool fine = c_fine != 0;
+
+  // rank in tile order of each segment's first tile of `take` rows
+  auto takes_of = [&](uint32_t m, uint32_t nt) -> uint32_t {
+    return (take == (uint32_t)kRows ? nt - 1 : 0u) + (tile_rows_of(m, nt - 1) == take ? 1u : 0u);
+  };
+  if (left) {
+    uint32_t mine = 0, all;
+    for (uint32_t s = s0; s < s1; s++)
+      if (!(info[s].flags & kSegSmall)) mine += takes_of(info[s].m, tiles_in(info[s].m));
+    uint32_t rank = block_scan(mine, wsum, &all);
+    for (uint32_t s = s0; s < s1; s++) {
+      info[s].tk = rank;
+      if (!(info[s].flags & kSegSmall)) rank += takes_of(info[s].m, tiles_in(info[s].m));
+    }
+    __syncthreads();
+  }
+  // The tiles of a segment are t = 0 .. nt - 1 from its end; all have kRows
+  // rows but the first, t = nt - 1, which has r1 rows.  A run [t0, t1) holds
+  // nf whole tiles (t < fe), of which the first nc are cut, and maybe the
+  // partial first tile.
+  struct RunPlan {
+    uint32_t nf, nc;  // whole tiles, cut whole tiles (a prefix of them)
+    bool part;        // holds the partial first tile
+    bool part_cut;
+    uint32_t r1;      // its rows
+  };
+  auto plan_run = [&](const SegInfo& v, uint32_t t0, uint32_t t1) -> RunPlan {
+    RunPlan q;
+    const uint32_t nt = tiles_in(v.m);
+    q.r1 = tile_rows_of(v.m, nt - 1);
+    const uint32_t fe = q.r1 == (uint32_t)kRows ? nt : nt - 1;  // whole tiles are t < fe
+    const uint32_t fend = min(t1, fe);
+    q.nf = fend > t0 ? fend - t0 : 0u;
+    // whole tiles are cut: all of them (a fine cut, or kRows >= from), else
+    // those whose rank among the tiles of `take` = kRows rows is below left
+    if (fine || (uint32_t)kRows >= from) {
+      q.nc = q.nf;
+    } else if (take == (uint32_t)kRows && left > v.tk) {
+      const uint32_t cend = min(fend, left - v.tk);  // t < left - tk
+      q.nc = cend > t0 ? cend - t0 : 0u;
+    } else {
+      q.nc = 0;
+    }
+    q.part = q.r1 < (uint32_t)kRows && nt - 1 >= t0 && nt - 1 < t1;
+    q.part_cut = q.part && (fine ? q.r1 > piece : (q.r1 >= from || (q.r1 == take && left > v.tk)));
+    return q;
+  };
+
+  // runs [r_lo, r_hi) of this thread, from the segment holding run r_lo;
+  // visit(s, v, t0, t1): tiles t0 .. t1 - 1 of segment s (values v)
+  const uint32_t r_lo = min(n_runs, tid * per_r), r_hi = min(n_runs, r_lo + per_r);
+  auto walk = [&](auto&& visit) {
+    if (r_lo >= r_hi) return;
+    uint32_t s = first_seg[tid];
+    SegInfo v = info[s];
+    uint32_t run = r_lo - v.rb;  // run of s
+    for (uint32_t k = r_lo; k < r_hi; k++) {
+      while ((v.flags & kSegSmall) || run * kRunTiles >= tiles_in(v.m)) {  // on to the next tiled segment
+        s++;
+        run = 0;
+        v = info[s];
+      }
+      const uint32_t t0 = run * kRunTiles;
+      visit(s, v, t0, min(tiles_in(v.m), t0 + kRunTiles));
+      run++;
+    }
+  };
+  // Count the entries by the rows each runs.  Uncut whole tiles (kRows
+  // rows) and whole pieces get slots by thread order, which is tile order;
+  // the other lengths (partial tiles, the remainders of cut tiles) by LDS
+  // atomics.
+  const uint32_t rem_full = piece ? (uint32_t)kRows % piece : 0u;  // remainder piece of a cut whole tile
+  uint32_t my_full = 0, my_pieces = 0;
+  walk([&](uint32_t s, const SegInfo& v, uint32_t t0, uint32_t t1) {
+    const RunPlan q = plan_run(v, t0, t1);
+    my_full += q.nf - q.nc;
+    if (q.nc) {
+      my_pieces += q.nc * ((uint32_t)kRows / piece);
+      if (rem_full) atomicAdd(&cursor[rem_full], q.nc);
+    }
+    if (q.part) {
+      if (!q.part_cut) {
+        atomicAdd(&cursor[q.r1], 1u);
+      } else {
+        my_pieces += q.r1 / piece;
+        if (q.r1 % piece) atomicAdd(&cursor[q.r1 % piece], 1u);
+      }
+    }
+    // a one-tile segment has one run: this thread owns its entry
+    if ((v.flags & kSegOneTile) && (q.nc || q.part_cut)) x.seg_cut[s] = 1u;
+  });
+  uint3 tot2;
+  const uint3 b2 = block_scan3(make_uint3(my_full, my_pieces, 0u), wsum3, &tot2);
+  const uint32_t full0 = b2.x, piece0 = b2.y, n_full = tot2.x, n_pieces = tot2.y;
+  if (tid < 64u) {  // start of each length's run, longest first: lane k holds rows kRows - k and kRows - 64 - k
+    const uint32_t ka = kRows - lane, kb = kRows - 64u - lane;
+    const bool has_b = kRows > 64 + (int)lane;
+    const uint32_t ca = cursor[ka] + (ka == (uint32_t)kRows ? n_full : 0u) + (ka == piece ? n_pieces : 0u);
+    const uint32_t cb = has_b ? cursor[kb] + (kb == piece ? n_pieces : 0u) : 0u;
+    const uint32_t ia = wave_incl_scan(ca, lane), tot_a = __shfl(ia, 63, 64);
+    const uint32_t ib = tot_a + wave_incl_scan(cb, lane);
+    // the atomics of a length start after its slots taken in thread order
+    cursor[ka] = ia - ca + (ka == (uint32_t)kRows ? n_full : 0u) + (ka == piece ? n_pieces : 0u);
+    if (has_b) cursor[kb] = ib - cb + (kb == piece ? n_pieces : 0u);
+    if (ka == (uint32_t)kRows) c_full_at = ia - ca;  // first slot of the whole tiles
+    if (ka == piece) c_piece_at = ia - ca;           // first slot of the whole pieces
+    if (has_b && kb == piece) c_piece_at = ib - cb;
+    if (lane == 63u) c_ents = ib;
+  }
+  __syncthreads();
+  uint32_t at_full = c_full_at + full0, at_piece = (n_pieces ? c_piece_at : 0u) + piece0;
+  walk([&](uint32_t s, const SegInfo& v, uint32_t t0, uint32_t t1) {
+    const RunPlan q = plan_run(v, t0, t1);
+    const uint32_t user = v.user, g0 = v.tb;
+    auto put = [&](uint32_t pos, uint32_t t, uint32_t r0, uint32_t r1) {
+      if (pos < x.cap) x.order[pos] = TileEnt{g0 + t, s, t | (r0 << 16) | (r1 << 24), user};
+    };
+    // pieces [r1 - piece, r1) from the tile's end down; the lowest may start
+    // below the tile's first row lo
+    auto pieces = [&](uint32_t t, uint32_t rows) {
+      const uint32_t lo = (uint32_t)kRows - rows;
+      for (uint32_t r1 = kRows; r1 > lo; r1 -= min(r1, piece)) {
+        const uint32_t r0 = r1 > piece ? r1 - piece : 0u, len = r1 - max(r0, lo);
+        put(len == piece ? at_piece++ : atomicAdd(&cursor[len], 1u), t, r0, r1);
+      }
+    };
+    // a cut whole tile: kRows / piece whole pieces, then the remainder, if any
+    const uint32_t per_tile = q.nc ? (uint32_t)kRows / piece : 0u;
+    for (uint32_t t = t0; t < t0 + q.nc; t++) {
+      for (uint32_t k = 0; k < per_tile; k++) put(at_piece++, t, kRows - (k + 1) * piece, kRows - k * piece);
+      if (rem_full) put(atomicAdd(&cursor[rem_full], 1u), t, 0u, rem_full);
+    }
+    for (uint32_t t = t0 + q.nc; t < t0 + q.nf; t++) put(at_full++, t, 0u, kRows);
+    if (q.part) {
+      const uint32_t t = tiles_in(v.m) - 1;
+      if (q.part_cut)
+        pieces(t, q.r1);
+      else
+        put(atomicAdd(&cursor[q.r1], 1u), t, 0u, kRows);
+    }
+  });
+  const uint32_t ents = c_ents;
+  for (uint32_t k = ents + tid; k < x.cap; k += nt_) x.order[k] = TileEnt{kNoTile, 0u, 0u, 0u};
+  if (tid == 0 && x.n_ents) *x.n_ents = ents;
+}
+
+// The expansion alone, for the library's test hook.
+__global__ __launch_bounds__(kExpandThreads) void k_expand(const SegBrief* brief, uint32_t n, ExpandArgs x) {
+  expand_tables(brief, n, x);
+}
+
+// ---------------------------------------------------------------------------
+// First kernel of a call.  It copies the call's staged tables (descriptors,
+// zero ranges, zeroed queue head, block ids) from the mapped host ring into
+// device scratch, zeroes the tile partials, settles every segment's first
+// verdict -- with labels, the owner check (OWNER_MIXED iff some row label
+// differs from the segment's user; the sentinels never equal a user), else
+// OK -- and forms E_K(J0) xor H*L of one-tile segments.  With an expansion,
+// workgroup 0 builds the tile tables and the work queue meanwhile from the
+// brief records; the other workgroups read descriptors and block ids where
+// the copy reads them, so no part waits on another.
+// ---------------------------------------------------------------------------
+struct PrologueArgs {
+  uint4* dst;
+  const uint4* src;  // nullptr: the tables are in dst already
+  size_t n16;        // 16-byte words of staged tables
+  const SegDesc* segs;  // where the descriptors are readable now (src or dst)
+  uint32_t n;
+  const uint32_t* labels;
+  const uint32_t* bids;
+  int32_t* verdicts;
+  KeyTableDev kt;
+  uint4* fin;
+  uint4* zero;
+  uint32_t n_zero;
+  bool expand;
+  const SegBrief* brief;  // where the brief records are readable now
+  ExpandArgs x;
+};
+
+__global__ __launch_bounds__(kPrologueThreads) void k_prologue(PrologueArgs a) {
   __shared__ uint32_t te[256];
-  const size_t gsz = (size_t)gridDim.x * blockDim.x;
-  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += gsz) dst[i] = src[i];
-  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n_zero; i += gsz)
-    zero[i] = make_uint4(0u, 0u, 0u, 0u);
-  if (!verdicts) return;
-  if (fin) {
+  const bool ex = a.expand && a.n > 0;
+  if (ex && blockIdx.x == 0) {
+    expand_tables(a.brief, a.n, a.x);
+    if (gridDim.x > 1) return;  // the other workgroups do the rest
+    __syncthreads();
+  }
+  // the other workgroups (all of them without an expansion, or workgroup 0
+  // after it when it is alone)
+  const bool sep = ex && gridDim.x > 1;
+  const uint32_t wg = sep ? blockIdx.x - 1 : blockIdx.x, n_wg = sep ? gridDim.x - 1 : gridDim.x;
+  const size_t gsz = (size_t)n_wg * blockDim.x, me = (size_t)wg * blockDim.x + threadIdx.x;
+  if (a.src)
+    for (size_t i = me; i < a.n16; i += gsz) a.dst[i] = a.src[i];
+  for (size_t i = me; i < a.n_zero; i += gsz) a.zero[i] = make_uint4(0u, 0u, 0u, 0u);
+  if (!a.verdicts) return;
+  const SegDesc* segs = a.segs;
+  if (a.fin) {
     for (uint32_t i = threadIdx.x; i < 256u; i += blockDim.x) te[i] = c_aes.te0[i];
     __syncthreads();
   }
-  for (uint32_t s = blockIdx.x; s < n; s += gridDim.x) {
-    if (fin && threadIdx.x < 64u && (segs[s].flags & kSegOneTile)) {
+  for (uint32_t s = wg; s < a.n; s += n_wg) {
+    if (a.fin && threadIdx.x < 64u && (segs[s].flags & kSegOneTile)) {
       // GCM a one-tile segment needs besides its tile: E_K(J0) xor H*L,
       // J0 = IV || BE32(1), H*L a wave sum over the set bits of the length
       // block (only its low 64 bits can be set) of the products H*x^(64+k)
       const uint32_t lane = threadIdx.x, user = segs[s].user;
       u128 z = u128_zero();
-      if (((segs[s].len * 8ull) >> (63 - lane)) & 1ull) z = ld_u128(kt.pow_hxl + (size_t)user * kHxLanes + lane);
+      if (((segs[s].len * 8ull) >> (63 - lane)) & 1ull) z = ld_u128(a.kt.pow_hxl + (size_t)user * kHxLanes + lane);
 #pragma unroll
       for (int j = 0; j < 4; j++) z.w[j] = wave_xor(z.w[j]);
       if (lane == 0) {
         const uint32_t j0[4] = {segs[s].iv[0], segs[s].iv[1], segs[s].iv[2], 0x01000000u};
         uint32_t e[4];
-        aes256_encrypt_tab(kt.rk + (size_t)user * 64u, j0, e, te);
-        fin[s] = make_uint4(e[0] ^ z.w[0], e[1] ^ z.w[1], e[2] ^ z.w[2], e[3] ^ z.w[3]);
+        aes256_encrypt_tab(a.kt.rk + (size_t)user * 64u, j0, e, te);
+        a.fin[s] = make_uint4(e[0] ^ z.w[0], e[1] ^ z.w[1], e[2] ^ z.w[2], e[3] ^ z.w[3]);
       }
     }
     int bad = 0;
-    if (labels) {
+    if (a.labels) {
       const uint64_t rb = segs[s].row_begin, rc = segs[s].row_count;
       const uint32_t user = segs[s].user;
-      for (uint64_t r = threadIdx.x; r < rc; r += blockDim.x) bad |= labels[bids ? bids[rb + r] : rb + r] != user;
+      for (uint64_t r = threadIdx.x; r < rc; r += blockDim.x) bad |= a.labels[a.bids ? a.bids[rb + r] : rb + r] != user;
       bad = __syncthreads_or(bad);
     }
-    if (threadIdx.x == 0) verdicts[s] = bad ? kVerdictOwnerMixed : kVerdictOk;
+    if (threadIdx.x == 0) a.verdicts[s] = bad ? kVerdictOwnerMixed : kVerdictOk;
   }
 }
 
@@ -816,15 +1246,17 @@ __global__ __launch_bounds__(256) void k_chunk_table(const SegDesc* __restrict__
   }
 }
 
-// Open through block tables: zero the chunks of requests that failed
-// authentication (their blocks passed the label check, so they are the
-// request's own; a request rejected by the label check writes nothing).  A
-// workgroup takes whole tiles of kTileBlocks blocks (the GCM kernel's tiles,
-// found through tile_base), so the work per workgroup is bounded.
-__global__ __launch_bounds__(256) void k_zero_chunks(const SegDesc* __restrict__ segs, uint32_t n,
+// Open: zero the output of segments that failed, tile by tile.  A workgroup
+// takes whole tiles of kTileBlocks blocks (the GCM kernel's tiles, found
+// through tile_base), so the work per workgroup is bounded.  Contiguous
+// output (chunk_off == nullptr): every segment whose verdict is not OK.
+// Through block tables: only requests that failed authentication -- their
+// blocks passed the label check, so they are the request's own; a request
+// rejected by the label check writes nothing.
+__global__ __launch_bounds__(256) void k_zero_failed(const SegDesc* __restrict__ segs, uint32_t n,
                                                      const uint32_t* __restrict__ tile_base, uint32_t n_tiles,
                                                      const int32_t* __restrict__ verdicts,
-                                                     const uint64_t* __restrict__ chunk_off, uint8_t* pbase,
+                                                     const uint64_t* __restrict__ chunk_off, uint8_t* base,
                                                      uint32_t chunk_shift) {
   const uint64_t cmask = (1ull << chunk_shift) - 1;
   for (uint32_t g = blockIdx.x; g < n_tiles; g += gridDim.x) {
@@ -836,14 +1268,26 @@ __global__ __launch_bounds__(256) void k_zero_chunks(const SegDesc* __restrict__
       else
         hi = mid;
     }
-    if (verdicts[lo] != kVerdictAuthFail) continue;
-    const uint64_t m = segs[lo].nblocks, c0 = segs[lo].chunk0;
+    const int32_t v = verdicts[lo];
+    if (chunk_off ? v != kVerdictAuthFail : v == kVerdictOk) continue;
+    const uint64_t m = segs[lo].nblocks;
     const uint64_t t = g - tile_base[lo];
     // tiles are aligned to the end of the segment, as in k_gcm_tiles
     const uint64_t end = m - t * (uint64_t)kTileBlocks;
     const uint64_t begin = end > kTileBlocks ? end - kTileBlocks : 0;
-    for (uint64_t i = begin + threadIdx.x; i < end; i += blockDim.x)
-      *(uint4*)(pbase + chunk_off[c0 + (i >> chunk_shift)] + ((i & cmask) << 4)) = make_uint4(0u, 0u, 0u, 0u);
+    if (chunk_off) {
+      const uint64_t c0 = segs[lo].chunk0;
+      for (uint64_t i = begin + threadIdx.x; i < end; i += blockDim.x)
+        *(uint4*)(base + chunk_off[c0 + (i >> chunk_shift)] + ((i & cmask) << 4)) = make_uint4(0u, 0u, 0u, 0u);
+    } else {
+      const uint64_t len = segs[lo].len;
+      uint8_t* p = base + segs[lo].byte_off;
+      const bool aligned = (segs[lo].flags & kSegAligned) != 0;
+      for (uint64_t i = begin + threadIdx.x; i < end; i += blockDim.x) {
+        const uint64_t rem = len - 16ull * i;
+        store_block(p + 16ull * i, u128_zero(), rem >= 16 ? 16u : (uint32_t)rem, aligned);
+      }
+    }
   }
 }
 
@@ -996,33 +1440,57 @@ hipError_t launch_chunk_table(const SegDesc* segs, uint32_t n_segs, const uint32
   return hipGetLastError();
 }
 
-hipError_t launch_zero_chunks(const SegDesc* segs, uint32_t n_segs, const uint32_t* tile_base, uint32_t n_tiles,
-                              const int32_t* verdicts, const uint64_t* chunk_off, uint8_t* pbase,
-                              uint32_t chunk_shift, uint32_t grid, hipStream_t s) {
+hipError_t launch_zero_failed(const SegDesc* segs, uint32_t n_segs, const uint32_t* tile_base, uint32_t n_tiles,
+                              const int32_t* verdicts, const uint64_t* chunk_off, uint8_t* base, uint32_t chunk_shift,
+                              uint32_t grid, hipStream_t s) {
   if (n_segs == 0 || n_tiles == 0) return hipSuccess;
   if (grid > n_tiles) grid = n_tiles;
-  hipLaunchKernelGGL(k_zero_chunks, dim3(grid), dim3(256), 0, s, segs, n_segs, tile_base, n_tiles, verdicts,
-                     chunk_off, pbase, chunk_shift);
+  hipLaunchKernelGGL(k_zero_failed, dim3(grid), dim3(256), 0, s, segs, n_segs, tile_base, n_tiles, verdicts,
+                     chunk_off, base, chunk_shift);
   return hipGetLastError();
 }
 
 
+hipError_t launch_expand(const SegBrief* brief, uint32_t n_segs, const ExpandArgs& x, hipStream_t s) {
+  if (n_segs == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_expand, dim3(1), dim3(kExpandThreads), 0, s, brief, n_segs, x);
+  return hipGetLastError();
+}
+
 hipError_t launch_prologue(void* dst, const void* src, size_t bytes, uint32_t n_segs, uint64_t bids_off,
                            const uint32_t* labels, int32_t* verdicts, const KeyTableDev* kt, uint4* fin,
-                           uint4* zero, uint32_t n_zero, hipStream_t s) {
+                           uint4* zero, uint32_t n_zero, uint64_t brief_off, const ExpandArgs* ex, hipStream_t s) {
   if (bytes & 15u) return hipErrorInvalidValue;
   const size_t n16 = src ? bytes / 16 : 0;
-  if (n16 == 0 && !verdicts && n_zero == 0) return hipSuccess;
+  const bool expand = ex != nullptr && n_segs > 0;
+  if (n16 == 0 && !verdicts && n_zero == 0 && !expand) return hipSuccess;
   if (n16 && (((uintptr_t)dst | (uintptr_t)src) & 15u)) return hipErrorInvalidValue;
+  if (expand && (brief_off & 15u || brief_off + 8ull * (n_segs + 1) > bytes)) return hipErrorInvalidValue;
   const uint8_t* rd = src ? (const uint8_t*)src : (const uint8_t*)dst;  // where the tables are readable now
-  uint64_t grid = cdiv(n16 > n_zero ? n16 : n_zero, 256u);
+  uint64_t grid = cdiv(n16 > n_zero ? n16 : n_zero, kPrologueThreads);
   if (verdicts && n_segs > grid) grid = n_segs;
   if (grid > 1024u) grid = 1024u;
   if (grid == 0) grid = 1;
-  hipLaunchKernelGGL(k_prologue, dim3((uint32_t)grid), dim3(256), 0, s, (uint4*)dst, (const uint4*)src, n16,
-                     (const SegDesc*)rd, n_segs, labels,
-                     bids_off == kNoBids ? (const uint32_t*)nullptr : (const uint32_t*)(rd + bids_off), verdicts,
-                     kt ? *kt : KeyTableDev{}, kt ? fin : nullptr, zero, n_zero);
+  if (expand) grid += 1;  // workgroup 0 expands the segment table
+  PrologueArgs a{};
+  a.dst = (uint4*)dst;
+  a.src = (const uint4*)src;
+  a.n16 = n16;
+  a.segs = (const SegDesc*)rd;
+  a.n = n_segs;
+  a.labels = labels;
+  a.bids = bids_off == kNoBids ? nullptr : (const uint32_t*)(rd + bids_off);
+  a.verdicts = verdicts;
+  a.kt = kt ? *kt : KeyTableDev{};
+  a.fin = kt ? fin : nullptr;
+  a.zero = zero;
+  a.n_zero = n_zero;
+  a.expand = expand;
+  if (expand) {
+    a.x = *ex;
+    a.brief = (const SegBrief*)(rd + brief_off);
+  }
+  hipLaunchKernelGGL(k_prologue, dim3((uint32_t)grid), dim3(kPrologueThreads), 0, s, a);
   return hipGetLastError();
 }
 

@@ -1,20 +1,27 @@
-"""Host logic of the per-block kernel's work queue (no GPU): the fine cut of
-short queues and the order of tiles and pieces, called through the
-library's internal C++ entry points on random segment tables.
+"""The work queue the segment-table expansion kernel builds on the device,
+called through the library's internal test hook on random segment tables.
 
-What the kernel relies on: every tile's rows that hold blocks are covered
-exactly once by its entries; a tile that is cut has no whole-tile entry (a
-whole tile stores its GHASH partial, pieces XOR theirs into it); entries
-come longest first; a one-tile segment whose tile is cut loses its one-tile
-flag and counts as a multi-entry segment; the entries fit the capacity the
-host allocates."""
+What the GCM kernels rely on: tile_base is the exclusive scan of each
+segment's tiles and the small list names the small segments in order; every
+tile's rows that hold blocks are covered exactly once by its entries; a tile
+that is cut has no whole-tile entry (a whole tile stores its GHASH partial,
+pieces XOR theirs into it); entries come longest first and the queue is
+padded with empty entries up to its capacity; the tiles cut are the ones the
+rule names (with fewer tiles than CUs every tile longer than ceil(rows /
+CUs); otherwise up to one per CU, the largest longer than a quarter tile);
+a one-tile segment whose tile is cut is marked cut (its tag comes from the
+finalize pass)."""
 import ctypes
 import subprocess
 
 import numpy as np
 import pytest
 
-from paper_2608_25431_amd import gift
+torch = pytest.importorskip("torch")
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU")]
+
+from paper_2608_25431_amd import gift  # noqa: E402
 
 # compile-time constants of the library (gift_internal.hpp)
 THREADS, ROWS = 1024, 128
@@ -22,6 +29,7 @@ TILE_BLOCKS = THREADS * ROWS
 PIECE_ROWS = ROWS // 4
 SMALL_MAX_BLOCKS = 64
 SEG_SMALL, SEG_ONE_TILE = 2, 4
+NO_TILE = 0xFFFFFFFF
 
 SEGDESC = np.dtype([("byte_off", "<u8"), ("len", "<u8"), ("row_begin", "<u8"), ("row_count", "<u8"),
                     ("iv", "<u4", 3), ("user", "<u4"), ("nblocks", "<u4"), ("flags", "<u4"), ("chunk0", "<u8")])
@@ -30,21 +38,15 @@ assert SEGDESC.itemsize == 64 and TILEENT.itemsize == 16
 
 
 @pytest.fixture(scope="module")
-def planner():
-    if not __import__("os").path.exists(gift.LIB_PATH):
-        from paper_2608_25431_amd import build
-        build.build()
+def expand():
     lib = gift.lib()
     out = subprocess.run(["nm", "-D", "--defined-only", gift.LIB_PATH], capture_output=True, text=True).stdout
     names = [l.split()[-1] for l in out.splitlines() if l.strip()]
-    cuts = getattr(lib, next(n for n in names if n.startswith("_ZN4gift9plan_cuts")))
-    order = getattr(lib, next(n for n in names if n.startswith("_ZN4gift10tile_order")))
-    cuts.argtypes = [ctypes.c_void_p, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint32,
-                     ctypes.POINTER(ctypes.c_uint32), ctypes.c_void_p]
-    cuts.restype = ctypes.c_uint32
-    order.argtypes = [ctypes.c_void_p, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_void_p, ctypes.c_void_p]
-    order.restype = ctypes.c_uint32
-    return cuts, order
+    fn = getattr(lib, next(n for n in names if n.startswith("_ZN4gift15expand_for_test")))
+    P, U32 = ctypes.c_void_p, ctypes.c_uint32
+    fn.argtypes = [P, U32, U32, P, P, P, P, U32, ctypes.POINTER(U32)]
+    fn.restype = ctypes.c_int
+    return fn
 
 
 def descs_of(nblocks, rng):
@@ -63,31 +65,54 @@ def tile_rows(m, t):
     return ROWS if missing <= 0 else ROWS - missing // THREADS
 
 
-def plan(planner, d, cus):
-    plan_cuts, tile_order = planner
+def plan(expand, d, cus):
+    """Runs the expansion kernel; returns the tile count, the flags before,
+    the segments left with more than one entry, the piece rows, which tiles
+    are cut, the entries, tile_base and the small list.  d's one-tile flag is
+    cleared where the kernel marks the segment cut."""
     n = len(d)
     n_tiles = int(sum(-(-int(m) // TILE_BLOCKS) for m, f in zip(d["nblocks"], d["flags"]) if not f & SEG_SMALL))
     flags0 = d["flags"].copy()
-    n_multi = ctypes.c_uint32(int(sum(1 for f in flags0 if not f & (SEG_SMALL | SEG_ONE_TILE))))
-    cut = np.full(max(n_tiles, 1), 7, np.uint8)
-    piece = plan_cuts(d.ctypes.data, n, n_tiles, cus, ctypes.byref(n_multi), cut.ctypes.data)
     cap = n_tiles + (ROWS // PIECE_ROWS - 1) * cus
-    order = np.zeros(max(cap, 1) + 8, TILEENT)
-    order[cap:]["g"] = 0xDEADBEEF  # guard entries past the capacity
-    n_ents = tile_order(d.ctypes.data, n, piece, cut.ctypes.data, order.ctypes.data) if n_tiles else 0
-    assert (order[cap:]["g"] == 0xDEADBEEF).all()
-    return n_tiles, flags0, n_multi.value, piece, cut[:n_tiles], order[:n_ents]
+    seg_cut = np.full(n, 0xEEEEEEEE, np.uint32)
+    tile_base = np.full(n + 1, 0xEEEEEEEE, np.uint32)
+    small = np.full(n, 0xEEEEEEEE, np.uint32)
+    order = np.zeros(max(cap, 1), TILEENT)
+    n_ents = ctypes.c_uint32(0)
+    assert expand(d.ctypes.data, n, cus, seg_cut.ctypes.data, tile_base.ctypes.data, small.ctypes.data,
+                  order.ctypes.data, cap, ctypes.byref(n_ents)) == 0
+    ne = n_ents.value
+    assert ne <= cap
+    assert (order[ne:cap]["g"] == NO_TILE).all(), "the queue is padded with empty entries"
+    assert set(np.unique(seg_cut)) <= {0, 1}
+    # a one-tile segment whose tile is cut takes the multi-entry path
+    d["flags"] = np.where(seg_cut == 1, d["flags"] & ~np.uint32(SEG_ONE_TILE), d["flags"])
+    ents = order[:ne]
+    r0, r1 = (ents["trow"] >> 16) & 0xFF, ents["trow"] >> 24
+    whole = (r0 == 0) & (r1 == ROWS)
+    cut = np.zeros(max(n_tiles, 1), np.uint8)
+    cut[ents["g"][~whole]] = 1
+    piece = int((r1 - r0)[~whole].max()) if (~whole).any() else 0
+    n_multi = sum(1 for i in range(n) if not d["flags"][i] & (SEG_SMALL | SEG_ONE_TILE))
+    return n_tiles, flags0, n_multi, piece, cut[:n_tiles], ents, tile_base, small
 
 
-def check(d, cus, n_tiles, flags0, n_multi, piece, cut, ents):
+def check(d, cus, n_tiles, flags0, n_multi, piece, cut, ents, tile_base_dev, small_dev):
     segs = [i for i in range(len(d)) if not flags0[i] & SEG_SMALL]
     tile_base, rows, g = {}, [], 0
-    for i in segs:
+    exp_tb = []
+    for i in range(len(d)):
+        exp_tb.append(g)
+        if i not in set(segs):
+            continue
         tile_base[i] = g
         nt = -(-int(d["nblocks"][i]) // TILE_BLOCKS)
         rows += [tile_rows(int(d["nblocks"][i]), t) for t in range(nt)]
         g += nt
     assert g == n_tiles
+    assert tile_base_dev.tolist() == exp_tb + [n_tiles], "tile_base: exclusive scan of tiles per segment"
+    small_segs = [i for i in range(len(d)) if flags0[i] & SEG_SMALL]
+    assert small_dev[:len(small_segs)].tolist() == small_segs, "the small segments, in table order"
     rows = np.array(rows, np.int64)
     assert set(np.unique(cut)) <= {0, 1}
     cut = cut.astype(bool)
@@ -121,6 +146,14 @@ def check(d, cus, n_tiles, flags0, n_multi, piece, cut, ents):
         run.append(b - a)
         covered.setdefault(int(ents["g"][k]), []).append((a, b, int(r0[k]), int(r1[k]), lo))
     assert run == sorted(run, reverse=True), "longest entries first"
+    # whole uncut tiles (the bulk of a long call) come in tile order, and so
+    # do the whole pieces of cut tiles, each tile's from its end down
+    gk = [int(ents["g"][k]) for k in range(len(ents)) if run[k] == ROWS]
+    assert gk == sorted(gk), "whole tiles in tile order"
+    if piece:
+        whole = [(int(ents["g"][k]), -int(r1[k])) for k in range(len(ents))
+                 if run[k] == piece and cut[int(ents["g"][k])] and int(r1[k]) - int(r0[k]) == piece]
+        assert whole == sorted(whole), "whole pieces in tile order"
     assert len(covered) == n_tiles
     for gg, parts in covered.items():
         parts.sort()
@@ -134,11 +167,10 @@ def check(d, cus, n_tiles, flags0, n_multi, piece, cut, ents):
             assert all((ROWS - p[3]) % piece == 0 and p[3] - p[2] <= piece for p in parts), "pieces end-aligned"
         else:
             assert len(parts) == 1 and parts[0][2:4] == (0, ROWS)
-    # one-tile flags: kept unless the tile was cut; the multi-entry count follows
+    # cut marks: exactly the one-tile segments whose tile was cut
     for i in segs:
         had = bool(flags0[i] & SEG_ONE_TILE)
         assert bool(d["flags"][i] & SEG_ONE_TILE) == (had and not cut[tile_base[i]])
-    assert n_multi == sum(1 for i in segs if not d["flags"][i] & SEG_ONE_TILE)
 
 
 REGIMES = {
@@ -153,33 +185,33 @@ REGIMES = {
 
 @pytest.mark.parametrize("regime", sorted(REGIMES))
 @pytest.mark.parametrize("cus", [256, 64, 7, 1])
-def test_queue_covers_every_row_once_longest_first(planner, regime, cus):
+def test_queue_covers_every_row_once_longest_first(expand, regime, cus):
     rng = np.random.default_rng(1000 * sorted(REGIMES).index(regime) + cus)
-    for n in (1, 2, 5, 33, 200):
+    for n in (1, 2, 5, 33, 200, 3000):
         d = descs_of(REGIMES[regime](rng, n), rng)
-        res = plan(planner, d, cus)
+        res = plan(expand, d, cus)
         check(d, cus, *res)
 
 
-def test_single_small_tile_is_cut_across_the_device(planner):
+def test_single_small_tile_is_cut_across_the_device(expand):
     # a 1.5 MiB segment (96 tile rows) on 256 CUs: 96 one-row pieces
     d = descs_of(np.array([96 * THREADS]), np.random.default_rng(1))
-    n_tiles, flags0, n_multi, piece, cut, ents = plan(planner, d, 256)
+    n_tiles, flags0, n_multi, piece, cut, ents, _, _ = plan(expand, d, 256)
     assert (n_tiles, piece, len(ents), n_multi) == (1, 1, 96, 1)
     assert not d["flags"][0] & SEG_ONE_TILE
 
 
-def test_full_device_queue_of_short_tiles_is_not_cut(planner):
+def test_full_device_queue_of_short_tiles_is_not_cut(expand):
     # as many short tiles as CUs: nothing to cut, one-tile segments keep their path
     d = descs_of(np.full(256, 3 * THREADS + 5), np.random.default_rng(2))
-    n_tiles, flags0, n_multi, piece, cut, ents = plan(planner, d, 256)
+    n_tiles, flags0, n_multi, piece, cut, ents, _, _ = plan(expand, d, 256)
     assert piece == 0 and len(ents) == 256 and n_multi == 0
     assert (d["flags"] & SEG_ONE_TILE).all()
 
 
-def test_one_tile_segments_past_the_cu_count_share_the_tail(planner):
+def test_one_tile_segments_past_the_cu_count_share_the_tail(expand):
     # 300 one-tile segments of 96 rows on 256 CUs: 256 of them are cut into
     # three pieces, so no CU runs two whole tiles while others idle
     d = descs_of(np.full(300, 96 * THREADS), np.random.default_rng(3))
-    n_tiles, flags0, n_multi, piece, cut, ents = plan(planner, d, 256)
+    n_tiles, flags0, n_multi, piece, cut, ents, _, _ = plan(expand, d, 256)
     assert (piece, int(cut.sum()), len(ents), n_multi) == (PIECE_ROWS, 256, 44 + 3 * 256, 256)
