@@ -81,6 +81,14 @@ __device__ __forceinline__ uint32_t xor_and(uint32_t a, uint32_t b, uint32_t c) 
   return __builtin_amdgcn_bitop3_b32(a, b, c, 0x78);
 }
 
+// x, unknown to the optimiser from here on: values derived from it are
+// computed where they are used, not hoisted across a loop and held in
+// registers (or spilled) until then
+__device__ __forceinline__ uint32_t opaque(uint32_t x) {
+  asm volatile("" : "+v"(x));
+  return x;
+}
+
 // ---------------------------------------------------------------------------
 // AES-256 key schedule (FIPS-197 Sec. 5.2, Nk = 8, Nr = 14).  Words are
 // little-endian u32 of the schedule bytes, so word c of round r XORs
@@ -339,7 +347,10 @@ __device__ inline u128 gf_mul_wave(const u128& x, const u128& y, uint32_t lane) 
     v1 = __builtin_amdgcn_alignbit(v0, v1, 8);
     v0 = xor3(xor3(v0 >> 8, t << 17, t << 22), t << 23, t << 24);
   }
-  const uint32_t xb = lane < 16u ? (x.w[n >> 2] >> (8u * (n & 3u))) & 0xFFu : 0u;  // byte n of x
+  // byte n of x, by shifts of its two halves (an index into x.w would go
+  // through private memory)
+  const uint64_t lo = ((uint64_t)x.w[1] << 32) | x.w[0], hi = ((uint64_t)x.w[3] << 32) | x.w[2];
+  const uint32_t xb = lane < 16u ? (uint32_t)(((n & 8u) ? hi : lo) >> (8u * (n & 7u))) & 0xFFu : 0u;
   uint32_t z0 = 0, z1 = 0, z2 = 0, z3 = 0;
 #pragma unroll
   for (int j = 0; j < 8; j++) {

@@ -329,9 +329,10 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
   // thread kPf0 + j: j < 512 tables; 512 + i descriptor word i (i < 16);
   // 528 + i round-key word i (i < 64); 592 entry and verdict; 593 fin
   auto prefetch = [&](uint32_t k) {
-    const uint32_t j = tid - kPf0;
+    const uint32_t j = opaque(tid) - kPf0;
     const TileEnt e = k < a.n_ents ? a.tile_order[k] : TileEnt{kNoTile, 0u, 0u, 0u};
     pf_tabs = false;
+    pf_w = make_uint4(0u, 0u, 0u, 0u);  // dead until the next prefetch: not carried across a tile
     if (j == 592u) {
       ti->g = e.g;
       ti->s = e.s;
@@ -366,7 +367,11 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
     __syncthreads();  // the tile's record and tables are in LDS; the previous tile is done with them
     const uint32_t g = __builtin_amdgcn_readfirstlane(ti->g);
     if (g == kNoTile) break;
-    if (tid == kPf0) claim = gridDim.x + atomicAdd(a.tile_counter, 1u);
+    // the thread index, recomputed per tile: per-lane values derived from it
+    // are formed here, not hoisted to the kernel's start and held (or
+    // spilled) across every tile
+    const uint32_t tid_t = opaque(tid);
+    if (tid_t == kPf0) claim = gridDim.x + atomicAdd(a.tile_counter, 1u);
     const uint32_t s = __builtin_amdgcn_readfirstlane(ti->s);
     const uint32_t trow = __builtin_amdgcn_readfirstlane(ti->trow);
     const uint32_t t = trow & 0xFFFFu;                                      // tile of the segment
@@ -380,7 +385,7 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
     const bool aligned = (flags & kSegAligned) != 0;
     // a one-tile segment whose tile is cut into pieces gets its tag from the finalize pass
     const bool one = (flags & kSegOneTile) != 0 && r0 == 0 && r1 == kRows;
-    if (one && tid == 0) red[kLeaders] = u128{{ti->fin.x, ti->fin.y, ti->fin.z, ti->fin.w}};  // for the tile end
+    if (one && tid_t == 0) red[kLeaders] = u128{{ti->fin.x, ti->fin.y, ti->fin.z, ti->fin.w}};  // for the tile end
     const int64_t base = (int64_t)m - (int64_t)(t + 1) * (int64_t)kTileBlocks;  // block index of virtual slot 0
     const int r_start = base < 0 ? (int)((uint64_t)(-base) / kThreads) : 0;
     const int r_lo = r_start > r0 ? r_start : r0;
@@ -409,7 +414,7 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
       // names a block of another owner, which keeps its contents.
       if (!SCATTER) {
         for (int r = r_lo; r < r1; r++) {
-          const int64_t i0 = base + (int64_t)r * kThreads + tid;
+          const int64_t i0 = base + (int64_t)r * kThreads + tid_t;
           if (i0 >= 0) {
             const uint64_t rem = len - 16ull * (uint64_t)i0;
             store_block(a.out + off + 16ull * (uint64_t)i0, u128_zero(), rem >= 16 ? 16u : (uint32_t)rem, aligned);
@@ -418,7 +423,7 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
       }
     } else {
       CtrCache cc;
-      const uint32_t c0 = 2u + (uint32_t)(base + (int64_t)tid);  // counter of this lane in row 0, mod 2^32
+      const uint32_t c0 = 2u + (uint32_t)(base + (int64_t)tid_t);  // counter of this lane in row 0, mod 2^32
       ctr_cache_init(cc, k0, k1, k2, c0, rk, tt, L);
 
       // rows where every lane holds a whole block and the segment is 16-byte
@@ -432,7 +437,7 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
       // starts
       constexpr bool PAGED = GATHER || SCATTER;
       auto chunk_of = [&](int r) -> uint64_t {
-        const uint64_t i0 = (uint64_t)(base + (int64_t)r * kThreads + tid);
+        const uint64_t i0 = (uint64_t)(base + (int64_t)r * kThreads + tid_t);
         return a.chunk_off[chunk0 + (i0 >> a.chunk_shift)];
       };
       uint64_t c_next = (PAGED && whole(r_lo)) ? chunk_of(r_lo) : 0;
@@ -449,7 +454,7 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
         if (fast) {
           // every lane's block index is >= 0 in these rows; pointer arithmetic
           // (not integers) keeps the global address space for the compiler
-          const uint64_t i0 = (uint64_t)(base + (int64_t)r * kThreads + tid);
+          const uint64_t i0 = (uint64_t)(base + (int64_t)r * kThreads + tid_t);
           uint8_t* pg = a.pbase + c_cur + ((i0 & cmask) << 4);
           src = GATHER ? pg : a.in + off + 16ull * i0;
           dst = SCATTER ? pg : a.out + off + 16ull * i0;
@@ -465,7 +470,7 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
           x = OPEN ? u128{{v.x, v.y, v.z, v.w}} : u128{{o.x, o.y, o.z, o.w}};
         } else {
           x = u128_zero();
-          const int64_t i0 = base + (int64_t)r * kThreads + tid;
+          const int64_t i0 = base + (int64_t)r * kThreads + tid_t;
           if (i0 >= 0) {
             const uint64_t boff = off + 16ull * (uint64_t)i0;
             const uint64_t rem = len - 16ull * (uint64_t)i0;
@@ -483,14 +488,17 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
       }
     }  // verdict OK
 
-    // Tile partial: lane tid contributes y * H^(kThreads + 1 - tid), its
+    // Tile partial: lane tid_t contributes y * H^(kThreads + 1 - tid_t), its
     // distance from the tile end plus the H^2 that every block's GHASH term
     // carries.  Wave w = g + kLeaders*i (leader g, i < kFold) needs
     // H^(64*kLeaders*(kFold - 1 - i)) * H^(64*kLeaders + 1 - 64*g - lane): leader
     // g folds its waves by Horner in W = H^(64*kLeaders) from the LDS tables,
     // then multiplies once by the per-lane power.
     const bool fold = verdict == kVerdictOk;
-    const uint32_t wave = tid >> 6, lane = tid & 63u;
+    // the wave index is uniform: held in a scalar register, it frees vector
+    // registers across the fold call
+    const uint32_t tid_e = opaque(tid);
+    const uint32_t wave = __builtin_amdgcn_readfirstlane(tid_e >> 6), lane = tid_e & 63u;
     u128* stage = (u128*)(smem + kLdsStage);
     if (tid == kPf0) ti->next_k = claim;
     // the leaders fetch their lane's power before the barrier, so the load
@@ -498,7 +506,7 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
     u128 hp = u128_zero();
     if (fold && wave < (uint32_t)kLeaders)
       hp = ld_u128(a.kt.pow_h + (size_t)user * kHPowers + (64u * kLeaders + 1u - 64u * wave - lane));
-    if (fold && wave >= (uint32_t)kLeaders) stage[tid - kPf0] = y;
+    if (fold && wave >= (uint32_t)kLeaders) stage[tid_e - kPf0] = y;
     __syncthreads();
     if (wave >= (uint32_t)kLeaders) {
       prefetch(ti->next_k);  // overlaps the fold
