@@ -1,4 +1,5 @@
-"""Builds the HIP library libgift.so (gfx950) in-tree.
+"""Builds the HIP library libgift.so (gfx950) in-tree, and libgift_probe.so
+(LDS-rate probes for the benchmark).
 
     python -m paper_2608_25431_amd.build
 """
@@ -11,17 +12,19 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libgift.so")
 SOURCES = [os.path.join(CSRC, "gift_kernels.hip"), os.path.join(CSRC, "gift_host.cpp"), os.path.join(CSRC, "gift_ift.cpp")]
+PROBE_SOURCE = os.path.join(CSRC, "gift_probe.hip")
+PROBE_LIB = os.path.join(HERE, "libgift_probe.so")
 ARCH = "gfx950"
 
 # Packed-FP32 instructions are disabled for all device code.
 HIP_FLAGS = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 
 
-def build(verbose: bool = False) -> str:
+def _hipcc(sources, lib, verbose):
     hipcc = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
-    tmp = LIB + ".tmp"
+    tmp = lib + ".tmp"
     cmd = [hipcc, f"--offload-arch={ARCH}", *HIP_FLAGS, "-shared", "-I", os.path.join(ROOT, "include"),
-           "-I", CSRC, *SOURCES, "-o", tmp]
+           "-I", CSRC, *sources, "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
@@ -32,7 +35,13 @@ def build(verbose: bool = False) -> str:
         raise RuntimeError(f"hipcc failed ({r.returncode})")
     if verbose and noise:
         sys.stderr.write("\n".join(noise) + "\n")
-    os.replace(tmp, LIB)
+    os.replace(tmp, lib)
+
+
+def build(verbose: bool = False) -> str:
+    """The library, and the LDS-rate probes the benchmark loads beside it."""
+    _hipcc(SOURCES, LIB, verbose)
+    _hipcc([PROBE_SOURCE], PROBE_LIB, verbose)
     return LIB
 
 

@@ -217,6 +217,37 @@ __device__ __forceinline__ u128 ghash_step_lds(const u128& y, const u128& x, con
   return u128{{a0, a1, a2, a3}};
 }
 
+// The same product for the tile end, one word of y (eight table reads) per
+// loop iteration: the words rotate through w0, so nothing is indexed at run
+// time, and the fold stays within the registers a call may clobber (more in
+// flight would make it save callee-saved registers to scratch at every tile
+// end).
+__device__ __forceinline__ u128 ghash_step_lds_lean(const u128& y, const u128& x, const uint8_t* gt) {
+  uint32_t a0 = x.w[0], a1 = x.w[1], a2 = x.w[2], a3 = x.w[3];
+  uint32_t w0 = y.w[0], w1 = y.w[1], w2 = y.w[2], w3 = y.w[3];
+#pragma unroll 1
+  for (int j = 0; j < 4; j++) {
+    const uint8_t* g = gt + j * 8 * 256;
+    uint4 e[8];
+#pragma unroll
+    for (int k = 0; k < 4; k++) {
+      e[2 * k] = lds128(g + (2 * k) * 256, nib_hi16(w0, k));
+      e[2 * k + 1] = lds128(g + (2 * k + 1) * 256, nib_lo16(w0, k));
+    }
+#pragma unroll
+    for (int k = 0; k < 8; k += 2) {
+      a0 = xor3(a0, e[k].x, e[k + 1].x);
+      a1 = xor3(a1, e[k].y, e[k + 1].y);
+      a2 = xor3(a2, e[k].z, e[k + 1].z);
+      a3 = xor3(a3, e[k].w, e[k + 1].w);
+    }
+    w0 = w1;
+    w1 = w2;
+    w2 = w3;
+  }
+  return u128{{a0, a1, a2, a3}};
+}
+
 __device__ __forceinline__ u128 load_block(const uint8_t* p, uint32_t n, bool aligned) {
   if (aligned && n == 16) {
     uint4 v = *(const uint4*)p;
@@ -277,7 +308,7 @@ __device__ __noinline__ void tile_fold(u128 v, uint32_t stage_off, uint32_t wt_o
   const u128* stage = (const u128*)(lds_byte*)(uintptr_t)stage_off;
   const uint8_t* wt = (const uint8_t*)(lds_byte*)(uintptr_t)wt_off;
 #pragma unroll 1
-  for (int i = 1; i < kFold; i++) v = ghash_step_lds(v, stage[64u * kLeaders * (i - 1)], wt);
+  for (int i = 1; i < kFold; i++) v = ghash_step_lds_lean(v, stage[64u * kLeaders * (i - 1)], wt);
   u128 z = gf_mul(v, hp);
 #pragma unroll
   for (int j = 0; j < 4; j++) z.w[j] = wave_xor(z.w[j]);
@@ -331,8 +362,6 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
   auto prefetch = [&](uint32_t k) {
     const uint32_t j = opaque(tid) - kPf0;
     const TileEnt e = k < a.n_ents ? a.tile_order[k] : TileEnt{kNoTile, 0u, 0u, 0u};
-    pf_tabs = false;
-    pf_w = make_uint4(0u, 0u, 0u, 0u);  // dead until the next prefetch: not carried across a tile
     if (j == 592u) {
       ti->g = e.g;
       ti->s = e.s;
@@ -359,6 +388,10 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
   };
   auto commit = [&]() {
     if (pf_tabs) ((uint4*)(smem + kLdsFold))[tid - kPf0] = pf_w;
+    // dead until the next prefetch (which the leader waves never run): not
+    // carried across the tile
+    pf_tabs = false;
+    pf_w = make_uint4(0u, 0u, 0u, 0u);
   };
   if (tid >= kPf0) prefetch(blockIdx.x);
 
