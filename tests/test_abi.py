@@ -129,3 +129,14 @@ def test_binding_checks_device_buffer_sizes():
         gift.seal(ok, 2, 64, segs, kt, nb, _FakeCuda(128, contiguous=False), ok)
     with pytest.raises(ValueError, match="nonces: 8 bytes"):
         gift.token_encrypt(segs, _FakeCuda(16), _FakeCuda(8), 2, kt, 0, _FakeCuda(32))
+
+
+def test_lds_probe_library_exports_its_entry_point(lib):
+    """The benchmark's LDS-rate probes live in a library of their own, which
+    exports one C entry point and nothing of the hot path."""
+    from paper_2608_25431_amd import build
+    assert os.path.exists(build.PROBE_LIB)
+    out = subprocess.run(["nm", "-D", "--defined-only", build.PROBE_LIB], capture_output=True, text=True).stdout
+    exported = {l.split()[-1] for l in out.splitlines() if l.strip()}
+    assert "gift_probe_lds" in exported
+    assert not (exported & declared_functions())
