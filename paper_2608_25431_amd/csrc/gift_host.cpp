@@ -126,6 +126,13 @@ gift_status hip_fail(hipError_t e, const char* what) {
   return fail(e == hipErrorOutOfMemory ? GIFT_E_NOMEM : GIFT_E_HIP, "%s: %s", what, hipGetErrorString(e));
 }
 
+// Events the library records only to learn on the host that enqueued work
+// has finished with a buffer (a staging slot, a call's scratch): no timing,
+// and no system-scope fence when the event completes, which would write back
+// and invalidate the caches after the preceding kernel (about 6 us of idle
+// queue per event); the host reads none of the results through them.
+constexpr unsigned kPollEvent = hipEventDisableTiming | hipEventDisableSystemFence;
+
 constexpr uint64_t kMaxSegBytes = ((1ull << 32) - 2) * 16ull;  // SP 800-38D Sec. 5.2.1.1
 constexpr int kMaxDevices = 64;
 
@@ -144,9 +151,13 @@ int device_cus(int dev) {
 
 // Pinned host staging ring per device.  A call's descriptors are copied
 // here and read into device scratch by the call's first kernel (a DMA copy
-// would make the compute queue wait for the copy engine, ~30 us per call);
-// a slot is reused only after the event recorded behind that kernel has
-// completed.
+// would make the compute queue wait for the copy engine, ~30 us per call).
+// The call enqueues all its kernels inside upload(), and one event recorded
+// behind the last of them guards the slot: the slot is reused only after
+// that event has completed.  The same event marks the end of the call's use
+// of its scratch (ScratchLease::release), so a call puts one event, not two,
+// into the queue (each costs the queue a few microseconds, and one between
+// two kernels stalls the second).
 class Staging {
  public:
   static constexpr size_t kCap = 8u << 20;
@@ -159,7 +170,7 @@ class Staging {
     hipError_t e = ring();
     while (e == hipSuccess && n_events_ < kEvents) {
       hipEvent_t ev;
-      e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
+      e = hipEventCreateWithFlags(&ev, kPollEvent);
       if (e == hipSuccess) {
         free_ev_.push_back(ev);
         n_events_++;
@@ -169,15 +180,19 @@ class Staging {
   }
 
   // Copies bytes into the ring, then consume(src) enqueues on s the kernel
-  // that reads them: src is the copy's device address, or nullptr when the
-  // bytes were DMA-copied to dst instead (no device address for the ring, or
-  // a table too large for it).  With no_alloc the call creates nothing: it
+  // that reads them and the rest of the call's work: src is the copy's
+  // device address, or nullptr when the bytes were DMA-copied to dst instead
+  // (no device address for the ring, or a table too large for it).  The
+  // event recorded behind that work is returned in *recorded (nullptr when
+  // none was: empty or very large tables).  With no_alloc the call creates nothing: it
   // needs a prepared ring with a device address and at most kMaxStaged
   // bytes, and when every pooled event is in flight it waits for the oldest
   // slot and takes its event.
   template <class F>
-  hipError_t upload(void* dst, const void* src, size_t bytes, hipStream_t s, F&& consume, bool no_alloc = false) {
+  hipError_t upload(void* dst, const void* src, size_t bytes, hipStream_t s, F&& consume, bool no_alloc = false,
+                    hipEvent_t* recorded = nullptr) {
     std::lock_guard<std::mutex> g(mu_);
+    if (recorded) *recorded = nullptr;
     if (bytes == 0) return consume((const void*)nullptr);
     if (no_alloc && (base_ == nullptr || dbase_ == nullptr || bytes > kMaxStaged || (bytes & 15u)))
       return hipErrorNotInitialized;
@@ -242,7 +257,7 @@ class Staging {
       return hipErrorNotInitialized;
     } else {
       n_events_++;
-      e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
+      e = hipEventCreateWithFlags(&ev, kPollEvent);
       if (e != hipSuccess) {
         (void)hipStreamSynchronize(s);
         return e;
@@ -256,6 +271,7 @@ class Staging {
     }
     live_.push_back(Slot{head_, need, ev, false});
     head_ += need;
+    if (recorded) *recorded = ev;
     return hipSuccess;
   }
 
@@ -306,9 +322,12 @@ inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 // was on the same stream).  A
 // lease holds the entry's lock until its call has enqueued all its work, so
 // two host threads on one stream cannot interleave their uses of the buffer.
-// The event recorded when a lease ends guards the rare cases where a buffer
-// is replaced (it is too small) or handed to another stream: the host waits
-// for its last use first.  When every entry of the device is busy on other
+// The event behind a lease's last use (the call's staging event, else one
+// recorded when the lease ends) guards the rare cases where a buffer is
+// replaced (it is too small) or handed to another stream: the host waits for
+// its last use first.  The staging ring records a pooled event again only
+// after it has completed, so a wait on an event the ring has since reused
+// waits for later work as well: longer, never too short.  When every entry of the device is busy on other
 // streams, a call falls back to stream-ordered allocation.
 struct ScratchEntry {
   std::mutex mu;
@@ -317,7 +336,8 @@ struct ScratchEntry {
   uint8_t* ptr = nullptr;
   size_t cap = 0;
   hipEvent_t done = nullptr;
-  bool recorded = false;  // done marks the last use of ptr
+  hipEvent_t last = nullptr;  // the event behind the last use of ptr: done, or the call's staging event
+  bool recorded = false;      // last marks the last use of ptr
   bool unsure = false;    // a use is not covered by done: synchronise the device first
 };
 
@@ -386,10 +406,11 @@ class ScratchLease {
           lk_ = std::move(l);
           // the handle may name another stream than the buffer's last use did
           hipError_t w = hipSuccess;
-          if (e_->unsure)
+          if (e_->unsure) {
             w = settle(*e_);
-          else if (e_->recorded)
-            w = hipStreamWaitEvent(s, e_->done, 0);
+          } else if (e_->recorded) {
+            w = hipStreamWaitEvent(s, e_->last, 0);
+          }
           if (w != hipSuccess) return w;
         }
       } else if (!e_) {
@@ -419,7 +440,7 @@ class ScratchLease {
       e_->cap = cap;
     }
     if (!e_->done) {
-      hipError_t w = hipEventCreateWithFlags(&e_->done, hipEventDisableTiming);
+      hipError_t w = hipEventCreateWithFlags(&e_->done, kPollEvent);
       if (w != hipSuccess) {
         e_->done = nullptr;
         return w;
@@ -429,15 +450,22 @@ class ScratchLease {
     return hipSuccess;
   }
 
-  // Ends the call's use of the buffer: after its last enqueued work.
-  hipError_t release() {
+  // Ends the call's use of the buffer: after its last enqueued work, which
+  // `shared` (an event already recorded behind it) marks, else an event
+  // recorded now.
+  hipError_t release(hipEvent_t shared = nullptr) {
     hipError_t r = hipSuccess;
     if (owned_) {
       r = hipFreeAsync(ptr, s_);
       owned_ = false;
     } else if (e_) {
       if (ptr) {
-        r = hipEventRecord(e_->done, s_);
+        if (shared) {
+          e_->last = shared;
+        } else {
+          r = hipEventRecord(e_->done, s_);
+          e_->last = e_->done;
+        }
         e_->recorded = r == hipSuccess;
         e_->unsure = r != hipSuccess;
       }
@@ -460,7 +488,7 @@ class ScratchLease {
       x.recorded = false;
     }
     if (x.recorded) {
-      hipError_t w = hipEventSynchronize(x.done);
+      hipError_t w = hipEventSynchronize(x.last);
       if (w != hipSuccess) return w;
       x.recorded = false;
     }
@@ -685,19 +713,13 @@ gift_status run_gcm(const gift_tensor* t, const gift_segment_table* st, gift_key
   const ExpandArgs ex{(uint32_t*)(scratch + o_tb), (uint32_t*)(scratch + o_sl), (TileEnt*)(scratch + o_to),
                       (uint32_t)Q.cap, cus, nullptr, (SegInfo*)(scratch + o_si), (uint32_t*)(scratch + o_sc),
                       kSmallMaxBlocks};
-  e = sg->upload(
-      scratch, host.data(), o_st, stream,
-      [&](const void* src) {
-        return launch_prologue(scratch, src, o_st, n, kNoBids, st->row_labels, n ? verdicts : nullptr, &kt->dev,
-                               (uint4*)(scratch + o_fn), (uint4*)(scratch + o_pt), P.n_tiles, o_br,
-                               n ? &ex : nullptr, stream);
-      },
-      no_alloc);
-  if (e != hipSuccess) return hip_fail(e, "staging upload");
-
   const SegDesc* d_desc = (const SegDesc*)(scratch + o_desc);
   gift_status rs = GIFT_OK;
-  do {
+  hipEvent_t call_ev = nullptr;  // recorded behind the call's last kernel
+  // the call's kernels after the prologue, enqueued while the staging slot is
+  // held, so that the one event behind the last of them frees the slot (an
+  // event between two kernels costs the queue several microseconds)
+  auto rest = [&]() -> hipError_t {
     if (n > 0) {
       GcmArgs a{};  // zero-initialised: no field is left undefined
       a.in = (const uint8_t*)t->data;
@@ -726,19 +748,19 @@ gift_status run_gcm(const gift_tensor* t, const gift_segment_table* st, gift_key
         e = hipEventRecord(prof_before, stream);
         if (e != hipSuccess) {
           rs = hip_fail(e, "profiling event");
-          break;
+          return e;
         }
       }
       e = launch_gcm_tiles(a, OPEN ? kModeOpen : 0, Q.grid, stream);
       if (e != hipSuccess) {
         rs = hip_fail(e, "gcm launch");
-        break;
+        return e;
       }
       if (prof_after && P.n_tiles > 0) {
         e = hipEventRecord(prof_after, stream);
         if (e != hipSuccess) {
           rs = hip_fail(e, "profiling event");
-          break;
+          return e;
         }
       }
       e = launch_gcm_small(a, OPEN, stream);
@@ -749,7 +771,7 @@ gift_status run_gcm(const gift_tensor* t, const gift_segment_table* st, gift_key
                                stream);
       if (e != hipSuccess) {
         rs = hip_fail(e, "gcm launch");
-        break;
+        return e;
       }
     }
     if (!P.zr.empty()) {
@@ -757,11 +779,26 @@ gift_status run_gcm(const gift_tensor* t, const gift_segment_table* st, gift_key
                              (uint32_t)device_cus(dev) * 4u, stream);
       if (e != hipSuccess) {
         rs = hip_fail(e, "zero-fill launch");
-        break;
+        return e;
       }
     }
-  } while (0);
-  e = lease.release();
+    return hipSuccess;
+  };
+  e = sg->upload(
+      scratch, host.data(), o_st, stream,
+      [&](const void* src) {
+        hipError_t r = launch_prologue(scratch, src, o_st, n, kNoBids, st->row_labels, n ? verdicts : nullptr,
+                                       &kt->dev, (uint4*)(scratch + o_fn), (uint4*)(scratch + o_pt), P.n_tiles, o_br,
+                                       n ? &ex : nullptr, stream);
+        if (r != hipSuccess) {
+          rs = hip_fail(r, "prologue launch");
+          return r;
+        }
+        return rest();
+      },
+      no_alloc, &call_ev);
+  if (e != hipSuccess && rs == GIFT_OK) rs = hip_fail(e, "staging upload");
+  e = lease.release(e == hipSuccess ? call_ev : nullptr);
   if (rs == GIFT_OK && e != hipSuccess) rs = hip_fail(e, "device scratch release");
   return rs;
 }
@@ -937,24 +974,19 @@ gift_status run_paged(const gift_paged_kv* kv, const gift_request* reqs, uint32_
   // block id), zeroes the tile partials and expands the segment table
   const ExpandArgs ex{(uint32_t*)(scratch + o_tb), (uint32_t*)(scratch + o_sl), (TileEnt*)(scratch + o_to),
                       (uint32_t)Q.cap, cus, nullptr, (SegInfo*)(scratch + o_si), (uint32_t*)(scratch + o_sc), 0u};
-  e = sg ? sg->upload(scratch, host.data(), o_st, stream,
-                      [&](const void* src) {
-                        return launch_prologue(scratch, src, o_st, n, o_bid, labels, verdicts, &kt->dev,
-                                               (uint4*)(scratch + o_fn), (uint4*)(scratch + o_pt), n_tiles, o_br,
-                                               &ex, stream);
-                      })
-         : hipErrorInvalidDevice;
-  if (e != hipSuccess) return hip_fail(e, "staging upload");
+  gift_status rs = GIFT_OK;
+  hipEvent_t call_ev = nullptr;  // recorded behind the call's last kernel
   const SegDesc* d_desc = (const SegDesc*)(scratch + o_desc);
   const uint32_t* d_bid = (const uint32_t*)(scratch + o_bid);
   uint64_t* d_ck = (uint64_t*)(scratch + o_ck);
-  gift_status rs = GIFT_OK;
-  do {
+  // the call's kernels after the prologue, enqueued while the staging slot is
+  // held (one event behind the last of them frees the slot)
+  auto rest = [&]() -> hipError_t {
     e = launch_chunk_table(d_desc, n, d_bid, kv->n_layers, kv->n_parts, kv->layer_stride, kv->block_stride,
                            kv->part_stride, d_ck, stream);
     if (e != hipSuccess) {
       rs = hip_fail(e, "paged expansion");
-      break;
+      return e;
     }
     GcmArgs a{};  // zero-initialised: no field is left undefined
     a.in = (const uint8_t*)in;
@@ -983,7 +1015,7 @@ gift_status run_paged(const gift_paged_kv* kv, const gift_request* reqs, uint32_
       e = hipEventRecord(g_prof_before, stream);
       if (e != hipSuccess) {
         rs = hip_fail(e, "profiling event");
-        break;
+        return e;
       }
     }
     e = launch_gcm_tiles(a, OPEN ? (kModeOpen | kModeScatter) : kModeGather, Q.grid, stream);
@@ -994,11 +1026,26 @@ gift_status run_paged(const gift_paged_kv* kv, const gift_request* reqs, uint32_
                              (uint8_t*)kv->base, shift, cus * 4u, stream);
     if (e != hipSuccess) {
       rs = hip_fail(e, "paged gcm launch");
-      break;
+      return e;
     }
-  } while (0);
+    return hipSuccess;
+  };
+  e = sg ? sg->upload(scratch, host.data(), o_st, stream,
+                      [&](const void* src) {
+                        hipError_t r = launch_prologue(scratch, src, o_st, n, o_bid, labels, verdicts, &kt->dev,
+                                                       (uint4*)(scratch + o_fn), (uint4*)(scratch + o_pt), n_tiles,
+                                                       o_br, &ex, stream);
+                        if (r != hipSuccess) {
+                          rs = hip_fail(r, "prologue launch");
+                          return r;
+                        }
+                        return rest();
+                      },
+                      false, &call_ev)
+         : hipErrorInvalidDevice;
+  if (e != hipSuccess && rs == GIFT_OK) rs = hip_fail(e, "staging upload");
   g_prof_before = g_prof_after = nullptr;
-  e = lease.release();
+  e = lease.release(e == hipSuccess ? call_ev : nullptr);
   if (rs == GIFT_OK && e != hipSuccess) rs = hip_fail(e, "device scratch release");
   return rs;
 }
@@ -1168,13 +1215,15 @@ gift_status gift_check_owner(const gift_segment_table* st, const uint32_t* label
   if (e != hipSuccess) return hip_fail(e, "device scratch");
   SegDesc* d = (SegDesc*)lease.ptr;
   Staging* sg = staging_for(dev);
+  hipEvent_t call_ev = nullptr;  // recorded behind the prologue
   e = sg ? sg->upload(d, P.descs.data(), bytes, stream,
                       [&](const void* src) {
                         return launch_prologue(d, src, bytes, n, kNoBids, labels, st->verdicts, nullptr, nullptr,
                                                nullptr, 0u, 0u, nullptr, stream);
-                      })
+                      },
+                      false, &call_ev)
          : hipErrorInvalidDevice;
-  hipError_t e2 = lease.release();
+  hipError_t e2 = lease.release(e == hipSuccess ? call_ev : nullptr);
   if (e != hipSuccess) return hip_fail(e, "check_owner");
   if (e2 != hipSuccess) return hip_fail(e2, "device scratch release");
   return GIFT_OK;
@@ -1207,26 +1256,39 @@ static gift_status run_tokens(bool decrypt, const gift_segment_table* st, uint64
     e = lease.acquire(dev, stream, sizeof(SegDesc) * n);
     if (e != hipSuccess) return hip_fail(e, "device scratch");
     d = (SegDesc*)lease.ptr;
-    Staging* sg = staging_for(dev);
-    const size_t bytes = sizeof(SegDesc) * n;
-    e = sg ? sg->upload(d, P.descs.data(), bytes, stream,
-                        [&](const void* src) {
-                          return launch_prologue(d, src, bytes, n, kNoBids, nullptr, nullptr, nullptr, nullptr,
-                                                 nullptr, 0u, 0u, nullptr, stream);
-                        })
-           : hipErrorInvalidDevice;
   }
   // uncovered tokens (rows no segment covers) get zero output: only when the
   // plan has such gaps is the output cleared first, the token kernel then
   // overwrites every covered entry
   const bool gaps = !P.zr.empty();
-  if (e == hipSuccess && gaps)
-    e = decrypt ? launch_wipe(tokens_out, 8ull * n_tokens, stream) : launch_wipe(blocks_out, 16ull * n_tokens, stream);
-  if (e == hipSuccess && gaps && decrypt && nonces_out) e = launch_wipe(nonces_out, 8ull * n_tokens, stream);
-  if (e == hipSuccess)
-    e = launch_tokens(d, n, decrypt, tokens, nonces, blocks_in, blocks_out, tokens_out, nonces_out, eos_token, kt->dev,
-                      stream);
-  hipError_t e2 = lease.release();
+  hipEvent_t call_ev = nullptr;  // recorded behind the call's last kernel
+  auto rest = [&]() -> hipError_t {
+    hipError_t r = hipSuccess;
+    if (gaps)
+      r = decrypt ? launch_wipe(tokens_out, 8ull * n_tokens, stream) : launch_wipe(blocks_out, 16ull * n_tokens, stream);
+    if (r == hipSuccess && gaps && decrypt && nonces_out) r = launch_wipe(nonces_out, 8ull * n_tokens, stream);
+    if (r == hipSuccess)
+      r = launch_tokens(d, n, decrypt, tokens, nonces, blocks_in, blocks_out, tokens_out, nonces_out, eos_token,
+                        kt->dev, stream);
+    return r;
+  };
+  if (n > 0) {
+    // the token kernels are enqueued while the staging slot is held (one
+    // event behind the last of them frees the slot)
+    Staging* sg = staging_for(dev);
+    const size_t bytes = sizeof(SegDesc) * n;
+    e = sg ? sg->upload(d, P.descs.data(), bytes, stream,
+                        [&](const void* src) {
+                          hipError_t r = launch_prologue(d, src, bytes, n, kNoBids, nullptr, nullptr, nullptr,
+                                                         nullptr, nullptr, 0u, 0u, nullptr, stream);
+                          return r != hipSuccess ? r : rest();
+                        },
+                        false, &call_ev)
+           : hipErrorInvalidDevice;
+  } else {
+    e = rest();
+  }
+  hipError_t e2 = lease.release(e == hipSuccess ? call_ev : nullptr);
   if (e != hipSuccess) return hip_fail(e, "token kernels");
   if (e2 != hipSuccess) return hip_fail(e2, "device scratch release");
   return GIFT_OK;
