@@ -16,7 +16,10 @@ launch configuration the benchmark times (tolerance zero: integer work).
   oracle's seal -- every byte and the tag; every byte of the other 24 against
   the oracle's GCTR (SP 800-38D Algorithm 3) over 64 MiB pieces, each from its
   own initial counter block, with the plaintext regenerated from the seed per
-  piece; then the in-place open back to the plaintext, every byte.
+  piece, and their tags from the oracle's GHASH of each ciphertext piece (GHASH
+  is linear: a segment's hash is the sum of its pieces' hashes, each times H
+  to the number of blocks after the piece, the length block last) and the
+  oracle's E_K(J0); then the in-place open back to the plaintext, every byte.
 
 The oracle runs segment by segment on a thread pool, longest jobs first; each
 segment goes through the oracle's own segmented entry points over a
@@ -125,6 +128,18 @@ def oracle_open_compare(w, t, ct_h, tags_h, back_h, ver_h, labels=None):
         return None
 
     return run_longest_first([(t.seg_bytes(i)[1], i) for i in range(len(t.segs))], one)
+
+
+def gf_pow(h, e):
+    """h^e in GF(2^128) by square and multiply over the oracle's multiply."""
+    r, b = (0x80).to_bytes(1, "big") + bytes(15), h  # the field's 1 is the bit string 10...0
+    while e:
+        if e & 1:
+            r = oracle.gf128_mul(r, b)
+        e >>= 1
+        if e:
+            b = oracle.gf128_mul(b, b)
+    return r
 
 
 def covered_exactly(t):
@@ -250,6 +265,8 @@ def test_llama3_70b_kv_in_place_against_oracle():
         _, ln = t.seg_bytes(i)
         jobs += [(min(PIECE, ln - o), "gctr", i, o) for o in range(0, ln, PIECE)]
 
+    hashes = {}  # (segment, piece offset) -> oracle GHASH of the ciphertext piece
+
     def one(job):
         ln, kind, i, o = job
         off, _ = t.seg_bytes(i)
@@ -269,17 +286,40 @@ def test_llama3_70b_kv_in_place_against_oracle():
             iv = oracle.segment_iv(w.nonce_base[u].tobytes(), int(s["iv_seq"]))
             icb = iv + (2 + o // 16).to_bytes(4, "big")
             exp = np.frombuffer(oracle.gctr(w.keys[u].tobytes(), icb, pt), np.uint8)
+            hashes[(i, o)] = oracle.ghash(h_of[u], got)
         if not np.array_equal(exp, got):
             return f"segment {i} ({kind}) at +{o}: ciphertext differs at byte {first_diff(exp, got)}"
         return None
 
+    h_of = {u: oracle.aes_encrypt_block(w.keys[u].tobytes(), bytes(16)) for u in set(int(x) for x in t.segs["user"])}
     t0 = time.perf_counter()
     bad = run_longest_first(jobs, one)
     whole_bytes = sum(t.seg_bytes(i)[1] for i in whole)
     log(f"llama3_70b_kv: {len(whole)} whole segments ({whole_bytes / 1e9:.2f} GB, tags too) and "
-        f"{(t.nbytes - whole_bytes) / 1e9:.2f} GB in {PIECE >> 20} MiB GCTR pieces against the oracle "
+        f"{(t.nbytes - whole_bytes) / 1e9:.2f} GB in {PIECE >> 20} MiB GCTR + GHASH pieces against the oracle "
         f"in {time.perf_counter() - t0:.0f} s")
     assert not bad, bad
+    # tags of the segments checked in pieces: S = sum over pieces of
+    # GHASH(piece) * H^(blocks after the piece, the length block included),
+    # plus L * H for the length block L; tag = E_K(J0) xor S
+    for i in range(n):
+        if i in whole:
+            continue
+        s = t.segs[i]
+        u = int(s["user"])
+        _, ln = t.seg_bytes(i)
+        assert ln % 16 == 0
+        m = ln // 16 + 1  # blocks hashed, the length block last
+        acc = bytes(16)
+        for o in range(0, ln, PIECE):
+            b = (o + min(PIECE, ln - o)) // 16
+            acc = bytes(x ^ y for x, y in zip(acc, oracle.gf128_mul(hashes[(i, o)], gf_pow(h_of[u], m - b))))
+        lblock = (0).to_bytes(8, "big") + (8 * ln).to_bytes(8, "big")
+        acc = bytes(x ^ y for x, y in zip(acc, oracle.gf128_mul(lblock, h_of[u])))
+        iv = oracle.segment_iv(w.nonce_base[u].tobytes(), int(s["iv_seq"]))
+        ekj0 = oracle.aes_encrypt_block(w.keys[u].tobytes(), iv + (1).to_bytes(4, "big"))
+        tag = bytes(x ^ y for x, y in zip(ekj0, acc))
+        assert tag == tags_h[i].tobytes(), f"segment {i}: tag differs from the oracle's"
     # in-place open: back to the plaintext, regenerated piece by piece
     _, ver2 = open_(d, t.n_rows, rb, t.segs, kt, w.nonce_base, tags, labels_dev=lab, out=d)
     assert (host(ver2)[:n] == gift.SEG_OK).all()
