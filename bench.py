@@ -357,6 +357,8 @@ def main():
     ap.add_argument("--no-labels", action="store_true", help="seal without the fused owner check")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run one plain 1 GiB device-to-device copy first (scales HBM byte counters)")
+    ap.add_argument("--library", default=None,
+                    help="time this libgift.so (e.g. one built from another commit) instead of the in-tree one")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU (--gpus 1). Segments are independent GCM messages: several GPUs "
@@ -369,6 +371,9 @@ def main():
 
     from paper_2608_25431_amd import gift
     from paper_2608_25431_amd import workloads as W
+    if args.library:
+        gift.LIB_PATH = os.path.abspath(args.library)
+        log(f"[bench] library {gift.LIB_PATH}")
 
     dev = "cuda:0"
     torch.cuda.set_device(0)
@@ -427,6 +432,7 @@ def main():
     log(f"[bench] warmup {args.warmup} done")
 
     wall = None
+    enqueue_us = None
     if not w.in_place:
         # the timed region: K calls back to back with no event between them
         torch.cuda.synchronize()
@@ -436,6 +442,18 @@ def main():
         torch.cuda.synchronize()
         wall = time.perf_counter() - t0
         log(f"[bench] timed {args.steps} steps: {wall * 1e3 / args.steps:.3f} ms/step")
+
+    if not w.in_place:
+        # host time of one call (until it returns, its work enqueued), each
+        # started with the GPU idle: the median of 21
+        enq = []
+        for _ in range(21):
+            torch.cuda.synchronize()
+            t1 = time.perf_counter()
+            step()
+            enq.append(time.perf_counter() - t1)
+        torch.cuda.synchronize()
+        enqueue_us = sorted(enq)[10] * 1e6
 
     # A second pass of K steps with events on the launch stream: the duration
     # of every step (for the median) and of its per-block kernel (events the
@@ -537,6 +555,7 @@ def main():
                    "step": ("seal+open pair in place; value and hbm_roofline_pct from the seal calls' own events"
                             if w.in_place else "one gift_seal call")},
         "median_ms_per_step": round(median_step_ms, 4),
+        "host_enqueue_us": None if enqueue_us is None else round(enqueue_us, 1),
         "hbm_roofline_pct": round(hbm_pct_step, 2),
         "open_gbps": None if open_gbps is None else round(open_gbps, 3),
         "key_setup_ms": round(key_setup_ms, 3),
@@ -548,6 +567,8 @@ def main():
     }
     if median_seal_ms is not None:
         res["median_seal_ms"] = round(median_seal_ms, 4)
+    if args.library:
+        res["library"] = args.library
     k_sorted = sorted(kern_ms)
     res["roofline"]["kernel_ms_median"] = round(k_sorted[len(k_sorted) // 2], 4)
     # The same kernel against the limit that binds it: its LDS reads per
