@@ -8,6 +8,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <atomic>
 #include <deque>
 #include <mutex>
 #include <string>
@@ -149,15 +150,29 @@ int device_cus(int dev) {
   return cus[dev];
 }
 
+// An event of the staging ring's pool and the number of times it has been
+// recorded.  The ring records a pooled event again only after its previous
+// recording has completed, so a holder that remembers the generation it saw
+// knows, when the count has moved on, that the work it waited for is done.
+struct PoolEvent {
+  hipEvent_t ev = nullptr;
+  std::atomic<uint64_t> gen{0};
+};
+// A recording of a pooled event: (event, generation), or none.
+struct EventMark {
+  PoolEvent* pe = nullptr;
+  uint64_t gen = 0;
+};
+
 // Pinned host staging ring per device.  A call's descriptors are copied
 // here and read into device scratch by the call's first kernel (a DMA copy
 // would make the compute queue wait for the copy engine, ~30 us per call).
-// The call enqueues all its kernels inside upload(), and one event recorded
-// behind the last of them guards the slot: the slot is reused only after
-// that event has completed.  The same event marks the end of the call's use
-// of its scratch (ScratchLease::release), so a call puts one event, not two,
-// into the queue (each costs the queue a few microseconds, and one between
-// two kernels stalls the second).
+// The call enqueues all its kernels inside upload(), and one pooled event
+// recorded behind the last of them guards the slot: the slot is reused only
+// after that event has completed.  The same recording marks the end of the
+// call's use of its scratch (ScratchLease::release), so a call puts one
+// event, not two, into the queue (each costs the queue a few microseconds,
+// and one between two kernels stalls the second).
 class Staging {
  public:
   static constexpr size_t kCap = 8u << 20;
@@ -169,12 +184,9 @@ class Staging {
     std::lock_guard<std::mutex> g(mu_);
     hipError_t e = ring();
     while (e == hipSuccess && n_events_ < kEvents) {
-      hipEvent_t ev;
-      e = hipEventCreateWithFlags(&ev, kPollEvent);
-      if (e == hipSuccess) {
-        free_ev_.push_back(ev);
-        n_events_++;
-      }
+      PoolEvent* pe = nullptr;
+      e = new_event(&pe);
+      if (e == hipSuccess) free_ev_.push_back(pe);
     }
     return e;
   }
@@ -183,16 +195,16 @@ class Staging {
   // that reads them and the rest of the call's work: src is the copy's
   // device address, or nullptr when the bytes were DMA-copied to dst instead
   // (no device address for the ring, or a table too large for it).  The
-  // event recorded behind that work is returned in *recorded (nullptr when
-  // none was: empty or very large tables).  With no_alloc the call creates nothing: it
+  // pooled event recorded behind that work is returned in *mark (none for
+  // empty or very large tables).  With no_alloc the call creates nothing: it
   // needs a prepared ring with a device address and at most kMaxStaged
   // bytes, and when every pooled event is in flight it waits for the oldest
   // slot and takes its event.
   template <class F>
   hipError_t upload(void* dst, const void* src, size_t bytes, hipStream_t s, F&& consume, bool no_alloc = false,
-                    hipEvent_t* recorded = nullptr) {
+                    EventMark* mark = nullptr) {
     std::lock_guard<std::mutex> g(mu_);
-    if (recorded) *recorded = nullptr;
+    if (mark) *mark = EventMark{};
     if (bytes == 0) return consume((const void*)nullptr);
     if (no_alloc && (base_ == nullptr || dbase_ == nullptr || bytes > kMaxStaged || (bytes & 15u)))
       return hipErrorNotInitialized;
@@ -216,13 +228,13 @@ class Staging {
     // retire finished slots oldest first, stopping at the first still in
     // flight (one query per call in the usual single-stream case); a slot in
     // flight that overlaps [head_, head_ + need) must finish first
-    while (!live_.empty() && (live_.front().done || hipEventQuery(live_.front().ev) == hipSuccess)) {
-      free_ev_.push_back(live_.front().ev);
+    while (!live_.empty() && (live_.front().done || hipEventQuery(live_.front().pe->ev) == hipSuccess)) {
+      free_ev_.push_back(live_.front().pe);
       live_.pop_front();
     }
     for (Slot& sl : live_)
       if (!sl.done && sl.off < head_ + need && head_ < sl.off + sl.len) {
-        hipError_t e = hipEventSynchronize(sl.ev);
+        hipError_t e = hipEventSynchronize(sl.pe->ev);
         if (e != hipSuccess) return e;
         sl.done = true;
       }
@@ -238,40 +250,42 @@ class Staging {
       (void)hipStreamSynchronize(s);  // the slot may still be read: let it drain
       return e;
     }
-    hipEvent_t ev;
     if (free_ev_.empty() && no_alloc && !live_.empty()) {
       // every pooled event is in flight: the oldest slot's event is the next free
-      e = hipEventSynchronize(live_.front().ev);
+      e = hipEventSynchronize(live_.front().pe->ev);
       if (e != hipSuccess) {
         (void)hipStreamSynchronize(s);
         return e;
       }
-      free_ev_.push_back(live_.front().ev);
+      free_ev_.push_back(live_.front().pe);
       live_.pop_front();
     }
+    PoolEvent* pe = nullptr;
     if (!free_ev_.empty()) {
-      ev = free_ev_.back();
+      pe = free_ev_.back();
       free_ev_.pop_back();
     } else if (no_alloc) {
       (void)hipStreamSynchronize(s);
       return hipErrorNotInitialized;
     } else {
-      n_events_++;
-      e = hipEventCreateWithFlags(&ev, kPollEvent);
+      e = new_event(&pe);
       if (e != hipSuccess) {
         (void)hipStreamSynchronize(s);
         return e;
       }
     }
-    e = hipEventRecord(ev, s);
+    // the generation moves on before the recording: a holder of the old one
+    // sees a completed recording either way
+    const uint64_t gen = pe->gen.fetch_add(1) + 1;
+    e = hipEventRecord(pe->ev, s);
     if (e != hipSuccess) {
       (void)hipStreamSynchronize(s);
-      free_ev_.push_back(ev);
+      free_ev_.push_back(pe);
       return e;
     }
-    live_.push_back(Slot{head_, need, ev, false});
+    live_.push_back(Slot{head_, need, pe, false});
     head_ += need;
-    if (recorded) *recorded = ev;
+    if (mark) *mark = EventMark{pe, gen};
     return hipSuccess;
   }
 
@@ -290,15 +304,27 @@ class Staging {
   }
   struct Slot {
     size_t off, len;
-    hipEvent_t ev;
+    PoolEvent* pe;
     bool done;  // its event has completed
   };
+  // a new pooled event (mu_ held, or before the ring is shared)
+  hipError_t new_event(PoolEvent** out) {
+    hipEvent_t ev;
+    hipError_t e = hipEventCreateWithFlags(&ev, kPollEvent);
+    if (e != hipSuccess) return e;
+    pool_.emplace_back();
+    pool_.back().ev = ev;
+    n_events_++;
+    *out = &pool_.back();
+    return hipSuccess;
+  }
   std::mutex mu_;
   uint8_t* base_ = nullptr;
   uint8_t* dbase_ = nullptr;  // base_ as the device addresses it (mapped pinned memory)
   size_t head_ = 0;
   std::deque<Slot> live_;  // in allocation order
-  std::vector<hipEvent_t> free_ev_;
+  std::deque<PoolEvent> pool_;  // stable addresses: holders keep pointers
+  std::vector<PoolEvent*> free_ev_;
   int n_events_ = 0;  // events created so far
 };
 
@@ -322,12 +348,12 @@ inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 // was on the same stream).  A
 // lease holds the entry's lock until its call has enqueued all its work, so
 // two host threads on one stream cannot interleave their uses of the buffer.
-// The event behind a lease's last use (the call's staging event, else one
-// recorded when the lease ends) guards the rare cases where a buffer is
-// replaced (it is too small) or handed to another stream: the host waits for
-// its last use first.  The staging ring records a pooled event again only
-// after it has completed, so a wait on an event the ring has since reused
-// waits for later work as well: longer, never too short.  When every entry of the device is busy on other
+// The event behind a call's last work (the call's pooled staging event,
+// else the entry's own, recorded when the lease ends) guards the rare cases
+// where a buffer is replaced (it is too small) or handed to another stream:
+// the host waits for its last use first.  A pooled event is held with the
+// generation it was recorded under: once the ring has recorded it again (for
+// any stream), that use has completed and nothing waits on it.  When every entry of the device is busy on other
 // streams, a call falls back to stream-ordered allocation.
 struct ScratchEntry {
   std::mutex mu;
@@ -335,9 +361,9 @@ struct ScratchEntry {
   hipStream_t stream = nullptr;
   uint8_t* ptr = nullptr;
   size_t cap = 0;
-  hipEvent_t done = nullptr;
-  hipEvent_t last = nullptr;  // the event behind the last use of ptr: done, or the call's staging event
-  bool recorded = false;      // last marks the last use of ptr
+  hipEvent_t done = nullptr;   // recorded at the end of a call that staged nothing
+  EventMark mark;              // else the call's staging event marks the last use of ptr
+  bool recorded = false;       // done or mark marks the last use of ptr
   bool unsure = false;    // a use is not covered by done: synchronise the device first
 };
 
@@ -409,7 +435,8 @@ class ScratchLease {
           if (e_->unsure) {
             w = settle(*e_);
           } else if (e_->recorded) {
-            w = hipStreamWaitEvent(s, e_->last, 0);
+            hipEvent_t ev = last_event(*e_);
+            if (ev) w = hipStreamWaitEvent(s, ev, 0);
           }
           if (w != hipSuccess) return w;
         }
@@ -450,22 +477,17 @@ class ScratchLease {
     return hipSuccess;
   }
 
-  // Ends the call's use of the buffer: after its last enqueued work, which
-  // `shared` (an event already recorded behind it) marks, else an event
-  // recorded now.
-  hipError_t release(hipEvent_t shared = nullptr) {
+  // Ends the call's use of the buffer, after its last enqueued work: marked
+  // by the call's staging event (m), else by the entry's event, recorded now.
+  hipError_t release(EventMark m = EventMark{}) {
     hipError_t r = hipSuccess;
     if (owned_) {
       r = hipFreeAsync(ptr, s_);
       owned_ = false;
     } else if (e_) {
       if (ptr) {
-        if (shared) {
-          e_->last = shared;
-        } else {
-          r = hipEventRecord(e_->done, s_);
-          e_->last = e_->done;
-        }
+        e_->mark = m;
+        if (!m.pe) r = hipEventRecord(e_->done, s_);
         e_->recorded = r == hipSuccess;
         e_->unsure = r != hipSuccess;
       }
@@ -488,11 +510,19 @@ class ScratchLease {
       x.recorded = false;
     }
     if (x.recorded) {
-      hipError_t w = hipEventSynchronize(x.last);
+      hipEvent_t ev = last_event(x);
+      hipError_t w = ev ? hipEventSynchronize(ev) : hipSuccess;
       if (w != hipSuccess) return w;
       x.recorded = false;
     }
     return hipSuccess;
+  }
+
+  // the event that still marks the entry's last use, or nullptr when that
+  // use has certainly completed (its pooled event was recorded again since)
+  static hipEvent_t last_event(const ScratchEntry& x) {
+    if (!x.mark.pe) return x.done;
+    return x.mark.pe->gen.load() == x.mark.gen ? x.mark.pe->ev : nullptr;
   }
 
   ScratchEntry* e_ = nullptr;
@@ -715,7 +745,7 @@ gift_status run_gcm(const gift_tensor* t, const gift_segment_table* st, gift_key
                       kSmallMaxBlocks};
   const SegDesc* d_desc = (const SegDesc*)(scratch + o_desc);
   gift_status rs = GIFT_OK;
-  hipEvent_t call_ev = nullptr;  // recorded behind the call's last kernel
+  EventMark call_ev;  // the event recorded behind the call's last kernel
   // the call's kernels after the prologue, enqueued while the staging slot is
   // held, so that the one event behind the last of them frees the slot (an
   // event between two kernels costs the queue several microseconds)
@@ -798,7 +828,7 @@ gift_status run_gcm(const gift_tensor* t, const gift_segment_table* st, gift_key
       },
       no_alloc, &call_ev);
   if (e != hipSuccess && rs == GIFT_OK) rs = hip_fail(e, "staging upload");
-  e = lease.release(e == hipSuccess ? call_ev : nullptr);
+  e = lease.release(call_ev);
   if (rs == GIFT_OK && e != hipSuccess) rs = hip_fail(e, "device scratch release");
   return rs;
 }
@@ -975,7 +1005,7 @@ gift_status run_paged(const gift_paged_kv* kv, const gift_request* reqs, uint32_
   const ExpandArgs ex{(uint32_t*)(scratch + o_tb), (uint32_t*)(scratch + o_sl), (TileEnt*)(scratch + o_to),
                       (uint32_t)Q.cap, cus, nullptr, (SegInfo*)(scratch + o_si), (uint32_t*)(scratch + o_sc), 0u};
   gift_status rs = GIFT_OK;
-  hipEvent_t call_ev = nullptr;  // recorded behind the call's last kernel
+  EventMark call_ev;  // the event recorded behind the call's last kernel
   const SegDesc* d_desc = (const SegDesc*)(scratch + o_desc);
   const uint32_t* d_bid = (const uint32_t*)(scratch + o_bid);
   uint64_t* d_ck = (uint64_t*)(scratch + o_ck);
@@ -1045,7 +1075,7 @@ gift_status run_paged(const gift_paged_kv* kv, const gift_request* reqs, uint32_
          : hipErrorInvalidDevice;
   if (e != hipSuccess && rs == GIFT_OK) rs = hip_fail(e, "staging upload");
   g_prof_before = g_prof_after = nullptr;
-  e = lease.release(e == hipSuccess ? call_ev : nullptr);
+  e = lease.release(call_ev);
   if (rs == GIFT_OK && e != hipSuccess) rs = hip_fail(e, "device scratch release");
   return rs;
 }
@@ -1215,7 +1245,7 @@ gift_status gift_check_owner(const gift_segment_table* st, const uint32_t* label
   if (e != hipSuccess) return hip_fail(e, "device scratch");
   SegDesc* d = (SegDesc*)lease.ptr;
   Staging* sg = staging_for(dev);
-  hipEvent_t call_ev = nullptr;  // recorded behind the prologue
+  EventMark call_ev;  // the event recorded behind the prologue
   e = sg ? sg->upload(d, P.descs.data(), bytes, stream,
                       [&](const void* src) {
                         return launch_prologue(d, src, bytes, n, kNoBids, labels, st->verdicts, nullptr, nullptr,
@@ -1223,7 +1253,7 @@ gift_status gift_check_owner(const gift_segment_table* st, const uint32_t* label
                       },
                       false, &call_ev)
          : hipErrorInvalidDevice;
-  hipError_t e2 = lease.release(e == hipSuccess ? call_ev : nullptr);
+  hipError_t e2 = lease.release(call_ev);
   if (e != hipSuccess) return hip_fail(e, "check_owner");
   if (e2 != hipSuccess) return hip_fail(e2, "device scratch release");
   return GIFT_OK;
@@ -1261,7 +1291,7 @@ static gift_status run_tokens(bool decrypt, const gift_segment_table* st, uint64
   // plan has such gaps is the output cleared first, the token kernel then
   // overwrites every covered entry
   const bool gaps = !P.zr.empty();
-  hipEvent_t call_ev = nullptr;  // recorded behind the call's last kernel
+  EventMark call_ev;  // the event recorded behind the call's last kernel
   auto rest = [&]() -> hipError_t {
     hipError_t r = hipSuccess;
     if (gaps)
@@ -1288,7 +1318,7 @@ static gift_status run_tokens(bool decrypt, const gift_segment_table* st, uint64
   } else {
     e = rest();
   }
-  hipError_t e2 = lease.release(e == hipSuccess ? call_ev : nullptr);
+  hipError_t e2 = lease.release(call_ev);
   if (e != hipSuccess) return hip_fail(e, "token kernels");
   if (e2 != hipSuccess) return hip_fail(e2, "device scratch release");
   return GIFT_OK;
