@@ -507,6 +507,48 @@ def test_two_threads_on_two_streams_share_a_key_table(kt3):
             assert ver[:2].tolist() == [gift.SEG_OK, gift.SEG_OK]
 
 
+def test_a_call_does_not_wait_for_another_streams_call(kt3):
+    # A call's staging event also marks its scratch buffer's last use, and the
+    # staging ring hands a completed event out again, here to a call on
+    # stream B queued behind a long busy wait.  The next call on stream A must
+    # not wait for stream B through that event.
+    import time
+    keys, nb, kt = kt3
+    n_rows, rb = 16, 8192
+    table = [(0, 8, 0, 900), (8, 8, 1, 901)]
+    data_np = rng.integers(0, 256, n_rows * rb, dtype=np.uint8)
+    d = dev_u8(data_np)
+    outs = [torch.empty_like(d) for _ in range(3)]
+    tags = [torch.zeros(32, dtype=torch.uint8, device=DEV) for _ in range(3)]
+    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+    # size a bounded busy wait of about 0.3 s on this GPU
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    torch.cuda._sleep(10 ** 7)
+    torch.cuda.synchronize()
+    per_cycle = (time.perf_counter() - t0) / 1e7
+    if per_cycle <= 0:
+        pytest.skip("torch.cuda._sleep does not wait on this build")
+    cycles = int(min(0.3 / per_cycle, 5e10))
+    gift.seal(d, n_rows, rb, table, kt, nb, outs[0], tags[0], stream=sa)
+    torch.cuda.synchronize()  # A's call is done: its staging event goes back to the ring's pool
+    with torch.cuda.stream(sb):
+        torch.cuda._sleep(cycles)
+    gift.seal(d, n_rows, rb, table, kt, nb, outs[1], tags[1], stream=sb)  # takes that event, behind the wait
+    t0 = time.perf_counter()
+    gift.seal(d, n_rows, rb, table, kt, nb, outs[2], tags[2], stream=sa)
+    sa.synchronize()
+    dt = time.perf_counter() - t0
+    b_busy = not sb.query()
+    torch.cuda.synchronize()
+    assert b_busy, "stream B finished before the check could see it"
+    assert dt < 0.1, f"the call on stream A waited {dt:.3f} s for stream B"
+    st, o_out, o_tags, _ = oracle.seal(data_np, n_rows, rb, table, keys, nb)
+    assert st == 0
+    for o, t in zip(outs, tags):
+        assert host(o).tobytes() == o_out.tobytes() and host(t).tobytes() == o_tags.tobytes()
+
+
 def test_scratch_reuse_across_streams_threads_and_sizes(kt3):
     # the library keeps each stream's device scratch between calls: more
     # streams than it caches (buffers change hands), two host threads on one
