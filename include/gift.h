@@ -291,7 +291,9 @@ gift_status gift_open_paged(const gift_paged_kv* kv, const gift_request* reqs, u
  *   out             device, n_tokens*16 bytes.
  *   st              segments over token indices; iv_seq, row_labels and
  *                   verdicts are not used; users must be < n_users.
- * Errors: GIFT_E_INVALID, GIFT_E_RANGE, GIFT_E_OVERLAP as for gift_seal.
+ * Errors: GIFT_E_INVALID, GIFT_E_RANGE, GIFT_E_OVERLAP as for gift_seal;
+ * GIFT_E_TOO_LARGE past 2^32 - 1 chunks of 64 tokens of one segment (about
+ * 2^38 tokens).
  */
 gift_status gift_token_encrypt(const gift_segment_table* st, const uint64_t* tokens, const uint64_t* nonces,
                                uint64_t n_tokens, gift_key_table kt, uint64_t eos_token, uint8_t* out,
@@ -307,6 +309,7 @@ gift_status gift_token_encrypt(const gift_segment_table* st, const uint64_t* tok
  * covered by no segment give 0.
  *   blocks      device, n_tokens*16 bytes.
  *   tokens_out  device, n_tokens u64; nonces_out device, n_tokens u64, or NULL.
+ * Errors as for gift_token_encrypt.
  */
 gift_status gift_token_decrypt(const gift_segment_table* st, const uint8_t* blocks, uint64_t n_tokens,
                                gift_key_table kt, uint64_t eos_token, uint64_t* tokens_out, uint64_t* nonces_out,

@@ -1279,11 +1279,27 @@ static gift_status run_tokens(bool decrypt, const gift_segment_table* st, uint64
   if (dev != kt->device) return fail(GIFT_E_INVALID, "key table belongs to device %d, current is %d", kt->device, dev);
   Plan P;
   build_plan(st->segs, n, n_tokens, 1, nullptr, nullptr, nullptr, P);
+  // staged: the descriptors, then the first 64-token chunk of each segment
+  // (an exclusive scan; the token kernel's work items are these chunks)
+  const size_t o_cb = sizeof(SegDesc) * n;
+  const size_t staged = o_cb + ((4ull * (n + 1) + 15) & ~(size_t)15);
+  std::vector<uint8_t> host(n > 0 ? staged : 0);
+  uint64_t n_chunks = 0;
+  if (n > 0) {
+    memcpy(host.data(), P.descs.data(), o_cb);
+    uint32_t* cb = (uint32_t*)(host.data() + o_cb);
+    for (uint32_t i = 0; i < n; i++) {
+      cb[i] = (uint32_t)n_chunks;
+      n_chunks += (st->segs[i].row_count + kTokenChunk - 1) / kTokenChunk;
+      if (n_chunks > UINT32_MAX) return fail(GIFT_E_TOO_LARGE, "more than 2^32 - 1 chunks of %u tokens", kTokenChunk);
+    }
+    cb[n] = (uint32_t)n_chunks;
+  }
   SegDesc* d = nullptr;
   hipError_t e = hipSuccess;
   ScratchLease lease;
   if (n > 0) {
-    e = lease.acquire(dev, stream, sizeof(SegDesc) * n);
+    e = lease.acquire(dev, stream, staged);
     if (e != hipSuccess) return hip_fail(e, "device scratch");
     d = (SegDesc*)lease.ptr;
   }
@@ -1298,18 +1314,17 @@ static gift_status run_tokens(bool decrypt, const gift_segment_table* st, uint64
       r = decrypt ? launch_wipe(tokens_out, 8ull * n_tokens, stream) : launch_wipe(blocks_out, 16ull * n_tokens, stream);
     if (r == hipSuccess && gaps && decrypt && nonces_out) r = launch_wipe(nonces_out, 8ull * n_tokens, stream);
     if (r == hipSuccess)
-      r = launch_tokens(d, n, decrypt, tokens, nonces, blocks_in, blocks_out, tokens_out, nonces_out, eos_token,
-                        kt->dev, stream);
+      r = launch_tokens(d, (const uint32_t*)((const uint8_t*)d + o_cb), n, (uint32_t)n_chunks, decrypt, tokens,
+                        nonces, blocks_in, blocks_out, tokens_out, nonces_out, eos_token, kt->dev, stream);
     return r;
   };
   if (n > 0) {
     // the token kernels are enqueued while the staging slot is held (one
     // event behind the last of them frees the slot)
     Staging* sg = staging_for(dev);
-    const size_t bytes = sizeof(SegDesc) * n;
-    e = sg ? sg->upload(d, P.descs.data(), bytes, stream,
+    e = sg ? sg->upload(d, host.data(), staged, stream,
                         [&](const void* src) {
-                          hipError_t r = launch_prologue(d, src, bytes, n, kNoBids, nullptr, nullptr, nullptr,
+                          hipError_t r = launch_prologue(d, src, staged, n, kNoBids, nullptr, nullptr, nullptr,
                                                          nullptr, nullptr, 0u, 0u, nullptr, stream);
                           return r != hipSuccess ? r : rest();
                         },

@@ -214,8 +214,11 @@ hipError_t launch_zero_failed(const SegDesc* segs, uint32_t n_segs, const uint32
                               uint32_t grid, hipStream_t s);
 // Per-token block encryption (decrypt == true: the inverse).  Rows of the
 // descriptors are token indices.
-hipError_t launch_tokens(const SegDesc* segs, uint32_t n_segs, bool decrypt, const uint64_t* tokens,
-                         const uint64_t* nonces, const uint8_t* blocks_in, uint8_t* blocks_out, uint64_t* tokens_out,
-                         uint64_t* nonces_out, uint64_t eos_token, KeyTableDev kt, hipStream_t s);
+// tokens per workgroup of the token kernel (chunks never span two segments)
+constexpr uint32_t kTokenChunk = 64;
+hipError_t launch_tokens(const SegDesc* segs, const uint32_t* chunk_base, uint32_t n_segs, uint32_t n_chunks,
+                         bool decrypt, const uint64_t* tokens, const uint64_t* nonces, const uint8_t* blocks_in,
+                         uint8_t* blocks_out, uint64_t* tokens_out, uint64_t* nonces_out, uint64_t eos_token,
+                         KeyTableDev kt, hipStream_t s);
 
 }  // namespace gift

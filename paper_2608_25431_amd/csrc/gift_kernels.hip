@@ -1216,11 +1216,17 @@ __global__ __launch_bounds__(256) void k_wipe(uint8_t* p, size_t bytes) {
 
 // ---------------------------------------------------------------------------
 // Per-token encryption (token || nonce as one block under the owner's key,
-// the end-of-sequence token as the all-0xFF block).  One workgroup per
-// segment; outputs of uncovered tokens were zeroed before this launch.
+// the end-of-sequence token as the all-0xFF block).  The work is cut into
+// chunks of 64 tokens of one segment: chunk_base[s] is the first chunk of
+// segment s (an exclusive scan of ceil(row_count / 64), chunk_base[n_segs] =
+// n_chunks), and a workgroup of 64 threads takes one chunk at a time,
+// finding its segment by binary search.  Outputs of uncovered tokens were
+// zeroed before this launch.
 // ---------------------------------------------------------------------------
 template <bool DECRYPT>
-__global__ __launch_bounds__(64) void k_tokens(const SegDesc* __restrict__ segs, uint32_t n_segs,
+__global__ __launch_bounds__(kTokenChunk) void k_tokens(const SegDesc* __restrict__ segs,
+                                                        const uint32_t* __restrict__ chunk_base, uint32_t n_segs,
+                                                        uint32_t n_chunks,
                                                const uint64_t* __restrict__ tokens,
                                                const uint64_t* __restrict__ nonces,
                                                const uint8_t* __restrict__ blocks_in, uint8_t* __restrict__ blocks_out,
@@ -1233,10 +1239,19 @@ __global__ __launch_bounds__(64) void k_tokens(const SegDesc* __restrict__ segs,
     isb[i] = c_aes.inv_sbox[i];
   }
   __syncthreads();
-  for (uint32_t s = blockIdx.x; s < n_segs; s += gridDim.x) {
+  for (uint32_t b = blockIdx.x; b < n_chunks; b += gridDim.x) {
+    // the segment of chunk b: chunk_base[lo] <= b < chunk_base[hi] throughout
+    uint32_t lo = 0, hi = n_segs;
+    while (hi - lo > 1u) {
+      const uint32_t mid = lo + (hi - lo) / 2u;
+      if (chunk_base[mid] <= b) lo = mid;
+      else hi = mid;
+    }
+    const uint32_t s = lo;
     const uint64_t rb = segs[s].row_begin, rc = segs[s].row_count;
     const uint32_t user = segs[s].user;
-    for (uint64_t i = threadIdx.x; i < rc; i += blockDim.x) {
+    const uint64_t i = (uint64_t)kTokenChunk * (b - chunk_base[s]) + threadIdx.x;
+    if (i < rc) {
       const uint64_t r = rb + i;
       if (!DECRYPT) {
         const uint64_t t = tokens[r], n = nonces[r];
@@ -1457,17 +1472,18 @@ hipError_t launch_zero_ranges(uint8_t* out, const ZeroRange* r, uint32_t n, cons
   return hipGetLastError();
 }
 
-hipError_t launch_tokens(const SegDesc* segs, uint32_t n_segs, bool decrypt, const uint64_t* tokens,
-                         const uint64_t* nonces, const uint8_t* blocks_in, uint8_t* blocks_out, uint64_t* tokens_out,
-                         uint64_t* nonces_out, uint64_t eos_token, KeyTableDev kt, hipStream_t s) {
-  if (n_segs == 0) return hipSuccess;
-  const uint32_t grid = n_segs < 65535u ? n_segs : 65535u;
+hipError_t launch_tokens(const SegDesc* segs, const uint32_t* chunk_base, uint32_t n_segs, uint32_t n_chunks,
+                         bool decrypt, const uint64_t* tokens, const uint64_t* nonces, const uint8_t* blocks_in,
+                         uint8_t* blocks_out, uint64_t* tokens_out, uint64_t* nonces_out, uint64_t eos_token,
+                         KeyTableDev kt, hipStream_t s) {
+  if (n_segs == 0 || n_chunks == 0) return hipSuccess;
+  const uint32_t grid = n_chunks < 65535u ? n_chunks : 65535u;
   if (decrypt)
-    hipLaunchKernelGGL(k_tokens<true>, dim3(grid), dim3(64), 0, s, segs, n_segs, tokens, nonces, blocks_in,
-                       blocks_out, tokens_out, nonces_out, eos_token, kt);
+    hipLaunchKernelGGL(k_tokens<true>, dim3(grid), dim3(kTokenChunk), 0, s, segs, chunk_base, n_segs, n_chunks,
+                       tokens, nonces, blocks_in, blocks_out, tokens_out, nonces_out, eos_token, kt);
   else
-    hipLaunchKernelGGL(k_tokens<false>, dim3(grid), dim3(64), 0, s, segs, n_segs, tokens, nonces, blocks_in,
-                       blocks_out, tokens_out, nonces_out, eos_token, kt);
+    hipLaunchKernelGGL(k_tokens<false>, dim3(grid), dim3(kTokenChunk), 0, s, segs, chunk_base, n_segs, n_chunks,
+                       tokens, nonces, blocks_in, blocks_out, tokens_out, nonces_out, eos_token, kt);
   return hipGetLastError();
 }
 

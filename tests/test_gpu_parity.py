@@ -877,6 +877,10 @@ def test_token_encryption_matches_oracle():
     # 100k tokens of one user (many rows per workgroup)
     big = W.u64s(1, "big_tok", 100000) % np.uint64(128256)
     token_case(w.keys, kt, [(0, 100000, 7, 0)], big, W.u64s(1, "big_non", 100000), eos)
+    # 64-token chunks that end inside, at and just past a segment, a table out
+    # of row order, gaps between segments
+    token_case(w.keys, kt, [(300, 65, 4, 0), (0, 64, 2, 0), (64, 63, 3, 0), (130, 1, 5, 0), (131, 128, 6, 0),
+                            (500, 200, 2, 1)], big[:800], W.u64s(2, "chunk_non", 800), eos)
     # validation agrees with the oracle
     dt, dn = dev_u64(tok[:8]), dev_u64(non[:8])
     out = torch.zeros(128, dtype=torch.uint8, device=DEV)
