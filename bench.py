@@ -239,7 +239,7 @@ def lds_probe(cus):
             "mixed_over_additive": round(clk[2] / additive, 3), "clock_mhz": round(min(mhz), 1)}
 
 
-def time_tokens(gift, W, torch, steps=50):
+def time_tokens(gift, W, torch, steps=200):
     """Per-token encryption (GIFT Sec. 4.5) of one decode step's output
     tokens: the decode_batch workload's 2588 tokens of 1024 users."""
     import numpy as np
