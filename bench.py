@@ -10,7 +10,9 @@ per-block AES-CTR/GHASH kernel and the per-segment tag finalize.  Inputs are
 resident in HBM before timing starts.  The timed pass runs the steps back to
 back with no event between them; a second pass of the same steps with
 events on the launch stream gives the median step and the per-block
-kernel's duration.  Re-sealing the same plaintext under the
+kernel's duration; host_enqueue_us is the host time of one call started
+with the GPU idle.  --library times another build of libgift.so (one made
+from an older commit, say) with this same protocol.  Re-sealing the same plaintext under the
 same IVs each step yields the same ciphertext, so no keystream is reused on
 new data.
 
