@@ -241,6 +241,27 @@ def lds_probe(cus):
             "mixed_over_additive": round(clk[2] / additive, 3), "clock_mhz": round(min(mhz), 1)}
 
 
+def hbm_copy(torch, nbytes=4 << 30, reps=5):
+    """The practical HBM ceiling beside the 8 TB/s peak: a plain
+    device-to-device copy (torch's copy kernel) of nbytes, read and write
+    bytes over its time, median of reps."""
+    src = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    ts = []
+    for _ in range(reps):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        dst.copy_(src)
+        b.record()
+        b.synchronize()
+        ts.append(a.elapsed_time(b) * 1e-3)
+    del src, dst
+    t = sorted(ts)[reps // 2]
+    return {"gbps": round(2 * nbytes / t / 1e9, 1), "bytes_moved": 2 * nbytes,
+            "kind": f"device-to-device copy of {nbytes >> 30} GiB (torch), read + written bytes, median of {reps}"}
+
+
 def time_tokens(gift, W, torch, steps=200):
     """Per-token encryption (GIFT Sec. 4.5) of one decode step's output
     tokens: the decode_batch workload's 2588 tokens of 1024 users."""
@@ -606,6 +627,9 @@ def main():
     if w.name == "llama3_8b_kv" and not w.in_place:
         res["paged_seal"] = time_paged(gift, t, w, kt, data, out, max(5, args.steps // 4), args.warmup, torch)
         log(f"[bench] paged seal: {res['paged_seal']}")
+    res["hbm_copy"] = hbm_copy(torch)
+    res["roofline"]["frac_of_copy"] = round(achieved / res["hbm_copy"]["gbps"], 4)
+    log(f"[bench] HBM copy: {res['hbm_copy']['gbps']} GB/s")
     res["token_encryption"] = time_tokens(gift, W, torch)
     log(f"[bench] token encryption: {res['token_encryption']}")
     res["host_tracking"] = time_host_tracking(gift)
