@@ -61,10 +61,11 @@ PROFILED_SOURCES = ["paper_2608_25431_amd/csrc/gift_kernels.hip", "paper_2608_25
                     "paper_2608_25431_amd/csrc/gift_internal.hpp"]
 
 
-def profiled_traffic(workload):
-    """HBM bytes per launch of the seal kernel from the committed rocprofv3
-    counter runs (profiles/traffic.json), or None when the kernel sources have
-    changed since those counters were taken or the workload differs."""
+def profiled_traffic(workload, field="traffic_bytes_per_launch"):
+    """A figure of the seal kernel from the committed rocprofv3 counter runs
+    (profiles/traffic.json): HBM bytes per launch, or VALU instructions per
+    block; None when the kernel sources have changed since those counters
+    were taken or the workload differs."""
     import hashlib
     try:
         rec = json.load(open(os.path.join(ROOT, "profiles", "traffic.json")))
@@ -75,7 +76,7 @@ def profiled_traffic(workload):
         return None
     if rec.get("sources_sha256") != h.hexdigest() or rec.get("workload") != workload:
         return None
-    return rec["traffic_bytes_per_launch"]
+    return rec.get(field)
 
 
 def worker_threads():
@@ -614,6 +615,19 @@ def main():
             "probe": probe,
             "peak_at_probe_clock": round(at_clock, 1),
             "frac_at_probe_clock": round(kernel_sealed / at_clock, 4)}
+    # The VALU ceiling of the same kernel: its VALU instructions per block
+    # (one lane-op per block per instruction, from the committed counter
+    # runs) against 64 lane-ops per CU per clock (4 SIMDs x 16 lanes) at 2.4 GHz.
+    valu = profiled_traffic(w.name, "valu_insts_per_block") if labels is not None else None
+    if valu:
+        cus_v = torch.cuda.get_device_properties(0).multi_processor_count
+        v_peak = 16 * cus_v * 64 * 2.4e9 / valu / 1e9
+        k_sealed = tiled / (k_ms * 1e-3) / 1e9
+        res["valu_roofline"] = {"bound": "valu", "kernel": "k_gcm_tiles<seal>", "achieved": round(k_sealed, 2),
+                                "peak": round(v_peak, 1), "unit": "GB/s sealed", "frac": round(k_sealed / v_peak, 4),
+                                "valu_insts_per_block": valu,
+                                "peak_source": "VALU instructions per block from the committed rocprofv3 counters "
+                                               "(SQ_INSTS_VALU), 64 lane-ops per CU per clock at 2.4 GHz"}
     # The target is half of the HBM roofline.  The kernel is bound by LDS
     # reads instead (T-table AES and table GHASH): its LDS ceiling, and the
     # AES lookups alone, expressed as fractions of the HBM roofline (2 bytes
