@@ -110,6 +110,8 @@ def test_brute_force_tiny_tensors(kt3, row_bytes):
     (1000, [1, 17, 2100, 3, 4200]),            # unaligned starts, multi-tile
     (65536 + 16, [33, 1, 70]),                 # aligned, tiles end mid-row
     (48, [1, 2, 21, 22, 23, 44000]),           # small segments next to a 2 MiB one
+    (16, [63, 64, 65, 1, 1024, 1025]),         # the small-segment limit (64 blocks) exactly, and one row of a tile
+    (1, [1023, 1024, 1025, 1, 15, 17]),        # byte lengths around 64 blocks and around one block
 ])
 def test_ragged_multi_tile_every_byte(kt3, row_bytes, rows):
     keys, nb, kt = kt3
