@@ -44,8 +44,25 @@ from paper_2608_25431_amd import workloads as W  # noqa: E402
 PIECE = 64 << 20  # bytes per oracle GCTR job on the in-place workload
 
 
+_capsys = None
+
+
+@pytest.fixture(autouse=True)
+def _progress_uncaptured(capsys):
+    """Progress lines go to the real stdout even when pytest captures the
+    tests' output (-q without -s), so a long comparison never falls silent."""
+    global _capsys
+    _capsys = capsys
+    yield
+    _capsys = None
+
+
 def log(msg):
-    print(f"[fullsize] {msg}", flush=True)
+    if _capsys is not None:
+        with _capsys.disabled():
+            print(f"[fullsize] {msg}", flush=True)
+    else:
+        print(f"[fullsize] {msg}", flush=True)
 
 
 def table1(t, i):
