@@ -27,3 +27,20 @@ def test_a_distributed_launch_is_refused():
 def test_unknown_workload_is_rejected():
     r = run("--workload", "no_such_workload")
     assert r.returncode != 0 and "invalid choice" in r.stderr
+
+
+def test_profiled_figures_belong_to_these_kernel_sources():
+    """The HBM traffic and VALU count that bench.py reports come from the
+    committed counter runs, and only while the kernel sources hash to the ones
+    profiled: a kernel change needs new counter runs (profiles/traffic.json)."""
+    import importlib.util
+    spec = importlib.util.spec_from_file_location("bench_mod", os.path.join(ROOT, "bench.py"))
+    bench = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(bench)
+    traffic = bench.profiled_traffic("llama3_8b_kv")
+    valu = bench.profiled_traffic("llama3_8b_kv", "valu_insts_per_block")
+    assert traffic is not None and valu is not None, "kernel sources changed since profiles/traffic.json"
+    # the algorithmic bytes of the workload's seal kernel, and at most 1% above them
+    assert 18123587584 <= traffic <= 1.01 * 18123587584
+    assert 300 < valu < 600
+    assert bench.profiled_traffic("tamper") is None  # profiled on one workload only
