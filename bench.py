@@ -219,27 +219,33 @@ def lds_probe(cus):
     address forms of the seal kernel: random 4-byte lookups into per-lane
     table copies (lane-reads per CU per clock) and 16-byte nibble-table reads
     (bytes per CU per clock), issued back to back with nothing else; a mixed
-    stream of both checks that their costs add; and the shader clock (MHz)."""
+    stream of both checks that their costs add; the vector-ALU rates of the
+    kernel's two most common instructions, v_bitop3_b32 and v_perm_b32
+    (lane-ops per CU per clock, independent instructions back to back); and
+    the shader clock (MHz)."""
     lib_path = os.path.join(ROOT, "paper_2608_25431_amd", "libgift_probe.so")
     if not os.path.exists(lib_path):
         return None
     L = ctypes.CDLL(lib_path)
     D = ctypes.POINTER(ctypes.c_double)
     L.gift_probe_lds.argtypes = [ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint32, D, D]
-    threads, batch, mixed32 = 1024, 15, 13  # per workgroup and step, as the probes issue them
+    threads, batch, mixed32, valu_ops = 1024, 15, 13, 8  # per workgroup and step, as the probes issue them
     clk, mhz = [], []
-    for mode in (0, 1, 2):
+    for mode in (0, 1, 2, 3, 4):
         c, m = ctypes.c_double(), ctypes.c_double()
         rc = L.gift_probe_lds(mode, cus, 20000, ctypes.byref(c), ctypes.byref(m))
         if rc != 0 or c.value <= 0:
-            raise RuntimeError(f"LDS probe {mode} failed (hipError {rc})")
+            raise RuntimeError(f"probe {mode} failed (hipError {rc})")
         clk.append(c.value)
         mhz.append(m.value)
     r32 = threads * batch / clk[0]
     r128 = threads * batch * 16 / clk[1]
     additive = threads * mixed32 / r32 + threads * (batch - mixed32) * 16 / r128
     return {"b32_lane_reads_per_clk": round(r32, 2), "b128_bytes_per_clk": round(r128, 1),
-            "mixed_over_additive": round(clk[2] / additive, 3), "clock_mhz": round(min(mhz), 1)}
+            "mixed_over_additive": round(clk[2] / additive, 3),
+            "valu_bitop3_lane_ops_per_clk": round(threads * valu_ops / clk[3], 2),
+            "valu_perm_lane_ops_per_clk": round(threads * valu_ops / clk[4], 2),
+            "clock_mhz": round(min(mhz), 1)}
 
 
 def hbm_copy(torch, nbytes=4 << 30, reps=5):
@@ -617,17 +623,33 @@ def main():
             "frac_at_probe_clock": round(kernel_sealed / at_clock, 4)}
     # The VALU ceiling of the same kernel: its VALU instructions per block
     # (one lane-op per block per instruction, from the committed counter
-    # runs) against 64 lane-ops per CU per clock (4 SIMDs x 16 lanes) at 2.4 GHz.
+    # runs), of which the committed instruction mix names the v_perm_b32 and
+    # v_bitop3_b32 ones, each at the lane-op rate its probe measures in this
+    # run and the rest at 64 per CU per clock (4 SIMDs x 16 lanes); at 2.4 GHz.
     valu = profiled_traffic(w.name, "valu_insts_per_block") if labels is not None else None
+    mix = profiled_traffic(w.name, "valu_mix_per_block") if labels is not None else None
     if valu:
         cus_v = torch.cuda.get_device_properties(0).multi_processor_count
-        v_peak = 16 * cus_v * 64 * 2.4e9 / valu / 1e9
+        if probe and mix:
+            n_perm, n_bitop3 = mix["v_perm_b32"], mix["v_bitop3_b32"]
+            clk_valu = (n_perm / probe["valu_perm_lane_ops_per_clk"]
+                        + n_bitop3 / probe["valu_bitop3_lane_ops_per_clk"] + (valu - n_perm - n_bitop3) / 64.0)
+            lane_ops = valu / clk_valu
+        else:
+            lane_ops = 64.0
+        v_peak = 16 * cus_v * lane_ops * 2.4e9 / valu / 1e9
         k_sealed = tiled / (k_ms * 1e-3) / 1e9
         res["valu_roofline"] = {"bound": "valu", "kernel": "k_gcm_tiles<seal>", "achieved": round(k_sealed, 2),
                                 "peak": round(v_peak, 1), "unit": "GB/s sealed", "frac": round(k_sealed / v_peak, 4),
                                 "valu_insts_per_block": valu,
+                                "lane_ops_per_cu_clk": round(lane_ops, 2), "mix_per_block": mix,
                                 "peak_source": "VALU instructions per block from the committed rocprofv3 counters "
-                                               "(SQ_INSTS_VALU), 64 lane-ops per CU per clock at 2.4 GHz"}
+                                               "(SQ_INSTS_VALU) at "
+                                               + ("the lane-op rates the VALU probes of libgift_probe.so measure in "
+                                                  "this run for v_perm_b32 and v_bitop3_b32, weighted by the kernel's "
+                                                  "committed instruction mix, and 64 for the rest"
+                                                  if probe and mix else "64 lane-ops (4 SIMDs x 16 lanes)")
+                                               + " per CU per clock, at the 2.4 GHz peak clock; not a published figure"}
     # The target is half of the HBM roofline.  The kernel is bound by LDS
     # reads instead (T-table AES and table GHASH): its LDS ceiling, and the
     # AES lookups alone, expressed as fractions of the HBM roofline (2 bytes

@@ -1,4 +1,5 @@
-// LDS read-rate probes for the benchmark's LDS ceiling of the seal kernel.
+// LDS read-rate and VALU issue-rate probes for the benchmark's LDS and VALU
+// ceilings of the seal kernel.
 //
 // The seal kernel's per-block work is bound by two kinds of LDS reads: random
 // 4-byte T-table lookups (each lane in its own copy of the table, so a wave's
@@ -10,7 +11,8 @@
 // with one wait per batch and no other arithmetic, on one 1024-thread
 // workgroup per CU with the LDS allocation of the seal kernel.  The shader
 // clock counts the batches' time; the reference clock beside it gives the
-// clock rate.
+// clock rate.  The VALU probes (k_valu) issue the kernel's two most common
+// vector instructions the same way.
 //
 // Built into libgift_probe.so, apart from the library: only the benchmark
 // loads it.
@@ -82,19 +84,61 @@ __global__ __launch_bounds__(kThreads) void k_probe(uint32_t steps, uint32_t* si
   }
 }
 
+// Vector-ALU rate of the seal kernel's two most common instructions: eight
+// accumulators per thread, each step one v_bitop3_b32 (OP 0) or one
+// v_perm_b32 (OP 1) per accumulator on its own and other accumulators'
+// values (the byte selectors stay fixed), so a wave always has independent
+// instructions to issue.  It holds the seal kernel's LDS allocation, so that
+// it too runs one workgroup per CU.
+template <int OP>
+__global__ __launch_bounds__(kThreads) void k_valu(uint32_t steps, uint32_t* sink, unsigned long long* stamps) {
+  __shared__ uint8_t smem[kLdsBytes];
+  if (threadIdx.x == 0) smem[kLdsBytes - 1u - (blockIdx.x & 63u)] = 1;
+  uint32_t a[8], sel[8];
+#pragma unroll
+  for (int k = 0; k < 8; k++) {
+    a[k] = (threadIdx.x + 1u) * (2654435761u + 40503u * (uint32_t)k);
+    sel[k] = ((threadIdx.x + (uint32_t)k) * 0x01030507u) & 0x07070707u;  // byte selectors 0-7
+  }
+  __syncthreads();
+  const unsigned long long c0 = __builtin_amdgcn_s_memtime(), r0 = __builtin_amdgcn_s_memrealtime();
+  for (uint32_t s = 0; s < steps; s++) {
+#pragma unroll
+    for (int k = 0; k < 8; k++) {
+      if (OP == 0)
+        a[k] = __builtin_amdgcn_bitop3_b32(a[k], a[(k + 1) & 7], a[(k + 3) & 7], 0x96);
+      else
+        a[k] = __builtin_amdgcn_perm(a[k], a[(k + 1) & 7], sel[k]);
+    }
+  }
+  __syncthreads();
+  const unsigned long long c1 = __builtin_amdgcn_s_memtime(), r1 = __builtin_amdgcn_s_memrealtime();
+  uint32_t acc = 0;
+#pragma unroll
+  for (int k = 0; k < 8; k++) acc ^= a[k];
+  if (threadIdx.x == 0) acc ^= smem[kLdsBytes - 1u - (blockIdx.x & 63u)];
+  sink[blockIdx.x * kThreads + threadIdx.x] = acc;
+  if (threadIdx.x == 0) {
+    stamps[2 * blockIdx.x] = c1 - c0;
+    stamps[2 * blockIdx.x + 1] = r1 - r0;
+  }
+}
+
 }  // namespace
 
 extern "C" {
 
-// Runs probe `mode` (0, 1 or 2, as above) on `cus` workgroups of `steps`
-// steps, once to warm up and once timed, and returns in *clk_per_step the
-// mean shader clocks per step of one workgroup (1024 threads, kBatch reads
-// each per step) and in *mhz the shader clock rate over the same interval
-// (shader clocks against the 100 MHz reference clock).  Synchronous on the
-// null stream; allocates and frees its own buffers.  Returns a hipError_t
-// (hipErrorInvalidValue for a bad mode, zero counts or null pointers).
+// Runs probe `mode` on `cus` workgroups of `steps` steps, once to warm up and
+// once timed, and returns in *clk_per_step the mean shader clocks per step
+// of one workgroup (1024 threads) and in *mhz the shader clock rate over the
+// same interval (shader clocks against the 100 MHz reference clock).  Modes
+// 0-2 are the LDS probes (kBatch reads per thread and step, as above); 3 and
+// 4 the VALU probes (8 v_bitop3_b32 or 8 v_perm_b32 per thread and step).
+// Synchronous on the null stream; allocates and frees its own buffers.
+// Returns a hipError_t (hipErrorInvalidValue for a bad mode, zero counts or
+// null pointers).
 int gift_probe_lds(uint32_t mode, uint32_t cus, uint32_t steps, double* clk_per_step, double* mhz) {
-  if (mode > 2 || cus == 0 || steps == 0 || !clk_per_step || !mhz) return (int)hipErrorInvalidValue;
+  if (mode > 4 || cus == 0 || steps == 0 || !clk_per_step || !mhz) return (int)hipErrorInvalidValue;
   uint32_t* sink = nullptr;
   unsigned long long* st = nullptr;
   hipError_t e = hipMalloc((void**)&sink, sizeof(uint32_t) * kThreads * cus);
@@ -103,6 +147,8 @@ int gift_probe_lds(uint32_t mode, uint32_t cus, uint32_t steps, double* clk_per_
     if (mode == 0) hipLaunchKernelGGL(k_probe<0>, dim3(cus), dim3(kThreads), 0, 0, steps, sink, st);
     if (mode == 1) hipLaunchKernelGGL(k_probe<1>, dim3(cus), dim3(kThreads), 0, 0, steps, sink, st);
     if (mode == 2) hipLaunchKernelGGL(k_probe<2>, dim3(cus), dim3(kThreads), 0, 0, steps, sink, st);
+    if (mode == 3) hipLaunchKernelGGL(k_valu<0>, dim3(cus), dim3(kThreads), 0, 0, steps, sink, st);
+    if (mode == 4) hipLaunchKernelGGL(k_valu<1>, dim3(cus), dim3(kThreads), 0, 0, steps, sink, st);
     e = hipGetLastError();
   }
   if (e == hipSuccess) e = hipDeviceSynchronize();

@@ -43,4 +43,6 @@ def test_profiled_figures_belong_to_these_kernel_sources():
     # the algorithmic bytes of the workload's seal kernel, and at most 1% above them
     assert 18123587584 <= traffic <= 1.01 * 18123587584
     assert 300 < valu < 600
+    mix = bench.profiled_traffic("llama3_8b_kv", "valu_mix_per_block")
+    assert mix is not None and 0 < mix["v_perm_b32"] + mix["v_bitop3_b32"] < valu
     assert bench.profiled_traffic("tamper") is None  # profiled on one workload only
