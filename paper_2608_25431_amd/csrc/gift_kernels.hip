@@ -702,7 +702,7 @@ __global__ __launch_bounds__(64) void k_small(GcmArgs a) {
       a.verdicts[s] = ok ? kVerdictOk : kVerdictAuthFail;
     }
   }
-  if (OPEN) ok = __shfl(ok, 0, 64);
+  if (OPEN) ok = __builtin_amdgcn_readlane((int)ok, 0) != 0;
   if (valid) store_block(dst, ok ? o : u128_zero(), n, aligned);
 }
 
@@ -745,20 +745,30 @@ __device__ __forceinline__ uint32_t tile_rows_of(uint32_t m, uint32_t t) {
   return base >= 0 ? (uint32_t)kRows : (uint32_t)kRows - (uint32_t)((uint64_t)(-base) / kThreads);
 }
 
-__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x, uint32_t lane) {
-#pragma unroll
-  for (int d = 1; d < 64; d <<= 1) {
-    const uint32_t y = __shfl_up(x, d, 64);
-    if (lane >= (uint32_t)d) x += y;
-  }
+// Inclusive prefix sum over the wave's 64 lanes on the VALU's data-parallel
+// primitives (no LDS round trips): row shifts by 1, 2, 4 and 8 scan each row
+// of 16 lanes (a lane with no source adds 0), then the broadcasts of lane 15
+// into rows 1 and 3 and of lane 31 into rows 2 and 3 carry the row totals up.
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x) {
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xF, 0xF, false);  // row_shr:1
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xF, 0xF, false);  // row_shr:2
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xF, 0xF, false);  // row_shr:4
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xF, 0xF, false);  // row_shr:8
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x142, 0xA, 0xF, false);  // row_bcast:15
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x143, 0xC, 0xF, false);  // row_bcast:31
   return x;
+}
+
+// The sum over the wave, in every lane.
+__device__ __forceinline__ uint32_t wave_sum(uint32_t x) {
+  return (uint32_t)__builtin_amdgcn_readlane((int)wave_incl_scan(x), 63);
 }
 
 // Exclusive prefix sum of v over the workgroup in thread order; *total gets
 // the sum of all.  wsum: one LDS word per wave.
 __device__ uint32_t block_scan(uint32_t v, uint32_t* wsum, uint32_t* total) {
   const uint32_t lane = threadIdx.x & 63u, wave = threadIdx.x >> 6;
-  const uint32_t x = wave_incl_scan(v, lane);
+  const uint32_t x = wave_incl_scan(v);
   __syncthreads();  // wsum is free
   if (lane == 63u) wsum[wave] = x;
   __syncthreads();
@@ -775,7 +785,7 @@ __device__ uint32_t block_scan(uint32_t v, uint32_t* wsum, uint32_t* total) {
 // Exclusive prefix sums of three values at once (one pass of barriers).
 __device__ uint3 block_scan3(uint3 v, uint3* wsum, uint3* total) {
   const uint32_t lane = threadIdx.x & 63u, wave = threadIdx.x >> 6;
-  const uint3 x = make_uint3(wave_incl_scan(v.x, lane), wave_incl_scan(v.y, lane), wave_incl_scan(v.z, lane));
+  const uint3 x = make_uint3(wave_incl_scan(v.x), wave_incl_scan(v.y), wave_incl_scan(v.z));
   __syncthreads();  // wsum is free
   if (lane == 63u) wsum[wave] = x;
   __syncthreads();
@@ -864,14 +874,14 @@ __device__ void expand_tables(const SegBrief* brief, uint32_t n, const ExpandArg
     my_whole += nt - 1;
     atomicAdd(&hist[r], 1u);
   }
-  // the whole tiles below each segment's first tile, and the rows, once per wave
-  for (int d = 32; d >= 1; d >>= 1) {
-    my_whole += __shfl_xor(my_whole, d, 64);
-    my_rows += __shfl_xor(my_rows, d, 64);
-  }
+  // the whole tiles below each segment's first tile, and the rows, once per
+  // wave.  The rows are read only with fewer tiles than CUs, when no thread
+  // has 2^20 of them; capped there, the sums stay within 32 bits.
+  my_whole = wave_sum(my_whole);
+  const uint32_t rows_w = wave_sum((uint32_t)min(my_rows, 1ull << 20));
   if (lane == 0u) {
     if (my_whole) atomicAdd(&hist[kRows], my_whole);
-    if (my_rows) atomicAdd(&rows_all, my_rows);
+    if (rows_w) atomicAdd(&rows_all, (unsigned long long)rows_w);
   }
   uint3 tot;
   const uint3 base0 = block_scan3(make_uint3(my_tiles, my_small, my_runs), wsum3, &tot);
@@ -918,9 +928,9 @@ __device__ void expand_tables(const SegBrief* brief, uint32_t n, const ExpandArg
       static_assert(kSpan <= 128, "two row counts per lane");
       const uint32_t ra = kRows - lane, rb = kRows - 64u - lane;
       const uint32_t ha = lane < kSpan ? hist[ra] : 0u, hb = lane + 64u < kSpan ? hist[rb] : 0u;
-      const uint32_t ia = wave_incl_scan(ha, lane);  // tiles of at least ra rows
-      const uint32_t tot_a = __shfl(ia, 63, 64);
-      const uint32_t ib = tot_a + wave_incl_scan(hb, lane);
+      const uint32_t ia = wave_incl_scan(ha);  // tiles of at least ra rows
+      const uint32_t tot_a = (uint32_t)__builtin_amdgcn_readlane((int)ia, 63);
+      const uint32_t ib = tot_a + wave_incl_scan(hb);
       // from = the least row count whose tiles and all longer ones fit in cus
       const unsigned long long fa = __ballot(lane < kSpan && ia <= x.cus);
       const unsigned long long fb = __ballot(lane + 64u < kSpan && ib <= x.cus);
@@ -928,11 +938,11 @@ __device__ void expand_tables(const SegBrief* brief, uint32_t n, const ExpandArg
       if (fb) {
         const uint32_t k = 63u - (uint32_t)__clzll(fb);  // the highest lane: the fewest rows
         from = kRows - 64u - k;
-        fit = __shfl(ib, k, 64);
+        fit = (uint32_t)__builtin_amdgcn_readlane((int)ib, (int)k);
       } else if (fa) {
         const uint32_t k = 63u - (uint32_t)__clzll(fa);
         from = kRows - k;
-        fit = __shfl(ia, k, 64);
+        fit = (uint32_t)__builtin_amdgcn_readlane((int)ia, (int)k);
       }
       left = x.cus - fit;
       if (left) {
@@ -1055,8 +1065,8 @@ __device__ void expand_tables(const SegBrief* brief, uint32_t n, const ExpandArg
     const bool has_b = kRows > 64 + (int)lane;
     const uint32_t ca = cursor[ka] + (ka == (uint32_t)kRows ? n_full : 0u) + (ka == piece ? n_pieces : 0u);
     const uint32_t cb = has_b ? cursor[kb] + (kb == piece ? n_pieces : 0u) : 0u;
-    const uint32_t ia = wave_incl_scan(ca, lane), tot_a = __shfl(ia, 63, 64);
-    const uint32_t ib = tot_a + wave_incl_scan(cb, lane);
+    const uint32_t ia = wave_incl_scan(ca), tot_a = (uint32_t)__builtin_amdgcn_readlane((int)ia, 63);
+    const uint32_t ib = tot_a + wave_incl_scan(cb);
     // the atomics of a length start after its slots taken in thread order
     cursor[ka] = ia - ca + (ka == (uint32_t)kRows ? n_full : 0u) + (ka == piece ? n_pieces : 0u);
     if (has_b) cursor[kb] = ib - cb + (kb == piece ? n_pieces : 0u);
