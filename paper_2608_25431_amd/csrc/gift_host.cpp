@@ -145,7 +145,9 @@ int device_cus(int dev) {
   if (cus[dev] == 0) {
     int v = 0;
     if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0) v = 256;
-    cus[dev] = v;
+    // the expansion sums tile rows in 32 bits, exactly while fewer tiles
+    // than CUs hold fewer than 2^20 rows: at most 8191 CUs
+    cus[dev] = v < 4096 ? v : 4096;
   }
   return cus[dev];
 }
