@@ -797,8 +797,11 @@ gift_status run_gcm(const gift_tensor* t, const gift_segment_table* st, gift_key
       }
       e = launch_gcm_small(a, OPEN, stream);
       if (e == hipSuccess) e = launch_gcm_finalize(a, OPEN, stream);
-      // open: segments that failed are zeroed after their verdicts are known
-      if (e == hipSuccess && OPEN)
+      // open: segments that failed are zeroed after their verdicts are known;
+      // without a finalize pass every verdict came from a kernel that zeroed
+      // its own failed segments (the small-segment kernel, or the tile kernel
+      // for an uncut one-tile segment)
+      if (e == hipSuccess && OPEN && Q.finalize)
         e = launch_zero_failed(d_desc, n, a.tile_base, P.n_tiles, verdicts, nullptr, (uint8_t*)out, 0u, cus * 4u,
                                stream);
       if (e != hipSuccess) {

@@ -323,6 +323,7 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
   constexpr bool OPEN = (MODE & kModeOpen) != 0;
   constexpr bool GATHER = (MODE & kModeGather) != 0, SCATTER = (MODE & kModeScatter) != 0;
   __shared__ __attribute__((aligned(16))) uint8_t smem[kLdsBytes];
+  __shared__ uint32_t tile_failed;  // open: the tag of the tile's one-tile segment did not match
   const uint32_t tid = threadIdx.x;
   uint8_t* tt = smem + kLdsAes;
   const uint8_t* gt = smem + kLdsGtab;
@@ -578,11 +579,28 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
             uint32_t diff = 0;
             for (int j = 0; j < 4; j++) diff |= tin[j] ^ tag.w[j];
             a.verdicts[s] = diff ? kVerdictAuthFail : kVerdictOk;
+            tile_failed = diff != 0u;
           }
         }
       } else if (one && !OPEN && lane == 0) {
         uint32_t* to = (uint32_t*)(a.tags_out + 16ull * s);  // rejected: zero tag
         for (int j = 0; j < 4; j++) to[j] = 0u;
+      }
+    }
+    // open of a contiguous tensor: a one-tile segment whose tag failed
+    // releases zeros only.  Its tile is the whole segment, so the workgroup
+    // zeroes it here (multi-tile and cut segments are zeroed by a later pass
+    // once the finalize pass has their verdicts).
+    if (OPEN && !GATHER && !SCATTER && one && fold) {
+      __syncthreads();  // tile_failed is written
+      if (tile_failed) {
+        for (int r = r_lo; r < r1; r++) {
+          const int64_t i0 = base + (int64_t)r * kThreads + tid_e;
+          if (i0 >= 0) {
+            const uint64_t rem = len - 16ull * (uint64_t)i0;
+            store_block(a.out + off + 16ull * (uint64_t)i0, u128_zero(), rem >= 16 ? 16u : (uint32_t)rem, aligned);
+          }
+        }
       }
     }
   }

@@ -368,6 +368,56 @@ def test_one_tile_segments_cut_at_the_queue_tail(kt3):
     assert host(back).tobytes() == exp_back.tobytes()
 
 
+def test_one_tile_open_tamper_without_finalize(kt3):
+    # At least one tile per CU, none longer than a 32-row piece: no tile is
+    # cut, every segment is an uncut one-tile segment, and the call has no
+    # finalize pass (the launch plan says so).  Open with ciphertext bits
+    # flipped in three segments and tag bits in three others: the tile
+    # kernel zeroes each failed tile itself (no later zeroing pass runs).
+    # Whole-block rows and rows with a ragged, unaligned last block; every
+    # byte and verdict equals the oracle's open of the tampered copy.
+    import ctypes
+    import subprocess
+    keys, nb, kt = kt3
+    lib = gift.lib()
+    out = subprocess.run(["nm", "-D", "--defined-only", gift.LIB_PATH], capture_output=True, text=True).stdout
+    names = [l.split()[-1] for l in out.splitlines() if l.strip()]
+
+    class QueuePlan(ctypes.Structure):
+        _fields_ = [("cap", ctypes.c_uint64), ("grid", ctypes.c_uint32), ("finalize", ctypes.c_bool)]
+    plan = getattr(lib, next(n for n in names if n.startswith("_ZN4gift10plan_queue")))
+    plan.argtypes = [ctypes.c_uint32, ctypes.c_uint64, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint32]
+    plan.restype = QueuePlan
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    r = np.random.default_rng(31)
+    for rb in (16384, 16408):
+        seg_rows = [int(x) for x in r.integers(1, 5, cus + 44)]
+        table, row = [], 0
+        for k, nr in enumerate(seg_rows):
+            row += int(r.integers(0, 2))  # gap rows
+            table.append((row, nr, k % 3, 7000 + k))
+            row += nr
+        n_rows, n = row, len(table)
+        tile_rows = [-(-(-(-nr * rb // 16)) // 1024) for nr in seg_rows]
+        assert not plan(n, sum(tile_rows), 0, max(tile_rows), cus).finalize
+        data = r.integers(0, 256, n_rows * rb, dtype=np.uint8)
+        st, ct_np, tg_np, _ = oracle.seal(data, n_rows, rb, table, keys, nb)
+        assert st == 0
+        ct_np, tg_np = ct_np.copy().reshape(-1), tg_np.copy().reshape(-1)
+        picks = [int(x) for x in r.choice(n, 6, replace=False)]
+        for i in picks[:3]:
+            b, nr, _, _ = table[i]
+            ct_np[b * rb + int(r.integers(0, nr * rb))] ^= np.uint8(1 << int(r.integers(0, 8)))
+        for i in picks[3:]:
+            tg_np[16 * i + int(r.integers(0, 16))] ^= np.uint8(1 << int(r.integers(0, 8)))
+        st, o_back, o_ver = oracle.open_(ct_np, n_rows, rb, table, keys, nb, tg_np)
+        assert st == 0
+        assert sorted(i for i in range(n) if o_ver[i] != gift.SEG_OK) == sorted(picks)
+        back, ver = open_(dev_u8(ct_np), n_rows, rb, table, kt, nb, dev_u8(tg_np))
+        assert host(ver)[:n].tolist() == o_ver.tolist(), rb
+        assert host(back).tobytes() == o_back.tobytes(), rb
+
+
 def test_in_place_rejection_and_tamper(kt3):
     # out == data with the owner check fused: a rejected segment is zeroed in
     # place and every other byte is sealed in place, for each kind of
