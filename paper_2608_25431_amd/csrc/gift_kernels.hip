@@ -1268,12 +1268,18 @@ __global__ __launch_bounds__(kTokenChunk) void k_tokens(const SegDesc* __restric
   }
   __syncthreads();
   for (uint32_t b = blockIdx.x; b < n_chunks; b += gridDim.x) {
-    // the segment of chunk b: chunk_base[lo] <= b < chunk_base[hi] throughout
+    // The segment of chunk b, chunk_base[lo] <= b < chunk_base[hi] throughout,
+    // by a 64-way search: lane l tests split point lo + l * step; chunk_base
+    // increases (every segment has a chunk), so the lanes that pass form a
+    // prefix, lane 0 always among them, and the last of them bounds the next
+    // interval.  Two rounds of loads for 4,096 segments instead of twelve.
     uint32_t lo = 0, hi = n_segs;
     while (hi - lo > 1u) {
-      const uint32_t mid = lo + (hi - lo) / 2u;
-      if (chunk_base[mid] <= b) lo = mid;
-      else hi = mid;
+      const uint32_t step = (hi - lo + 63u) / 64u;
+      const uint32_t p = lo + threadIdx.x * step;
+      const unsigned long long pass = __ballot(p < hi && chunk_base[p] <= b);
+      lo += (63u - (uint32_t)__clzll(pass)) * step;
+      hi = min(hi, lo + step);
     }
     const uint32_t s = lo;
     const uint64_t rb = segs[s].row_begin, rc = segs[s].row_count;

@@ -933,6 +933,16 @@ def test_token_encryption_matches_oracle():
     # of row order, gaps between segments
     token_case(w.keys, kt, [(300, 65, 4, 0), (0, 64, 2, 0), (64, 63, 3, 0), (130, 1, 5, 0), (131, 128, 6, 0),
                             (500, 200, 2, 1)], big[:800], W.u64s(2, "chunk_non", 800), eos)
+    # segment counts around the 64-way chunk search's steps (one, two and three
+    # rounds), segments of 1-130 tokens (one to three chunks each)
+    r = np.random.default_rng(64)
+    for n_seg in (63, 64, 65, 4097):
+        rows = r.integers(1, 131, n_seg)
+        starts = np.concatenate([[0], np.cumsum(rows)[:-1]])
+        segs = [(int(b), int(c), int(u), 0) for b, c, u in zip(starts, rows, r.integers(0, 1024, n_seg))]
+        n_tok = int(rows.sum())
+        token_case(w.keys, kt, segs, W.u64s(3, "search_tok", n_tok) % np.uint64(128256),
+                   W.u64s(3, "search_non", n_tok), eos)
     # validation agrees with the oracle
     dt, dn = dev_u64(tok[:8]), dev_u64(non[:8])
     out = torch.zeros(128, dtype=torch.uint8, device=DEV)
