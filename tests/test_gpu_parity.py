@@ -374,8 +374,9 @@ def test_one_tile_open_tamper_without_finalize(kt3):
     # finalize pass (the launch plan says so).  Open with ciphertext bits
     # flipped in three segments and tag bits in three others: the tile
     # kernel zeroes each failed tile itself (no later zeroing pass runs).
-    # Whole-block rows and rows with a ragged, unaligned last block; every
-    # byte and verdict equals the oracle's open of the tampered copy.
+    # Whole-block rows and rows with a ragged, unaligned last block, out of
+    # place and in place; every byte and verdict equals the oracle's open of
+    # the tampered copy.
     import ctypes
     import subprocess
     keys, nb, kt = kt3
@@ -416,6 +417,11 @@ def test_one_tile_open_tamper_without_finalize(kt3):
         back, ver = open_(dev_u8(ct_np), n_rows, rb, table, kt, nb, dev_u8(tg_np))
         assert host(ver)[:n].tolist() == o_ver.tolist(), rb
         assert host(back).tobytes() == o_back.tobytes(), rb
+        # in place: the failed tiles are zeroed over their own ciphertext
+        buf = dev_u8(ct_np)
+        back, ver = open_(buf, n_rows, rb, table, kt, nb, dev_u8(tg_np), out=buf)
+        assert host(ver)[:n].tolist() == o_ver.tolist(), rb
+        assert host(buf).tobytes() == o_back.tobytes(), rb
 
 
 def test_in_place_rejection_and_tamper(kt3):
