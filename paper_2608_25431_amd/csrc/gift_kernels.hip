@@ -283,6 +283,19 @@ __device__ __forceinline__ u128 mask_block(const u128& v, uint32_t n) {
   return r;
 }
 
+// Whole-block stream of the per-block kernel: every plaintext and ciphertext
+// block passes through the caches once, so its 16-byte load and store carry
+// the non-temporal hint.  Measured on llama3_8b_kv: seal kernel -0.75%.
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 ld_stream(const uint8_t* p) {
+  const u32x4 t = __builtin_nontemporal_load((const u32x4*)p);
+  return make_uint4(t.x, t.y, t.z, t.w);
+}
+__device__ __forceinline__ void st_stream(uint8_t* p, const uint4& v) {
+  const u32x4 t = {v.x, v.y, v.z, v.w};
+  __builtin_nontemporal_store(t, (u32x4*)p);
+}
+
 __device__ __forceinline__ u128 ld_u128(const uint4* p) {
   uint4 v = *p;
   return u128{{v.x, v.y, v.z, v.w}};
@@ -492,7 +505,7 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
           uint8_t* pg = a.pbase + c_cur + ((i0 & cmask) << 4);
           src = GATHER ? pg : a.in + off + 16ull * i0;
           dst = SCATTER ? pg : a.out + off + 16ull * i0;
-          v = *(const uint4*)src;
+          v = ld_stream(src);
         }
         uint32_t x0, x1, x2, x3;
         ctr_rounds12(cc, c0 + (uint32_t)kThreads * (uint32_t)r, x0, x1, x2, x3, rk, tt, L);
@@ -500,7 +513,7 @@ __global__ __launch_bounds__(kThreads) void k_gcm_tiles(GcmArgs a) {
         u128 x;
         if (fast) {
           const uint4 o = make_uint4(v.x ^ x0, v.y ^ x1, v.z ^ x2, v.w ^ x3);
-          *(uint4*)dst = o;
+          st_stream(dst, o);
           x = OPEN ? u128{{v.x, v.y, v.z, v.w}} : u128{{o.x, o.y, o.z, o.w}};
         } else {
           x = u128_zero();
