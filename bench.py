@@ -248,6 +248,31 @@ def lds_probe(cus):
             "clock_mhz": round(min(mhz), 1)}
 
 
+def lds_ceiling(probe, cus, clock_hz=2.4e9):
+    """Sealed GB/s the seal kernel's LDS reads allow: per 16-byte block 197
+    four-byte T-table reads (at the probe's lane-reads per CU-clock) and 32
+    sixteen-byte GHASH reads (at its bytes per CU-clock), on cus CUs at
+    clock_hz.  Also returns the CU-clocks per block."""
+    cycles = 197 / probe["b32_lane_reads_per_clk"] + 32 * 16 / probe["b128_bytes_per_clk"]
+    return 16 * cus * clock_hz / cycles / 1e9, cycles
+
+
+def valu_ceiling(valu, mix, probe, cus, clock_hz=2.4e9):
+    """Sealed GB/s the seal kernel's VALU instructions allow: valu lane-ops
+    per block, of which mix names the v_perm_b32 and v_bitop3_b32 ones, each
+    at the lane-op rate its probe measured, the rest at 64 per CU-clock (4
+    SIMDs x 16 lanes); without a probe or a mix all at 64.  Also returns the
+    effective lane-ops per CU-clock."""
+    if probe and mix:
+        n_perm, n_bitop3 = mix["v_perm_b32"], mix["v_bitop3_b32"]
+        clk = (n_perm / probe["valu_perm_lane_ops_per_clk"] + n_bitop3 / probe["valu_bitop3_lane_ops_per_clk"]
+               + (valu - n_perm - n_bitop3) / 64.0)
+        lane_ops = valu / clk
+    else:
+        lane_ops = 64.0
+    return 16 * cus * lane_ops * clock_hz / valu / 1e9, lane_ops
+
+
 def hbm_copy(torch, nbytes=4 << 30, reps=5):
     """The practical HBM ceiling beside the 8 TB/s peak: a plain
     device-to-device copy (torch's copy kernel) of nbytes, read and write
@@ -606,11 +631,10 @@ def main():
     # rates the LDS probes measure in this run.
     probe = lds_probe(torch.cuda.get_device_properties(0).multi_processor_count)
     if probe:
-        lds_cycles = 197 / probe["b32_lane_reads_per_clk"] + 32 * 16 / probe["b128_bytes_per_clk"]
         cus = torch.cuda.get_device_properties(0).multi_processor_count
         kernel_sealed = tiled / (k_ms * 1e-3) / 1e9
-        at_peak = 16 * cus * 2.4e9 / lds_cycles / 1e9  # sealed GB/s at the 2.4 GHz peak clock
-        at_clock = 16 * cus * probe["clock_mhz"] * 1e6 / lds_cycles / 1e9
+        at_peak, lds_cycles = lds_ceiling(probe, cus)  # sealed GB/s at the 2.4 GHz peak clock
+        at_clock, _ = lds_ceiling(probe, cus, probe["clock_mhz"] * 1e6)
         res["lds_roofline"] = {
             "bound": "lds", "kernel": "k_gcm_tiles<seal>", "achieved": round(kernel_sealed, 2),
             "peak": round(at_peak, 1), "unit": "GB/s sealed", "frac": round(kernel_sealed / at_peak, 4),
@@ -630,14 +654,7 @@ def main():
     mix = profiled_traffic(w.name, "valu_mix_per_block") if labels is not None else None
     if valu:
         cus_v = torch.cuda.get_device_properties(0).multi_processor_count
-        if probe and mix:
-            n_perm, n_bitop3 = mix["v_perm_b32"], mix["v_bitop3_b32"]
-            clk_valu = (n_perm / probe["valu_perm_lane_ops_per_clk"]
-                        + n_bitop3 / probe["valu_bitop3_lane_ops_per_clk"] + (valu - n_perm - n_bitop3) / 64.0)
-            lane_ops = valu / clk_valu
-        else:
-            lane_ops = 64.0
-        v_peak = 16 * cus_v * lane_ops * 2.4e9 / valu / 1e9
+        v_peak, lane_ops = valu_ceiling(valu, mix, probe, cus_v)
         k_sealed = tiled / (k_ms * 1e-3) / 1e9
         res["valu_roofline"] = {"bound": "valu", "kernel": "k_gcm_tiles<seal>", "achieved": round(k_sealed, 2),
                                 "peak": round(v_peak, 1), "unit": "GB/s sealed", "frac": round(k_sealed / v_peak, 4),
